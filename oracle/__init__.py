@@ -1,0 +1,159 @@
+"""CPU oracle of the tail-aware serving simulation (ctypes binding).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, by the smoke check and by the
+benchmark's CPU-baseline leg. The product package never imports it, and it
+imports nothing from the product package except the seeded input records
+(``paper_2606_18431_amd.workloads``, which holds no scheduling arithmetic).
+
+The C source (``tas_oracle.c``) is plain and sequential; see its header for the
+paper passages it follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "tas_oracle.c")
+LIB = os.path.join(HERE, "libtas_oracle.so")
+LEVELS = 24
+EINVAL, EINFEASIBLE, EOVERFLOW, ELIVELOCK, ESTATE = -1, -2, -5, -6, -7
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (-O2, plain C11, pthreads)."""
+    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        tmp = LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-D_GNU_SOURCE", "-fPIC", "-shared",
+                               "-Wall", "-Wextra", "-o", tmp, SRC, "-lm", "-lpthread"])
+        os.replace(tmp, LIB)
+    return LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            build()
+        L = ctypes.CDLL(LIB)
+        P = ctypes.c_void_p
+        i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+        L.tas_oracle_boost_table.argtypes = [f64, i32, f64, P]
+        L.tas_oracle_boost_table.restype = ctypes.c_int
+        L.tas_oracle_run.argtypes = [i32, i32, P, P, P, i32, P, P, P, P, P, P, P, i64,
+                                     P, P, P, P, P, P, i32]
+        L.tas_oracle_run.restype = ctypes.c_int
+        L.tas_oracle_log.argtypes = [i32, P, P, P, i32, i32, i32, i64, P, P, i64, P, P, P, P,
+                                     P, i64, P, i64, P, i64, P, P, P]
+        L.tas_oracle_log.restype = ctypes.c_int
+        L.tas_oracle_percentile.argtypes = [P, i32, i32]
+        L.tas_oracle_percentile.restype = ctypes.c_uint32
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def boost_table(gamma: float, k: int, tau_us: float = 5000.0) -> np.ndarray:
+    out = np.zeros(LEVELS, np.int64)
+    rc = lib().tas_oracle_boost_table(float(gamma), int(k), float(tau_us), _p(out))
+    if rc:
+        raise ValueError(f"boost table rejected (gamma={gamma}, k={k}, tau={tau_us})")
+    return out
+
+
+def tables(settings: np.ndarray, tau_us: float) -> np.ndarray:
+    """The oracle's own boost tables for a settings array: an explicit table
+    where one is given, else the table of gamma; zeros for FCFS/SRPT."""
+    out = np.zeros((len(settings), LEVELS), np.int64)
+    for i, s in enumerate(settings):
+        if int(s["policy"]) != 2:
+            continue
+        if int(s["table_given"]):
+            out[i] = s["boost_us"]
+        else:
+            out[i] = boost_table(float(s["gamma"]), int(s["k"]), tau_us)
+    return out
+
+
+def _eng(engine) -> np.ndarray:
+    return np.array([engine.max_seqs, engine.max_tokens, engine.chunk, engine.kv_blocks,
+                     engine.block_tokens, engine.iter_base_us, engine.iter_tok_us,
+                     engine.iter_ctx_div], np.int32)
+
+
+def run(w, n_threads: int | None = None, max_iters: int | None = None):
+    """Simulate every instance of workload ``w``. Returns a dict of host arrays:
+    ttft/ttlt/tbtmax [n_inst, n_req] uint32, counters [n_inst, 8] int64,
+    pct [n_inst, 3, 3] uint32, status [n_inst] int32, rc."""
+    s = w.settings
+    n_inst, n_req = len(s), w.n_req
+    arr = np.ascontiguousarray(w.arrival_us, np.int64)
+    pr = np.ascontiguousarray(w.prompt, np.int32)
+    de = np.ascontiguousarray(w.decode, np.int32)
+    tr = np.ascontiguousarray(s["trace"], np.int32)
+    po = np.ascontiguousarray(s["policy"], np.int32)
+    kk = np.ascontiguousarray(s["k"], np.int32)
+    mg = np.ascontiguousarray(s["memguard"], np.int32)
+    dl = np.ascontiguousarray(s["delta_us"], np.int64)
+    tb = np.ascontiguousarray(tables(s, w.engine.tau_us))
+    out = dict(
+        ttft=np.zeros((n_inst, n_req), np.uint32),
+        ttlt=np.zeros((n_inst, n_req), np.uint32),
+        tbtmax=np.zeros((n_inst, n_req), np.uint32),
+        counters=np.zeros((n_inst, 8), np.int64),
+        pct=np.zeros((n_inst, 3, 3), np.uint32),
+        status=np.zeros(n_inst, np.int32),
+    )
+    mi = w.engine.max_iters if max_iters is None else max_iters
+    nt = n_threads or os.cpu_count() or 1
+    rc = lib().tas_oracle_run(w.n_traces, n_req, _p(arr), _p(pr), _p(de), n_inst, _p(tr),
+                              _p(po), _p(kk), _p(mg), _p(dl), _p(tb), _p(_eng(w.engine)),
+                              int(mi), _p(out["ttft"]), _p(out["ttlt"]), _p(out["tbtmax"]),
+                              _p(out["counters"]), _p(out["pct"]), _p(out["status"]), int(nt))
+    out["rc"] = rc
+    return out
+
+
+def log(arrival, prompt, decode, engine, policy, k=1, memguard=0, delta_us=0, table=None,
+        gamma=None, max_iters=None, cap_iter=1 << 20, cap_batch=1 << 22, cap_evict=1 << 20):
+    """Run one instance and return its schedule log (see tas_oracle.h)."""
+    arrival = np.ascontiguousarray(arrival, np.int64)
+    prompt = np.ascontiguousarray(prompt, np.int32)
+    decode = np.ascontiguousarray(decode, np.int32)
+    n = len(arrival)
+    if table is None:
+        table = (boost_table(gamma, k, engine.tau_us) if gamma is not None
+                 else np.zeros(LEVELS, np.int64))
+    table = np.ascontiguousarray(table, np.int64)
+    o = dict(ttft=np.zeros(n, np.uint32), ttlt=np.zeros(n, np.uint32),
+             tbtmax=np.zeros(n, np.uint32), counters=np.zeros(8, np.int64))
+    it = np.zeros((cap_iter, 6), np.int64)
+    bt = np.zeros((cap_batch, 2), np.int32)
+    ev = np.zeros((cap_evict, 3), np.int64)
+    ni, nb, ne = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    mi = engine.max_iters if max_iters is None else max_iters
+    rc = lib().tas_oracle_log(n, _p(arrival), _p(prompt), _p(decode), policy, k, memguard,
+                              int(delta_us), _p(table), _p(_eng(engine)), int(mi),
+                              _p(o["ttft"]), _p(o["ttlt"]), _p(o["tbtmax"]), _p(o["counters"]),
+                              _p(it), cap_iter, _p(bt), cap_batch, _p(ev), cap_evict,
+                              ctypes.byref(ni), ctypes.byref(nb), ctypes.byref(ne))
+    o["rc"] = rc
+    o["iters"] = it[: ni.value].copy()
+    o["batch"] = bt[: nb.value].copy()
+    o["evict"] = ev[: ne.value].copy()
+    return o
+
+
+def percentile(values: np.ndarray, q: int) -> int:
+    v = np.ascontiguousarray(values, np.uint32)
+    return int(lib().tas_oracle_percentile(_p(v), len(v), int(q)))

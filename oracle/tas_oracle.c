@@ -1,0 +1,481 @@
+/*
+ * tas_oracle.c - plain, sequential CPU oracle of the serving simulation.
+ *
+ * TEST INFRASTRUCTURE ONLY (see tas_oracle.h). It is written for a reader who
+ * checks it against the paper by eye: one request array, one candidate list
+ * re-ranked from scratch every iteration, linear victim searches, no
+ * incremental structures beyond keeping the previous order as the start of an
+ * insertion sort (which sorts any input; the previous order only makes it fast).
+ *
+ * Paper passages followed (arXiv 2606.18431):
+ *   Formulation / Notation          request (a_i, s_pre, s_dec); T_i = C_i - a_i
+ *   Eq. boost_function              b_gamma(w) = (1/gamma) ln(1/(1-exp(-gamma w)))
+ *   Phase 2 (UniBoost-Base)         Phi(i,t) = a_i - b(max(w_i, s_pre)), argmin
+ *   Phase 2 preemption protocol     hysteresis: preempt only if better by delta
+ *   Phase 3 (MemGuard), Eq. memguard_level  w_hat = k 2^floor(log2(max(w,k)/k)),
+ *                                   dispatched => non-evictable until the next
+ *                                   threshold
+ *   Algorithm 1                     per iteration: keys for every active
+ *                                   request, greedy batch fill under M and the
+ *                                   KV capacity, victim selection + swap-out,
+ *                                   ExecuteOneStep, UpdateStats
+ *   Phase 4                         t_p = inf{t : Fbar(t) <= (100-p)/100}
+ *
+ * Where the paper is silent, the readings are (each is listed, with its
+ * reason, in the design notes of the repository):
+ *   - signal w = P + dec (prompt plus emitted tokens; monotone in both phases)
+ *   - boost in microseconds: table[level] = round(tau * b_gamma(k 2^level))
+ *   - ExecuteOneStep: dt = base + tok * sum(n) + floor(sum(kv + n) / div)
+ *   - swap-out = recompute preemption: KV dropped, emitted tokens kept, the
+ *     request re-prefills P + dec tokens when readmitted
+ *   - victim = worst (key, idx) resident not already in this batch; voluntary
+ *     victims must be evictable (MemGuard) and worse than the candidate by
+ *     delta; when none exists a resident candidate forces out the worst other
+ *     resident, or itself; a waiting candidate that does not fit closes
+ *     admissions for the rest of the iteration
+ *   - the iteration that completes the prefill emits the first token; times
+ *     are iteration ends; arrivals join at the next iteration start
+ *   - SRPT key = remaining computed tokens P + D - 1 - kv; FCFS key = a_i
+ */
+#include "tas_oracle.h"
+
+#include <math.h>
+#include <pthread.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { PENDING = 0, WAITING = 1, RESIDENT = 2, DONE = 3 };
+enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2 };
+
+typedef struct {
+    int32_t N;
+    const int64_t *a;
+    const int32_t *P, *D;
+    int32_t policy, k, memguard;
+    int64_t delta;
+    const int64_t *bt;
+    int32_t M, T, c, Kb, bs, base, tok, div;
+    int64_t max_iters;
+} inst_t;
+
+typedef struct {
+    int8_t st;
+    int8_t in_batch;
+    int32_t kv;    /* tokens whose KV is resident */
+    int32_t dec;   /* tokens emitted so far */
+    int32_t guard; /* MemGuard level at the latest dispatch */
+    int64_t key;   /* priority key, frozen at iteration start */
+    int64_t t_first, t_last, tbt_max;
+    int64_t evicted_at; /* iteration in which it was last evicted, or -1 */
+} req_t;
+
+typedef struct {
+    int64_t *it;
+    int64_t it_cap, n_it;
+    int32_t *b;
+    int64_t b_cap, n_b;
+    int64_t *ev;
+    int64_t ev_cap, n_ev;
+    int full;
+} log_t;
+
+/* ------------------------------------------------------------ boost table */
+
+/* ln(1 - exp(-x)) for x > 0, evaluated accurately on both sides of ln 2
+ * (Maechler 2012, "Accurately computing log(1 - exp(-|a|))"). */
+static double log1mexp(double x) {
+    return x <= 0.6931471805599453 ? log(-expm1(-x)) : log1p(-exp(-x));
+}
+
+int tas_oracle_boost_table(double gamma, int32_t k, double tau_us, int64_t *out) {
+    if (!(gamma > 0.0) || k < 1 || !(tau_us > 0.0)) return TOR_EINVAL;
+    const double cap = 4398046511104.0; /* 2^42 */
+    for (int j = 0; j < TOR_LEVELS; j++) {
+        double w = (double)k * ldexp(1.0, j); /* quantized signal k * 2^j */
+        double b = -log1mexp(gamma * w) / gamma; /* b_gamma(w), tokens */
+        double us = tau_us * b;
+        out[j] = us >= cap ? (int64_t)cap : (int64_t)llround(us);
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------ helpers */
+
+static int64_t blocks(int64_t tokens, int32_t bs) { return (tokens + bs - 1) / bs; }
+
+/* MemGuard level: floor(log2(max(w,k)/k)), capped at the table's last entry.
+ * floor(log2(x)) of the real ratio equals that of floor(x) because every
+ * threshold 2^j is an integer. */
+static int32_t level_of(int64_t w, int32_t k) {
+    int64_t q = (w > k ? w : k) / k;
+    int32_t L = 0;
+    while (q >= 2) {
+        q >>= 1;
+        L++;
+    }
+    return L < TOR_LEVELS - 1 ? L : TOR_LEVELS - 1;
+}
+
+static int64_t key_of(const inst_t *I, int32_t r, const req_t *q) {
+    switch (I->policy) {
+    case P_FCFS:
+        return I->a[r];
+    case P_SRPT:
+        return (int64_t)I->P[r] + I->D[r] - 1 - q->kv;
+    default:
+        return I->a[r] - I->bt[level_of((int64_t)I->P[r] + q->dec, I->k)];
+    }
+}
+
+/* (ka, ia) > (kb, ib) in lexicographic order */
+static int lex_gt(int64_t ka, int32_t ia, int64_t kb, int32_t ib) {
+    return ka > kb || (ka == kb && ia > ib);
+}
+
+static void evict(req_t *q, int64_t *U, int32_t bs, int64_t iter) {
+    *U -= blocks(q->kv, bs);
+    q->kv = 0;
+    q->st = WAITING;
+    q->evicted_at = iter;
+}
+
+/* ------------------------------------------------------------ one instance */
+
+static int simulate(const inst_t *I, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
+                    int64_t *cnt, log_t *lg) {
+    const int32_t N = I->N;
+    for (int32_t i = 0; i < N; i++) {
+        if (I->P[i] < 1 || I->D[i] < 1 || I->a[i] < 0 || (i && I->a[i] < I->a[i - 1]))
+            return TOR_EINVAL;
+        if (blocks((int64_t)I->P[i] + I->D[i] - 1, I->bs) > I->Kb) return TOR_EINFEASIBLE;
+    }
+    req_t *R = (req_t *)calloc((size_t)N, sizeof *R);
+    int32_t *act = (int32_t *)malloc(sizeof(int32_t) * (size_t)N);
+    int32_t *bidx = (int32_t *)malloc(sizeof(int32_t) * (size_t)I->M);
+    int32_t *bn = (int32_t *)malloc(sizeof(int32_t) * (size_t)I->M);
+    int status = 0;
+    if (!R || !act || !bidx || !bn) {
+        status = TOR_EINVAL;
+        goto out;
+    }
+    for (int32_t i = 0; i < N; i++) R[i].evicted_at = -1;
+
+    int64_t t = 0, U = 0, iters = 0, reqiters = 0, tokens = 0, ev_vol = 0, ev_forced = 0;
+    int64_t maxU = 0, idle = 0;
+    int32_t next = 0, nact = 0;
+
+    for (;;) {
+        /* O2 arrivals: a_i <= t joins the waiting set (idx order). */
+        while (next < N && I->a[next] <= t) {
+            R[next].st = WAITING;
+            act[nact++] = next++;
+        }
+        /* O3 idle server: jump to the next arrival. */
+        if (nact == 0) {
+            if (next == N) break;
+            idle += I->a[next] - t;
+            t = I->a[next];
+            continue;
+        }
+        /* O4/O5 keys of every active request, then rank by (key, idx). */
+        for (int32_t j = 0; j < nact; j++) R[act[j]].key = key_of(I, act[j], &R[act[j]]);
+        for (int32_t j = 1; j < nact; j++) {
+            int32_t x = act[j];
+            int64_t kx = R[x].key;
+            int32_t m = j;
+            while (m > 0 && lex_gt(R[act[m - 1]].key, act[m - 1], kx, x)) {
+                act[m] = act[m - 1];
+                m--;
+            }
+            act[m] = x;
+        }
+
+        /* O6 greedy batch formation in priority order. */
+        int32_t nb = 0, closed = 0;
+        int64_t used = 0;
+        for (int32_t j = 0; j < nact; j++) {
+            if (nb == I->M || used == I->T) break;
+            int32_t r = act[j];
+            req_t *q = &R[r];
+            if (q->evicted_at == iters) continue;
+            if (q->st == WAITING && closed) continue;
+            int64_t need = (int64_t)I->P[r] + q->dec - q->kv;
+            int64_t n = need;
+            if (n > I->c) n = I->c;
+            if (n > I->T - used) n = I->T - used;
+            int64_t dU = blocks(q->kv + n, I->bs) - blocks(q->kv, I->bs);
+            for (;;) {
+                if (U + dU <= I->Kb) {
+                    if (q->st == WAITING) { /* dispatch */
+                        q->st = RESIDENT;
+                        q->guard = level_of((int64_t)I->P[r] + q->dec, I->k);
+                    }
+                    q->in_batch = 1;
+                    bidx[nb] = r;
+                    bn[nb] = (int32_t)n;
+                    nb++;
+                    used += n;
+                    U += dU;
+                    break;
+                }
+                /* voluntary victim: worst eligible resident outside the batch */
+                int32_t v = -1;
+                for (int32_t m = 0; m < nact; m++) {
+                    int32_t x = act[m];
+                    const req_t *p = &R[x];
+                    if (x == r || p->st != RESIDENT || p->in_batch) continue;
+                    if (I->memguard &&
+                        !(level_of((int64_t)I->P[x] + p->dec, I->k) > p->guard))
+                        continue;
+                    if (!lex_gt(p->key - I->delta, x, q->key, r)) continue;
+                    if (v < 0 || lex_gt(p->key, x, R[v].key, v)) v = x;
+                }
+                if (v >= 0) {
+                    evict(&R[v], &U, I->bs, iters);
+                    ev_vol++;
+                    if (lg && lg->n_ev < lg->ev_cap) {
+                        int64_t *e = lg->ev + 3 * lg->n_ev++;
+                        e[0] = iters, e[1] = v, e[2] = 0;
+                    } else if (lg)
+                        lg->full = 1;
+                    continue;
+                }
+                if (q->st == RESIDENT) {
+                    /* forced: worst other resident outside the batch, else r */
+                    for (int32_t m = 0; m < nact; m++) {
+                        int32_t x = act[m];
+                        const req_t *p = &R[x];
+                        if (x == r || p->st != RESIDENT || p->in_batch) continue;
+                        if (v < 0 || lex_gt(p->key, x, R[v].key, v)) v = x;
+                    }
+                    int self = v < 0;
+                    if (self) v = r;
+                    evict(&R[v], &U, I->bs, iters);
+                    ev_forced++;
+                    if (lg && lg->n_ev < lg->ev_cap) {
+                        int64_t *e = lg->ev + 3 * lg->n_ev++;
+                        e[0] = iters, e[1] = v, e[2] = 1;
+                    } else if (lg)
+                        lg->full = 1;
+                    if (self) break;
+                    continue;
+                }
+                closed = 1; /* a waiting request that does not fit */
+                break;
+            }
+        }
+        /* O7 */
+        if (nb == 0) {
+            status = TOR_ESTATE;
+            goto out;
+        }
+        if (U > maxU) maxU = U;
+
+        /* O8 cost of the step. */
+        int64_t sum_n = 0, sum_ctx = 0;
+        for (int32_t b = 0; b < nb; b++) {
+            sum_n += bn[b];
+            sum_ctx += (int64_t)R[bidx[b]].kv + bn[b];
+        }
+        int64_t dt = I->base + (int64_t)I->tok * sum_n + sum_ctx / I->div;
+        int64_t t_end = t + dt;
+        if (lg) {
+            if (lg->n_it < lg->it_cap) {
+                int32_t nw = 0, nr = 0;
+                for (int32_t m = 0; m < nact; m++) {
+                    nw += R[act[m]].st == WAITING;
+                    nr += R[act[m]].st == RESIDENT;
+                }
+                int64_t *e = lg->it + 6 * lg->n_it++;
+                e[0] = t, e[1] = dt, e[2] = nb, e[3] = U, e[4] = nw, e[5] = nr;
+            } else
+                lg->full = 1;
+            for (int32_t b = 0; b < nb; b++) {
+                if (lg->n_b < lg->b_cap) {
+                    lg->b[2 * lg->n_b] = bidx[b];
+                    lg->b[2 * lg->n_b + 1] = bn[b];
+                    lg->n_b++;
+                } else
+                    lg->full = 1;
+            }
+        }
+
+        /* O9 execute: advance KV, emit tokens, record latencies, complete. */
+        for (int32_t b = 0; b < nb; b++) {
+            int32_t r = bidx[b];
+            req_t *q = &R[r];
+            q->in_batch = 0;
+            q->kv += bn[b];
+            if (q->kv == I->P[r] + q->dec) {
+                q->dec++;
+                if (q->dec == 1)
+                    q->t_first = t_end;
+                else if (t_end - q->t_last > q->tbt_max)
+                    q->tbt_max = t_end - q->t_last;
+                q->t_last = t_end;
+                if (q->dec == I->D[r]) {
+                    q->st = DONE;
+                    U -= blocks(q->kv, I->bs);
+                    q->kv = 0;
+                }
+            }
+        }
+
+        /* O10 advance the clock and the counters. */
+        t = t_end;
+        iters++;
+        reqiters += nb;
+        tokens += sum_n;
+        if (iters > I->max_iters) {
+            status = TOR_ELIVELOCK;
+            goto out;
+        }
+        int32_t w = 0;
+        for (int32_t j = 0; j < nact; j++)
+            if (R[act[j]].st != DONE) act[w++] = act[j];
+        nact = w;
+    }
+
+    /* O11 per-request outputs, relative to arrival. */
+    for (int32_t i = 0; i < N; i++) {
+        int64_t f = R[i].t_first - I->a[i], l = R[i].t_last - I->a[i], g = R[i].tbt_max;
+        if (f > 0xFFFFFFFFll || l > 0xFFFFFFFFll || g > 0xFFFFFFFFll) {
+            status = TOR_EOVERFLOW;
+            goto out;
+        }
+        ttft[i] = (uint32_t)f;
+        ttlt[i] = (uint32_t)l;
+        tbtmax[i] = (uint32_t)g;
+    }
+    cnt[0] = iters, cnt[1] = reqiters, cnt[2] = tokens, cnt[3] = ev_vol;
+    cnt[4] = ev_forced, cnt[5] = t, cnt[6] = maxU, cnt[7] = idle;
+out:
+    free(R);
+    free(act);
+    free(bidx);
+    free(bn);
+    return status;
+}
+
+/* ------------------------------------------------------------ percentiles */
+
+static int cmp_u32(const void *x, const void *y) {
+    uint32_t a = *(const uint32_t *)x, b = *(const uint32_t *)y;
+    return (a > b) - (a < b);
+}
+
+uint32_t tas_oracle_percentile(const uint32_t *v, int32_t n, int32_t q) {
+    if (n <= 0) return 0;
+    uint32_t *s = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)n);
+    memcpy(s, v, sizeof(uint32_t) * (size_t)n);
+    qsort(s, (size_t)n, sizeof(uint32_t), cmp_u32);
+    int64_t rank = ((int64_t)q * n + 99) / 100; /* ceil(q n / 100) */
+    if (rank < 1) rank = 1;
+    uint32_t out = s[rank - 1];
+    free(s);
+    return out;
+}
+
+/* ------------------------------------------------------------ driver */
+
+typedef struct {
+    int32_t n_req, n_inst;
+    const int64_t *arrival;
+    const int32_t *prompt, *decode;
+    const int32_t *trace, *policy, *k, *memguard;
+    const int64_t *delta, *table;
+    const int32_t *eng;
+    int64_t max_iters;
+    uint32_t *ttft, *ttlt, *tbtmax, *pct;
+    int64_t *counters;
+    int32_t *status;
+    int32_t next; /* work counter */
+} job_t;
+
+static void fill_inst(inst_t *I, const int32_t *eng, int32_t n_req, const int64_t *a,
+                      const int32_t *P, const int32_t *D, int32_t policy, int32_t k,
+                      int32_t memguard, int64_t delta, const int64_t *bt, int64_t max_iters) {
+    I->N = n_req, I->a = a, I->P = P, I->D = D;
+    I->policy = policy, I->k = k, I->memguard = memguard, I->delta = delta, I->bt = bt;
+    I->M = eng[0], I->T = eng[1], I->c = eng[2], I->Kb = eng[3], I->bs = eng[4];
+    I->base = eng[5], I->tok = eng[6], I->div = eng[7];
+    I->max_iters = max_iters;
+}
+
+static void run_one(job_t *J, int32_t i) {
+    int32_t tr = J->trace[i];
+    size_t off = (size_t)tr * (size_t)J->n_req;
+    inst_t I;
+    fill_inst(&I, J->eng, J->n_req, J->arrival + off, J->prompt + off, J->decode + off,
+              J->policy[i], J->k[i], J->memguard[i], J->delta[i], J->table + (size_t)i * 24,
+              J->max_iters);
+    size_t o = (size_t)i * (size_t)J->n_req;
+    int st = simulate(&I, J->ttft + o, J->ttlt + o, J->tbtmax + o, J->counters + (size_t)i * 8,
+                      NULL);
+    J->status[i] = st;
+    if (st == 0) {
+        const uint32_t *m[3] = {J->ttft + o, J->ttlt + o, J->tbtmax + o};
+        const int32_t qs[3] = {50, 90, 99};
+        for (int a = 0; a < 3; a++)
+            for (int b = 0; b < 3; b++)
+                J->pct[(size_t)i * 9 + a * 3 + b] = tas_oracle_percentile(m[a], J->n_req, qs[b]);
+    }
+}
+
+static void *worker(void *arg) {
+    job_t *J = (job_t *)arg;
+    for (;;) {
+        int32_t i = __atomic_fetch_add(&J->next, 1, __ATOMIC_RELAXED);
+        if (i >= J->n_inst) break;
+        run_one(J, i);
+    }
+    return NULL;
+}
+
+int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
+                   const int32_t *prompt, const int32_t *decode, int32_t n_inst,
+                   const int32_t *trace, const int32_t *policy, const int32_t *k,
+                   const int32_t *memguard, const int64_t *delta, const int64_t *table,
+                   const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
+                   uint32_t *tbtmax, int64_t *counters, uint32_t *pct, int32_t *status,
+                   int32_t n_threads) {
+    if (n_traces < 1 || n_req < 1 || n_inst < 0) return TOR_EINVAL;
+    for (int32_t i = 0; i < n_inst; i++)
+        if (trace[i] < 0 || trace[i] >= n_traces || policy[i] < 0 || policy[i] > 2 || k[i] < 1)
+            return TOR_EINVAL;
+    if (eng[0] < 1 || eng[1] < 1 || eng[2] < 1 || eng[2] > eng[1] || eng[3] < 1 || eng[4] < 1 ||
+        eng[5] < 1 || eng[6] < 0 || eng[7] < 1)
+        return TOR_EINVAL;
+    job_t J = {n_req, n_inst, arrival, prompt, decode, trace, policy, k, memguard, delta, table,
+               eng, max_iters, ttft, ttlt, tbtmax, pct, counters, status, 0};
+    if (n_threads < 1) n_threads = 1;
+    if (n_threads > n_inst) n_threads = n_inst > 0 ? n_inst : 1;
+    pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)n_threads);
+    int started = 0;
+    for (int32_t w = 1; w < n_threads; w++)
+        if (pthread_create(&th[w], NULL, worker, &J) == 0) started++;
+        else break;
+    worker(&J);
+    for (int32_t w = 1; w <= started; w++) pthread_join(th[w], NULL);
+    free(th);
+    for (int32_t i = 0; i < n_inst; i++)
+        if (status[i]) return status[i];
+    return 0;
+}
+
+int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
+                   const int32_t *decode, int32_t policy, int32_t k, int32_t memguard,
+                   int64_t delta, const int64_t *table, const int32_t *eng,
+                   int64_t max_iters, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
+                   int64_t *counters, int64_t *log_iter, int64_t iter_cap,
+                   int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
+                   int64_t evict_cap, int64_t *n_iter, int64_t *n_batch, int64_t *n_evict) {
+    inst_t I;
+    fill_inst(&I, eng, n_req, arrival, prompt, decode, policy, k, memguard, delta, table,
+              max_iters);
+    log_t lg = {log_iter, iter_cap, 0, log_batch, batch_cap, 0, log_evict, evict_cap, 0, 0};
+    int st = simulate(&I, ttft, ttlt, tbtmax, counters, &lg);
+    *n_iter = lg.n_it, *n_batch = lg.n_b, *n_evict = lg.n_ev;
+    if (lg.full) return TOR_EINVAL;
+    return st;
+}

@@ -1,0 +1,312 @@
+"""Seeded synthetic serving workloads: request traces and policy-setting grids.
+
+This module only draws inputs. It holds none of the scheduling arithmetic: no
+priorities, no boost curve, no batch formation. Both the HIP path and the CPU
+oracle consume exactly the arrays produced here.
+
+Request model (paper, section "Formulation", Notation): request i is the tuple
+(a_i arrival time, s_pre prompt length known at arrival, s_dec decode length
+not revealed to a blind policy). Traces are stored structure-of-arrays,
+trace-major, arrival-sorted: ``arrival_us[t, i]`` (int64 microseconds,
+non-decreasing in i), ``prompt[t, i]`` and ``decode[t, i]`` (int32 tokens, >= 1).
+
+Five workloads are defined (``make(cfg)``):
+
+0  tiny: 1 trace x 8 settings, 1,000 requests, Poisson 4 req/s, seed 0.
+1  chat-heavy sweep: 64 traces x 64 settings, 10,000 requests, utilisation 0.85.
+2  reasoning-heavy under KV pressure: 64 x 64, 10,000 requests, 8,192 KV blocks.
+3  bursty arrivals + decode-length shift: 128 x 32, 20,000 requests, 2-state MMPP.
+4  large sweep: 256 x 64, 50,000 requests, 60/40 blend of the 1 and 2 laws.
+
+The policy-parameter grid per trace: setting 0 = FCFS, setting 1 = oracle-length
+SRPT, then pairs (UniBoost with MemGuard, vanilla boost) over log-spaced gamma.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+
+FCFS, SRPT, BOOST = 0, 1, 2
+POLICY_NAMES = {FCFS: "fcfs", SRPT: "srpt", BOOST: "boost"}
+LEVELS = 24
+
+# One numpy record per instance; field order mirrors the C struct tas_setting.
+SETTING_DTYPE = np.dtype(
+    [
+        ("trace", np.int32),
+        ("policy", np.int32),
+        ("k", np.int32),
+        ("memguard", np.int32),
+        ("delta_us", np.int64),
+        ("gamma", np.float64),
+        ("table_given", np.int32),
+        ("pad", np.int32),
+        ("boost_us", np.int64, (LEVELS,)),
+    ]
+)
+
+
+@dataclasses.dataclass
+class Engine:
+    """Serving-engine limits and the integer iteration cost model.
+
+    Iteration time in microseconds = base + tok * sum(n) + floor(sum(ctx) / div).
+    """
+
+    max_seqs: int = 64
+    max_tokens: int = 8192
+    chunk: int = 1024
+    kv_blocks: int = 16384
+    block_tokens: int = 16
+    iter_base_us: int = 5000
+    iter_tok_us: int = 2
+    iter_ctx_div: int = 100
+    max_iters: int = 1 << 40
+    tau_us: float = 5000.0  # microseconds per token of boost (one decode step)
+
+
+@dataclasses.dataclass
+class Workload:
+    name: str
+    arrival_us: np.ndarray  # int64 [n_traces, n_req]
+    prompt: np.ndarray  # int32 [n_traces, n_req]
+    decode: np.ndarray  # int32 [n_traces, n_req]
+    engine: Engine
+    settings: np.ndarray  # SETTING_DTYPE [n_inst]
+    meta: dict = dataclasses.field(default_factory=dict)
+
+    @property
+    def n_traces(self) -> int:
+        return int(self.arrival_us.shape[0])
+
+    @property
+    def n_req(self) -> int:
+        return int(self.arrival_us.shape[1])
+
+    @property
+    def n_inst(self) -> int:
+        return int(self.settings.shape[0])
+
+    def subset(self, inst_ids) -> "Workload":
+        """The same traces with only the chosen instances (order kept)."""
+        inst_ids = np.asarray(inst_ids, dtype=np.int64)
+        return dataclasses.replace(self, settings=self.settings[inst_ids].copy())
+
+
+# ---------------------------------------------------------------- settings
+
+
+def setting(trace, policy, k=1, memguard=0, delta_us=0, gamma=0.0, table=None):
+    s = np.zeros((), dtype=SETTING_DTYPE)
+    s["trace"], s["policy"], s["k"], s["memguard"] = trace, policy, k, memguard
+    s["delta_us"], s["gamma"] = delta_us, gamma
+    if table is not None:
+        t = np.asarray(table, dtype=np.int64)
+        s["boost_us"][: len(t)] = t
+        s["boost_us"][len(t):] = t[-1] if len(t) else 0
+        s["table_given"] = 1
+    return s
+
+
+UNIBOOST = dict(k=256, memguard=1, delta_us=100_000)  # defaults k=256, delta=0.1 s
+VANILLA = dict(k=1, memguard=0, delta_us=0)
+
+
+def settings_grid(n_traces: int, n_settings: int) -> np.ndarray:
+    """Per trace: FCFS, SRPT, then (UniBoost, vanilla) pairs over a gamma grid
+    log-spaced on [1e-5, 1e-1] per token. Instance id = trace * S + s."""
+    assert n_settings >= 4 and n_settings % 2 == 0
+    g = (n_settings - 2) // 2
+    gammas = 10.0 ** np.linspace(-5.0, -1.0, g)
+    out = np.zeros(n_traces * n_settings, dtype=SETTING_DTYPE)
+    for t in range(n_traces):
+        for s in range(n_settings):
+            if s == 0:
+                rec = setting(t, FCFS)
+            elif s == 1:
+                rec = setting(t, SRPT)
+            else:
+                var = VANILLA if (s - 2) % 2 else UNIBOOST
+                rec = setting(t, BOOST, gamma=float(gammas[(s - 2) // 2]), **var)
+            out[t * n_settings + s] = rec
+    return out
+
+
+# ---------------------------------------------------------------- lengths
+
+
+def _lognormal(rng, n, median, sigma, lo, hi):
+    z = rng.standard_normal(n)
+    return np.clip(np.rint(np.exp(math.log(median) + sigma * z)), lo, hi).astype(np.int32)
+
+
+def _pareto(rng, n, alpha, xm, lo, hi):
+    u = 1.0 - rng.random(n)  # (0, 1]
+    return np.clip(np.rint(xm * u ** (-1.0 / alpha)), lo, hi).astype(np.int32)
+
+
+def _decode_reasoning(rng, n):
+    """80% lognormal(median 150, sigma 1) + 20% Pareto(alpha 1.5, min 2000), clip 32768."""
+    heavy = rng.random(n) < 0.2
+    ln = _lognormal(rng, n, 150, 1.0, 1, 32768)
+    pa = _pareto(rng, n, 1.5, 2000, 1, 32768)
+    return np.where(heavy, pa, ln).astype(np.int32)
+
+
+# ---------------------------------------------------------------- load calibration
+
+
+def offered_cost_us(prompt, decode, eng: Engine):
+    """Expected busy microseconds each request adds, for arrival-rate calibration.
+
+    Every iteration a request takes part in costs base/M_eff (its share of the
+    fixed cost), plus tok per computed token, plus ctx/div per token of context.
+    M_eff is the concurrency the KV budget allows. Calibration only: it sets the
+    Poisson rate and never enters the simulation.
+    """
+    p = prompt.astype(np.float64)
+    d = decode.astype(np.float64)
+    c = float(eng.chunk)
+    nch = np.ceil(p / c)
+    mean_ctx = np.mean((p + d / 2.0) * d) / np.mean(d)
+    m_eff = min(float(eng.max_seqs), eng.kv_blocks * eng.block_tokens / mean_ctx)
+    prefill_ctx = c * (nch - 1.0) * nch / 2.0 + p
+    decode_ctx = (d - 1.0) * p + (d - 1.0) * d / 2.0
+    return (
+        (nch + d - 1.0) * eng.iter_base_us / m_eff
+        + eng.iter_tok_us * (p + d - 1.0)
+        + (prefill_ctx + decode_ctx) / eng.iter_ctx_div
+    )
+
+
+def _poisson_arrivals(rng, n, lam_per_us):
+    gaps = rng.exponential(1.0 / lam_per_us, n)
+    return np.floor(np.cumsum(gaps)).astype(np.int64)
+
+
+def _mmpp_arrivals(rng, n, lam0, lam1, dwell_us):
+    """2-state Markov-modulated Poisson arrivals; start state drawn from the
+    stationary law (equal mean dwell => 1/2 each)."""
+    state = int(rng.random() < 0.5)
+    t = 0.0
+    out = []
+    count = 0
+    while count < n:
+        d = rng.exponential(dwell_us)
+        lam = lam1 if state else lam0
+        expect = lam * d
+        m = int(expect + 6.0 * math.sqrt(expect + 1.0) + 8)
+        while True:
+            gaps = rng.exponential(1.0 / lam, m)
+            cs = np.cumsum(gaps)
+            if cs[-1] > d:
+                break
+            m *= 2
+        inside = t + cs[cs <= d]
+        out.append(inside)
+        count += inside.size
+        t += d
+        state ^= 1
+    arr = np.concatenate(out)[:n]
+    return np.floor(arr).astype(np.int64)
+
+
+# ---------------------------------------------------------------- configs
+
+
+def _engine(cfg: int) -> Engine:
+    if cfg == 0:
+        return Engine(kv_blocks=16384)
+    if cfg == 1:
+        return Engine(kv_blocks=32768)
+    if cfg == 2:
+        return Engine(kv_blocks=8192)
+    if cfg == 3:
+        return Engine(kv_blocks=16384)
+    if cfg == 4:
+        return Engine(max_seqs=256, max_tokens=16384, kv_blocks=32768)
+    raise ValueError(cfg)
+
+
+SHAPES = {0: (1, 8, 1000), 1: (64, 64, 10000), 2: (64, 64, 10000), 3: (128, 32, 20000),
+          4: (256, 64, 50000)}
+NAMES = {0: "tiny", 1: "chat-heavy", 2: "reasoning-kv-pressure", 3: "bursty-shift",
+         4: "large-sweep"}
+
+
+def _trace(cfg: int, trace: int, n: int, eng: Engine):
+    rng = np.random.default_rng(0 if cfg == 0 else [cfg, trace])
+    if cfg == 0:
+        p = _lognormal(rng, n, 512, 1.0, 16, 4096)
+        d = _lognormal(rng, n, 200, 1.2, 1, 8192)
+        arr = _poisson_arrivals(rng, n, 4.0e-6)
+        return arr, p, d
+    if cfg == 1:
+        p = _lognormal(rng, n, 768, 1.0, 16, 4096)
+        d = _lognormal(rng, n, 180, 1.0, 1, 4096)
+        rho = 0.85
+    elif cfg == 2:
+        p = _lognormal(rng, n, 256, 1.0, 16, 4096)
+        d = _decode_reasoning(rng, n)
+        rho = 0.9
+    elif cfg == 3:
+        p = _lognormal(rng, n, 512, 1.0, 16, 4096)
+        half = n // 2
+        d = np.concatenate([_lognormal(rng, half, 150, 1.2, 1, 8192),
+                            _lognormal(rng, n - half, 900, 1.2, 1, 8192)])
+        post = slice(half, n)
+        lam_avg = 0.8 * (n - half) / offered_cost_us(p[post], d[post], eng).sum()
+        lam_b = lam_avg / 3.5  # time-average rate of {1x, 6x} with equal dwell
+        arr = _mmpp_arrivals(rng, n, lam_b, 6.0 * lam_b, 30.0e6)
+        return arr, p, d
+    elif cfg == 4:
+        chat = rng.random(n) < 0.6
+        p = np.where(chat, _lognormal(rng, n, 768, 1.0, 16, 4096),
+                     _lognormal(rng, n, 256, 1.0, 16, 4096)).astype(np.int32)
+        d = np.where(chat, _lognormal(rng, n, 180, 1.0, 1, 4096),
+                     _decode_reasoning(rng, n)).astype(np.int32)
+        rho = 0.95
+    else:
+        raise ValueError(cfg)
+    lam = rho * n / offered_cost_us(p, d, eng).sum()
+    arr = _poisson_arrivals(rng, n, lam)
+    return arr, p, d
+
+
+def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
+         n_req: int | None = None) -> Workload:
+    """Build workload ``cfg``. The optional overrides shrink it (fewer traces,
+    settings or requests) for tests; traces keep their seeds, so trace t of a
+    shrunk workload equals trace t of the full one when n_req is unchanged."""
+    T0, S0, N0 = SHAPES[cfg]
+    T = T0 if n_traces is None else n_traces
+    S = S0 if n_settings is None else n_settings
+    N = N0 if n_req is None else n_req
+    eng = _engine(cfg)
+    arr = np.empty((T, N), np.int64)
+    pr = np.empty((T, N), np.int32)
+    de = np.empty((T, N), np.int32)
+    for t in range(T):
+        arr[t], pr[t], de[t] = _trace(cfg, t, N, eng)
+    if cfg == 0 and S == 8:
+        st = [setting(0, FCFS), setting(0, SRPT)]
+        st += [setting(0, BOOST, gamma=g, **UNIBOOST)
+               for g in (1e-4, 3e-4, 1e-3, 3e-3, 1e-2, 3e-2)]
+        sets = np.stack(st * T)
+        sets["trace"] = np.repeat(np.arange(T), 8)
+    else:
+        sets = settings_grid(T, S)
+    return Workload(NAMES[cfg], arr, pr, de, eng, sets,
+                    meta=dict(cfg=cfg, n_traces=T, n_settings=S, n_req=N))
+
+
+def small_random(seed: int, n_req: int, *, rate_per_s: float = 20.0, p_med=64, d_med=20,
+                 p_max=512, d_max=256):
+    """A small random trace (for tests): lognormal lengths, Poisson arrivals."""
+    rng = np.random.default_rng([99, seed])
+    p = _lognormal(rng, n_req, p_med, 1.0, 1, p_max)
+    d = _lognormal(rng, n_req, d_med, 1.0, 1, d_max)
+    arr = _poisson_arrivals(rng, n_req, rate_per_s * 1e-6)
+    return arr, p, d
