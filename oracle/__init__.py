@@ -52,6 +52,8 @@ def lib():
         L.tas_oracle_log.argtypes = [i32, P, P, P, i32, i32, i32, i64, P, P, i64, P, P, P, P,
                                      P, i64, P, i64, P, i64, P, P, P]
         L.tas_oracle_log.restype = ctypes.c_int
+        L.tas_oracle_level.argtypes = [i64, i32]
+        L.tas_oracle_level.restype = ctypes.c_int32
         L.tas_oracle_percentile.argtypes = [P, i32, i32]
         L.tas_oracle_percentile.restype = ctypes.c_uint32
         _lib = L
@@ -152,6 +154,10 @@ def log(arrival, prompt, decode, engine, policy, k=1, memguard=0, delta_us=0, ta
     o["batch"] = bt[: nb.value].copy()
     o["evict"] = ev[: ne.value].copy()
     return o
+
+
+def level(w: int, k: int) -> int:
+    return int(lib().tas_oracle_level(int(w), int(k)))
 
 
 def percentile(values: np.ndarray, q: int) -> int:

@@ -116,6 +116,8 @@ static int32_t level_of(int64_t w, int32_t k) {
     return L < TOR_LEVELS - 1 ? L : TOR_LEVELS - 1;
 }
 
+int32_t tas_oracle_level(int64_t w, int32_t k) { return level_of(w, k); }
+
 static int64_t key_of(const inst_t *I, int32_t r, const req_t *q) {
     switch (I->policy) {
     case P_FCFS:

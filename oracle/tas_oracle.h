@@ -72,6 +72,10 @@ int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
                    int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
                    int64_t evict_cap, int64_t *n_iter, int64_t *n_batch, int64_t *n_evict);
 
+/* MemGuard level of signal w at granularity k: floor(log2(max(w,k)/k)),
+ * capped at 23 (paper, Eq. memguard_level). */
+int32_t tas_oracle_level(int64_t w, int32_t k);
+
 /* Nearest-rank percentile of n values: the value at sorted position
  * ceil(q*n/100) - 1. */
 uint32_t tas_oracle_percentile(const uint32_t *v, int32_t n, int32_t q);

@@ -1,0 +1,211 @@
+"""Invariants of the serving simulation, checked on the oracle's schedule log.
+
+The replay below rebuilds every request's KV, emitted tokens and timestamps
+from the logged batches and evictions alone, re-derives each iteration's
+duration from the cost model, and checks the result against the oracle's
+outputs and the rules: KV capacity, batch limits, work conservation, token
+conservation, completion exactly once, FCFS dispatch order, the MemGuard
+eligibility of every voluntary eviction and the Phase 3 revision bound.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_18431_amd import workloads as W
+
+
+def blocks(x, bs):
+    return -(-x // bs)
+
+
+def replay(a, p, d, e, o, policy, k=1, memguard=0):
+    N = len(a)
+    bs = e.block_tokens
+    kv = np.zeros(N, np.int64)
+    dec = np.zeros(N, np.int64)
+    guard = np.full(N, -1, np.int64)
+    t_first = np.full(N, -1, np.int64)
+    t_last = np.full(N, -1, np.int64)
+    tbt = np.zeros(N, np.int64)
+    done = np.zeros(N, bool)
+    first_dispatch = []
+    evicted_kv_total = 0
+    vol_per_req = np.zeros(N, np.int64)
+    ev = o["evict"]
+    ev_ptr = 0
+    row = 0
+    t_expect = 0
+    idle = 0
+    for i, (t0, dt, nb, U, nw, nr) in enumerate(o["iters"]):
+        # I3: the clock only jumps over idle time
+        if t0 != t_expect:
+            assert t0 > t_expect
+            active = [r for r in range(N) if a[r] <= t_expect and not done[r]]
+            assert not active, "clock jumped while requests were active"
+            assert t0 == min(a[r] for r in range(N) if not done[r] and a[r] > t_expect)
+            idle += t0 - t_expect
+        resident_before = {r for r in range(N) if kv[r] > 0}
+        # evictions of this iteration
+        evicted = set()
+        while ev_ptr < len(ev) and ev[ev_ptr][0] == i:
+            _, v, forced = ev[ev_ptr]
+            ev_ptr += 1
+            assert kv[v] > 0 and not done[v]
+            if not forced:
+                vol_per_req[v] += 1
+                if memguard:  # I9: MemGuard eligibility
+                    assert oracle.level(int(p[v] + dec[v]), k) > guard[v]
+            evicted_kv_total += kv[v]
+            kv[v] = 0
+            evicted.add(v)
+        batch = o["batch"][row:row + nb]
+        row += nb
+        # I2 batch limits
+        assert 1 <= nb <= e.max_seqs
+        ns = batch[:, 1].astype(np.int64)
+        assert np.all(ns >= 1) and np.all(ns <= e.chunk) and ns.sum() <= e.max_tokens
+        members = batch[:, 0].tolist()
+        assert len(set(members)) == nb
+        assert not (set(members) & evicted)
+        for r in members:
+            assert a[r] <= t0 and not done[r]
+            assert kv[r] < p[r] + dec[r]
+            if kv[r] == 0:
+                guard[r] = oracle.level(int(p[r] + dec[r]), k)
+                if r not in first_dispatch:
+                    first_dispatch.append(r)
+        # no request may wait while the batch still has room (stop rule), except
+        # evicted ones and waiting ones after a failed admission: residents
+        # outside the batch must have been evicted this iteration
+        if nb < e.max_seqs and ns.sum() < e.max_tokens:
+            for r in resident_before:
+                assert r in members or r in evicted
+        # cost model and I1
+        ctx = sum(int(kv[r] + n) for r, n in zip(members, ns))
+        assert dt == e.iter_base_us + e.iter_tok_us * int(ns.sum()) + ctx // e.iter_ctx_div
+        for r, n in zip(members, ns):
+            kv[r] += n
+        u_now = sum(blocks(int(kv[r]), bs) for r in range(N) if kv[r] > 0)
+        assert U == u_now and 0 <= U <= e.kv_blocks
+        t_end = t0 + dt
+        for r, n in zip(members, ns):
+            assert kv[r] <= p[r] + dec[r]
+            if kv[r] == p[r] + dec[r]:
+                dec[r] += 1
+                if dec[r] == 1:
+                    t_first[r] = t_end
+                else:
+                    tbt[r] = max(tbt[r], t_end - t_last[r])
+                t_last[r] = t_end
+                if dec[r] == d[r]:
+                    done[r] = True
+                    kv[r] = 0
+        t_expect = t_end
+    assert ev_ptr == len(ev) and row == len(o["batch"])
+    # I4 completion exactly once; outputs
+    assert np.all(done) and np.array_equal(dec, d.astype(np.int64))
+    assert np.array_equal(o["ttft"].astype(np.int64), t_first - a)
+    assert np.array_equal(o["ttlt"].astype(np.int64), t_last - a)
+    assert np.array_equal(o["tbtmax"].astype(np.int64), tbt)
+    c = o["counters"]
+    assert c[0] == len(o["iters"])  # iterations
+    assert c[1] == int(o["iters"][:, 2].sum())  # I10 request-iterations
+    # I6 token conservation
+    assert c[2] == int((p.astype(np.int64) + d - 1).sum()) + evicted_kv_total
+    assert c[3] + c[4] == len(ev)
+    assert c[5] == t_expect and c[5] == int(o["iters"][:, 1].sum()) + idle  # I3
+    assert c[6] == int(o["iters"][:, 3].max())
+    assert c[7] == idle
+    # I5 decode gaps are at least one base step each
+    assert np.all(o["ttlt"].astype(np.int64) - o["ttft"] >= (d.astype(np.int64) - 1) * e.iter_base_us)
+    if policy == 0:  # I7 FCFS dispatches in arrival order
+        assert first_dispatch == sorted(first_dispatch)
+    if memguard:  # Phase 3 revision bound per request
+        for r in range(N):
+            bound = 1 + math.floor(math.log2(max(int(p[r] + d[r]), k) / k))
+            assert vol_per_req[r] <= bound
+    return dict(first_dispatch=first_dispatch, vol=vol_per_req)
+
+
+ENGINES = [
+    W.Engine(max_seqs=8, kv_blocks=96, chunk=128, max_tokens=512),
+    W.Engine(max_seqs=4, kv_blocks=48, chunk=64, max_tokens=96),
+    W.Engine(max_seqs=16, kv_blocks=400, chunk=256, max_tokens=1024),
+]
+POLICIES = [
+    dict(policy=0),
+    dict(policy=1),
+    dict(policy=2, k=16, memguard=1, delta_us=20000, gamma=1e-3),
+    dict(policy=2, k=1, memguard=0, delta_us=0, gamma=1e-3),
+    dict(policy=2, k=32, memguard=1, delta_us=0, gamma=3e-2),
+]
+
+
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("ei", range(len(ENGINES)))
+@pytest.mark.parametrize("pi", range(len(POLICIES)))
+def test_replay_invariants(seed, ei, pi):
+    e = ENGINES[ei]
+    pol = POLICIES[pi]
+    a, p, d = W.small_random(seed * 10 + ei, 160, rate_per_s=60.0, p_max=400, d_max=200)
+    o = oracle.log(a, p, d, e, pol["policy"], k=pol.get("k", 1), memguard=pol.get("memguard", 0),
+                   delta_us=pol.get("delta_us", 0), gamma=pol.get("gamma"))
+    assert o["rc"] == 0
+    replay(a, p, d, e, o, pol["policy"], k=pol.get("k", 1), memguard=pol.get("memguard", 0))
+
+
+def test_replay_sees_evictions():
+    """The invariant suite must exercise the eviction paths."""
+    e = ENGINES[1]
+    a, p, d = W.small_random(3, 160, rate_per_s=60.0, p_max=400, d_max=200)
+    o = oracle.log(a, p, d, e, 0)
+    assert o["counters"][3] > 0 and o["counters"][4] > 0
+
+
+def test_alone_is_a_lower_bound():
+    """I8: nobody finishes sooner than it would alone."""
+    e = ENGINES[0]
+    a, p, d = W.small_random(11, 120, rate_per_s=60.0, p_max=400, d_max=200)
+    o = oracle.log(a, p, d, e, 2, k=16, memguard=1, delta_us=20000, gamma=1e-3)
+    for r in range(len(a)):
+        alone = oracle.log([0], [p[r]], [d[r]], e, 0)
+        assert o["ttlt"][r] >= alone["ttlt"][0]
+
+
+def test_run_matches_log_and_percentiles():
+    """The multi-instance driver and the single-instance log agree, and the
+    reported percentiles are nearest-rank over the latencies."""
+    w = W.make(1, n_traces=2, n_settings=6, n_req=400)
+    out = oracle.run(w, n_threads=4)
+    assert out["rc"] == 0
+    for i, s in enumerate(w.settings):
+        t = int(s["trace"])
+        tb = oracle.tables(w.settings[i:i + 1], w.engine.tau_us)[0]
+        o = oracle.log(w.arrival_us[t], w.prompt[t], w.decode[t], w.engine, int(s["policy"]),
+                       k=int(s["k"]), memguard=int(s["memguard"]), delta_us=int(s["delta_us"]),
+                       table=tb)
+        for key in ("ttft", "ttlt", "tbtmax"):
+            assert np.array_equal(out[key][i], o[key])
+        assert np.array_equal(out["counters"][i], o["counters"])
+        for m, key in enumerate(("ttft", "ttlt", "tbtmax")):
+            for qi, q in enumerate((50, 90, 99)):
+                ref = np.quantile(o[key].astype(np.float64), q / 100, method="inverted_cdf")
+                assert out["pct"][i, m, qi] == int(ref)
+
+
+def test_error_paths():
+    e = W.Engine(kv_blocks=4)
+    # infeasible: one request needs more KV than exists
+    o = oracle.log([0], [100], [1], e, 0)
+    assert o["rc"] == oracle.EINFEASIBLE
+    # livelock guard
+    o = oracle.log([0, 0], [16, 16], [50, 50], W.Engine(), 0, max_iters=10)
+    assert o["rc"] == oracle.ELIVELOCK
+    # overflow: a latency beyond 2^32-1 us
+    o = oracle.log([0], [1], [900_000], W.Engine(kv_blocks=1 << 20), 0)
+    assert o["rc"] == oracle.EOVERFLOW
+    # unsorted arrivals
+    o = oracle.log([10, 5], [16, 16], [2, 2], W.Engine(), 0)
+    assert o["rc"] == oracle.EINVAL
