@@ -1,0 +1,175 @@
+"""Benchmark: simulated request-iterations per second on one MI355X.
+
+One step = one pass of the whole path over one synthetic sweep: the
+simulation kernel over every (trace, policy setting) instance, then the
+percentile kernel. Inputs (traces, settings) are resident in HBM before the
+timed region. Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 4]
+
+Roofline: the simulation kernel is counted against HBM bandwidth with
+algorithmic bytes of 32 B per request-iteration (read + write of the request's
+kv / emitted / last-token / max-gap state) plus 28 B per request-instance
+(16 B of trace in, 12 B of latencies out). `traffic` comes from the committed
+rocprofv3 counter summary when it was taken on the current kernel sources.
+The CPU baseline is the oracle, timed on the host cores over one trace's
+settings (a bounded sample of the same sweep).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+BYTES_PER_REQITER = 32
+BYTES_PER_REQINST = 28
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "sim_kernel_counters.json")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("tas_sim.hip", "tas_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2606_18431_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed counter summary, if it matches
+    the current kernel source and workload; else None."""
+    try:
+        d = json.load(open(COUNTERS_FILE))
+    except (OSError, ValueError):
+        return None
+    if d.get("source_hash") != kernel_source_hash() or d.get("workload") != workload:
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, n_threads: int):
+    import oracle
+
+    oracle.build()
+    t0 = int(w.settings["trace"][0])
+    sel = np.nonzero(w.settings["trace"] == t0)[0]
+    sub = w.subset(sel)
+    tic = time.perf_counter()
+    o = oracle.run(sub, n_threads=n_threads)
+    dt = time.perf_counter() - tic
+    reqit = int(o["counters"][:, 1].sum())
+    return o, sel, dict(value=reqit / dt, unit="request-iterations/s", cores=n_threads,
+                        kind="oracle", seconds=round(dt, 3),
+                        sample=f"trace {t0}, all {len(sel)} settings ({len(sel)} of {w.n_inst} "
+                               f"instances, {reqit} request-iterations)")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=4, choices=[0, 1, 2, 3, 4])
+    ap.add_argument("--traces", type=int, default=None, help="shrink the sweep (testing)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
+    ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this path runs on one GPU; --gpus {args.gpus} is not supported "
+              "(instances are independent; see the multi-GPU note in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2606_18431_amd import tas
+    from paper_2606_18431_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = W.make(args.workload, n_traces=args.traces)
+    name = f"{W.NAMES[args.workload]}: {w.n_traces} traces x {w.meta['n_settings']} settings x " \
+           f"{w.n_req} requests"
+    print(f"[bench] building {name}", file=sys.stderr, flush=True)
+    sim = tas.Simulation(w, device=dev)
+    stream = torch.cuda.current_stream()
+
+    for i in range(args.warmup):
+        sim.step(stream)
+        torch.cuda.synchronize()
+        print(f"[bench] warmup {i} done", file=sys.stderr, flush=True)
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    tic = time.perf_counter()
+    for e0, e1, e2 in ev:
+        e0.record(stream)
+        sim.run(stream)
+        e1.record(stream)
+        sim.percentiles(stream)
+        e2.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - tic
+    sim_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))
+    pct_ms = float(np.mean([b.elapsed_time(c) for _, b, c in ev]))
+    step_ms = float(np.mean([a.elapsed_time(c) for a, _, c in ev]))
+    out = sim.results(latencies=False)
+    if out["rc"] != 0:
+        print(f"[bench] device error {out['rc']}: {tas.tas_strerror(out['rc'])}", file=sys.stderr)
+        sys.exit(1)
+    reqiters = int(out["counters"][:, 1].sum())
+    iters = int(out["counters"][:, 0].sum())
+    n_reqinst = w.n_inst * w.n_req
+    value = reqiters / (step_ms / 1e3)
+    alg_bytes = BYTES_PER_REQITER * reqiters + BYTES_PER_REQINST * n_reqinst
+    achieved = alg_bytes / (sim_ms / 1e3) / 1e9
+    traffic = measured_traffic(name)
+
+    res = {
+        "metric": "simulated request-iterations/sec (1 GPU)",
+        "value": value,
+        "unit": "request-iterations/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic (seeded traces; no datasets)",
+        "config": {"workload": name, "instances": w.n_inst, "requests_per_instance": w.n_req,
+                   "max_seqs": w.engine.max_seqs, "max_tokens": w.engine.max_tokens,
+                   "kv_blocks": w.engine.kv_blocks, "request_iterations": reqiters,
+                   "iterations": iters, "sim_kernel_ms": sim_ms, "pctl_kernel_ms": pct_ms,
+                   "wall_s": wall, "lds_list_cap": tas.tas_list_cap(sim.ctx)},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
+                     "kernel": "sim_kernel",
+                     "algorithmic_bytes_per_launch": alg_bytes},
+    }
+    sim.close()
+    if not args.no_cpu:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        o, sel, cb = cpu_baseline(w, args.cpu_threads)
+        res["cpu_baseline"] = cb
+        # the same sample, checked against the GPU results of the timed run
+        sim2 = tas.Simulation(w.subset(sel), device=dev)
+        sim2.step(stream)
+        g = sim2.results()
+        sim2.close()
+        res["sample_parity"] = bool(all(np.array_equal(g[k], o[k]) for k in
+                                        ("ttft", "ttlt", "tbtmax", "counters", "pct")))
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

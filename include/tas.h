@@ -1,0 +1,196 @@
+/*
+ * tas.h - C ABI of the batched tail-aware serving simulation on MI355X.
+ *
+ * A sweep is a set of INSTANCES. Each instance pairs one synthetic request
+ * trace with one scheduling-policy setting and is simulated independently,
+ * iteration by iteration, as a continuous-batching LLM server:
+ *
+ *   - request i is (a_i arrival us, P_i prompt tokens known at arrival,
+ *     D_i decode tokens unknown to a blind policy)
+ *     (arXiv 2606.18431, section "Formulation", Notation);
+ *   - every iteration ranks the waiting and resident requests by a priority
+ *     key, smaller first, ties by request index:
+ *       TAS_FCFS   key = a_i                                   (Table 1, FCFS)
+ *       TAS_SRPT   key = P_i + D_i - 1 - kv_i  (exact remaining tokens;
+ *                  Table 1, SRPT with perfect length knowledge)
+ *       TAS_BOOST  key = a_i - boost_us[level(P_i + dec_i)]    (Phase 2 unified
+ *                  key Phi = a - b_gamma(w~) with w~ = max(w, s_pre); Phase 3
+ *                  MemGuard quantization level = floor(log2(max(w,k)/k)))
+ *   - a greedy pass fills the batch under a sequence cap, a token budget and a
+ *     KV-block budget, evicting (recompute preemption) the worst resident when
+ *     KV runs out; MemGuard and the hysteresis delta restrict voluntary
+ *     evictions (Algorithm 1; Phase 2 preemption protocol; Phase 3);
+ *   - the iteration costs base + tok * sum(tokens) + floor(sum(context)/div) us
+ *     (the engine's forward step, Algorithm 1 ExecuteOneStep, replaced by an
+ *     integer cost model);
+ *   - each request's TTFT, TTLT and maximum inter-token gap are recorded, and
+ *     reduced per instance to nearest-rank P50/P90/P99 (Phase 4, t_p).
+ *
+ * Everything is integer arithmetic; results are deterministic and independent
+ * of the launch configuration.
+ *
+ * Memory. Host pointers are marked HOST, device pointers DEVICE. The caller
+ * owns all memory: the workspace and every output buffer are device
+ * allocations made by the caller (for instance PyTorch tensors), which must
+ * stay allocated and untouched until the stream has been synchronised and the
+ * context destroyed. The context holds host metadata only; tas_destroy frees
+ * that and nothing else. One context is used by one host thread at a time.
+ *
+ * Streams. `stream` is a hipStream_t passed as void*; NULL is the default
+ * stream. tas_run, tas_percentiles, tas_latencies and tas_counters enqueue
+ * work and return without waiting; calls on one context must use one stream,
+ * or the caller orders them.
+ *
+ * Errors. Functions return TAS_OK (0) or a negative TAS_E* code; no C++
+ * exception crosses the ABI. Per-instance device errors are sticky and are
+ * reported by tas_status.
+ */
+#ifndef TAS_H
+#define TAS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    TAS_OK = 0,
+    TAS_EINVAL = -1,      /* invalid argument or input (see tas_create)        */
+    TAS_EINFEASIBLE = -2, /* a request needs more KV than the budget holds     */
+    TAS_ENOMEM = -3,      /* workspace too small                               */
+    TAS_EHIP = -4,        /* a HIP runtime call failed                         */
+    TAS_EOVERFLOW = -5,   /* a latency does not fit 32 bits of microseconds   */
+    TAS_ELIVELOCK = -6,   /* an instance exceeded max_iters iterations         */
+    TAS_ESTATE = -7,      /* internal consistency check failed                 */
+    TAS_ECAPACITY = -8    /* an instance outgrew its on-chip candidate list    */
+};
+
+enum { TAS_FCFS = 0, TAS_SRPT = 1, TAS_BOOST = 2 };
+
+#define TAS_LEVELS 24
+
+/* Request traces, trace-major structure-of-arrays (all HOST, read during
+ * tas_create only). Every trace holds n_req requests sorted by arrival. */
+typedef struct {
+    int32_t n_traces;
+    int32_t n_req;              /* 1 <= n_req < 2^20                           */
+    const int64_t *arrival_us;  /* [n_traces*n_req], 0 <= a < 2^41, sorted     */
+    const int32_t *prompt;      /* [n_traces*n_req], >= 1                      */
+    const int32_t *decode;      /* [n_traces*n_req], >= 1; P + D < 2^24        */
+} tas_traces;
+
+/* One instance: a trace and a policy setting. */
+typedef struct {
+    int32_t trace;    /* index into the traces                                 */
+    int32_t policy;   /* TAS_FCFS, TAS_SRPT or TAS_BOOST                       */
+    int32_t k;        /* MemGuard granularity in tokens (BOOST), >= 1          */
+    int32_t memguard; /* 1: a dispatched request is non-evictable until its
+                         level passes the level it was dispatched at (BOOST)  */
+    int64_t delta_us; /* hysteresis: a voluntary victim's key must exceed the
+                         candidate's by more than delta (BOOST), >= 0          */
+    double gamma;     /* BOOST: > 0 builds boost_us from the gamma-Boost curve
+                         (tas_boost_table); 0 uses boost_us as given           */
+    int32_t table_given; /* 1: boost_us is an explicit table (gamma ignored)  */
+    int32_t reserved;
+    int64_t boost_us[TAS_LEVELS]; /* explicit table: non-increasing, in
+                                     [0, 2^42]                                 */
+} tas_setting;
+
+/* Engine limits, cost model and the instance list (HOST). */
+typedef struct {
+    int32_t max_seqs;      /* sequences per iteration, >= 1                    */
+    int32_t max_tokens;    /* tokens per iteration, >= chunk                   */
+    int32_t chunk;         /* prefill chunk, >= 1                              */
+    int32_t kv_blocks;     /* KV budget in blocks, >= 1                        */
+    int32_t block_tokens;  /* tokens per KV block, >= 1                        */
+    int32_t iter_base_us;  /* iteration cost: base + tok*sum(n)                */
+    int32_t iter_tok_us;   /*   + floor(sum(kv+n) / ctx_div), base >= 1        */
+    int32_t iter_ctx_div;  /*   ctx_div >= 1                                   */
+    int64_t max_iters;     /* per-instance iteration limit (TAS_ELIVELOCK)     */
+    double tau_us;         /* microseconds per token of boost, > 0             */
+    int32_t list_cap;      /* on-chip candidate entries per instance; 0 picks
+                              a default from max_seqs                          */
+    int32_t spill_cap;     /* waiting entries per instance kept in HBM beyond
+                              the on-chip list; 0 = n_req                      */
+    int32_t n_inst;
+    int32_t reserved;
+    const tas_setting *inst; /* [n_inst]                                       */
+} tas_params;
+
+typedef struct tas_ctx tas_ctx;
+
+/* Bytes of device workspace tas_create needs for these inputs, or 0 if the
+ * arguments are invalid. */
+size_t tas_workspace_bytes(const tas_traces *traces, const tas_params *params);
+
+/* Validate the inputs, build every boost table, lay out the workspace and
+ * copy the traces and settings into it (synchronous host-to-device copies).
+ * d_ws: DEVICE buffer of ws_bytes >= tas_workspace_bytes(...), 256-byte
+ * aligned, owned by the caller. *out receives a new context.
+ * Returns TAS_EINVAL if: n_req < 1 or >= 2^20; an arrival is negative,
+ * >= 2^41 or out of order; P or D < 1; P + D >= 2^24; a trace index is out of
+ * range; policy unknown; k < 1 (BOOST); delta < 0; memguard or delta nonzero
+ * for FCFS/SRPT; gamma <= 0 without table_given (BOOST); an explicit table not
+ * non-increasing or outside [0, 2^42]; chunk > max_tokens; any engine limit
+ * < 1; tau <= 0; list_cap too small for max_seqs or above the LDS limit.
+ * TAS_EINFEASIBLE if ceil((P + D - 1) / block_tokens) > kv_blocks for some
+ * request. TAS_ENOMEM if ws_bytes is too small. TAS_EHIP if a copy fails. */
+int tas_create(const tas_traces *traces, const tas_params *params, void *d_ws, size_t ws_bytes,
+               tas_ctx **out);
+
+/* Enqueue the simulation of every instance on `stream` (one workgroup per
+ * instance). Per-request latencies, counters and errors land in the
+ * workspace. */
+int tas_run(tas_ctx *ctx, void *stream);
+
+/* Enqueue the nearest-rank percentile reduction: d_out DEVICE uint32
+ * [n_inst][3][3] = {TTFT, TTLT, TBTmax} x {P50, P90, P99}, the value at
+ * sorted position ceil(q*n_req/100) - 1 (Phase 4, t_p). Call after tas_run on
+ * the same stream. */
+int tas_percentiles(tas_ctx *ctx, uint32_t *d_out, void *stream);
+
+/* Enqueue device-to-device copies of the per-request latencies, DEVICE
+ * uint32 [n_inst][n_req] each, microseconds relative to arrival; any pointer
+ * may be NULL to skip that array. */
+int tas_latencies(tas_ctx *ctx, uint32_t *d_ttft, uint32_t *d_ttlt, uint32_t *d_tbtmax,
+                  void *stream);
+
+/* Enqueue a copy of the per-instance counters, DEVICE int64 [n_inst][8]:
+ * iterations, request-iterations (sum of batch sizes), computed tokens,
+ * voluntary evictions, forced evictions, final clock us, peak KV blocks,
+ * idle us. */
+int tas_counters(tas_ctx *ctx, int64_t *d_out, void *stream);
+
+/* Synchronise the stream of the last enqueued call and return TAS_OK or the
+ * first per-instance error (lowest instance index), e.g. TAS_ELIVELOCK,
+ * TAS_EOVERFLOW, TAS_ECAPACITY; TAS_EHIP if the stream reports a failure. */
+int tas_status(tas_ctx *ctx);
+
+/* Per-instance status codes, DEVICE int32 [n_inst] (enqueued copy). */
+int tas_instance_status(tas_ctx *ctx, int32_t *d_out, void *stream);
+
+/* Free the context's host metadata; device memory is untouched. */
+void tas_destroy(tas_ctx *ctx);
+
+/* A static English description of a return code. */
+const char *tas_strerror(int code);
+
+/* The gamma-Boost table (Eq. boost_function): out[j] = min(2^42,
+ * round(tau_us * b_gamma(k 2^j))) with b_gamma(w) = (1/gamma) ln(1/(1 -
+ * exp(-gamma w))), evaluated in double precision on the host. out: HOST
+ * int64[TAS_LEVELS]. Returns TAS_EINVAL unless gamma > 0, k >= 1, tau > 0. */
+int tas_boost_table(double gamma, int32_t k, double tau_us, int64_t *out);
+
+/* The boost table an instance uses (as built by tas_create). out: HOST
+ * int64[TAS_LEVELS]. */
+int tas_instance_table(const tas_ctx *ctx, int32_t inst, int64_t *out);
+
+/* The on-chip candidate-list capacity the context uses per instance. */
+int32_t tas_list_cap(const tas_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

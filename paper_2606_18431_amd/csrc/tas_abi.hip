@@ -1,0 +1,310 @@
+// tas_abi.hip - host side of the C ABI declared in include/tas.h.
+//
+// tas_create validates the inputs on the host (so every rejection is testable
+// without a GPU), builds each instance's boost table, lays the workspace out
+// and copies the traces and settings into it once. tas_run / tas_percentiles
+// only enqueue kernels; nothing on the path allocates.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "tas.h"
+#include "tas_internal.h"
+
+struct tas_ctx {
+    int32_t n_traces = 0, n_req = 0, n_inst = 0, list_cap = 0, spill_cap = 0;
+    int64_t lds_bytes = 0;
+    tas::SimArgs args{};
+    std::vector<tas::DevSetting> settings;
+    hipStream_t last_stream = nullptr;
+};
+
+namespace {
+
+constexpr int64_t kMaxLds = 160 * 1024;  // gfx950 LDS per workgroup
+constexpr int64_t kTwo41 = int64_t(1) << 41;
+constexpr int64_t kTwo42 = int64_t(1) << 42;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Layout {
+    size_t arrival, prompt, decode, settings, tfirst, tlast, tbtw, ttft, ttlt, tbtmax, counters,
+        status, spill, ovf, total;
+};
+
+int32_t default_list_cap(int32_t max_seqs) {
+    int64_t lc = (int64_t)max_seqs + std::max<int64_t>(2 * (int64_t)max_seqs, 256);
+    lc = (lc + 63) / 64 * 64;
+    return (int32_t)lc;
+}
+
+bool engine_ok(const tas_params *p) {
+    return p->max_seqs >= 1 && p->max_tokens >= 1 && p->chunk >= 1 && p->chunk <= p->max_tokens &&
+           p->kv_blocks >= 1 && p->block_tokens >= 1 && p->iter_base_us >= 1 &&
+           p->iter_tok_us >= 0 && p->iter_ctx_div >= 1 && p->max_iters >= 1 &&
+           p->tau_us > 0.0 && std::isfinite(p->tau_us) && p->n_inst >= 0 &&
+           p->list_cap >= 0 && p->spill_cap >= 0 && (p->n_inst == 0 || p->inst != nullptr);
+}
+
+bool shape_ok(const tas_traces *t) {
+    return t && t->n_traces >= 1 && t->n_req >= 1 && t->n_req < (1 << 20) && t->arrival_us &&
+           t->prompt && t->decode;
+}
+
+// Effective capacities; false if invalid.
+bool caps(const tas_traces *t, const tas_params *p, int32_t *lc, int32_t *sc) {
+    int32_t l = p->list_cap ? p->list_cap : default_list_cap(p->max_seqs);
+    if ((int64_t)l < (int64_t)p->max_seqs + 64) return false;
+    if (tas::lds_bytes_for(l) > kMaxLds) return false;
+    int32_t s = p->spill_cap ? p->spill_cap : t->n_req;
+    *lc = l;
+    *sc = s;
+    return true;
+}
+
+bool layout(const tas_traces *t, const tas_params *p, int32_t lc, int32_t sc, Layout *L) {
+    const size_t tn = (size_t)t->n_traces * (size_t)t->n_req;
+    const size_t in = (size_t)p->n_inst * (size_t)t->n_req;
+    size_t o = 0;
+    L->arrival = o, o = align256(o + tn * 8);
+    L->prompt = o, o = align256(o + tn * 4);
+    L->decode = o, o = align256(o + tn * 4);
+    L->settings = o, o = align256(o + (size_t)p->n_inst * sizeof(tas::DevSetting));
+    L->tfirst = o, o = align256(o + in * 8);
+    L->tlast = o, o = align256(o + in * 8);
+    L->tbtw = o, o = align256(o + in * 4);
+    L->ttft = o, o = align256(o + in * 4);
+    L->ttlt = o, o = align256(o + in * 4);
+    L->tbtmax = o, o = align256(o + in * 4);
+    L->counters = o, o = align256(o + (size_t)p->n_inst * 8 * 8);
+    L->status = o, o = align256(o + (size_t)p->n_inst * 4);
+    L->spill = o, o = align256(o + (size_t)p->n_inst * (size_t)sc * sizeof(tas::Rec));
+    L->ovf = o, o = align256(o + (size_t)p->n_inst * (size_t)lc * sizeof(tas::Rec));
+    L->total = o;
+    return true;
+}
+
+// ln(1 - exp(-x)) for x > 0, accurate on both sides of ln 2 (Maechler 2012).
+double log1mexp(double x) { return x <= 0.6931471805599453 ? std::log(-std::expm1(-x)) : std::log1p(-std::exp(-x)); }
+
+int check_setting(const tas_setting &s, int32_t n_traces) {
+    if (s.trace < 0 || s.trace >= n_traces) return TAS_EINVAL;
+    if (s.policy < TAS_FCFS || s.policy > TAS_BOOST) return TAS_EINVAL;
+    if (s.delta_us < 0) return TAS_EINVAL;
+    if (s.policy != TAS_BOOST) {
+        if (s.memguard != 0 || s.delta_us != 0) return TAS_EINVAL;
+        return TAS_OK;
+    }
+    if (s.k < 1 || (s.memguard != 0 && s.memguard != 1)) return TAS_EINVAL;
+    if (s.delta_us >= kTwo42) return TAS_EINVAL;
+    if (s.table_given) {
+        for (int j = 0; j < TAS_LEVELS; j++) {
+            if (s.boost_us[j] < 0 || s.boost_us[j] > kTwo42) return TAS_EINVAL;
+            if (j && s.boost_us[j] > s.boost_us[j - 1]) return TAS_EINVAL;
+        }
+    } else if (!(s.gamma > 0.0) || !std::isfinite(s.gamma)) {
+        return TAS_EINVAL;
+    }
+    return TAS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tas_boost_table(double gamma, int32_t k, double tau_us, int64_t *out) {
+    if (!out || !(gamma > 0.0) || !std::isfinite(gamma) || k < 1 || !(tau_us > 0.0)) return TAS_EINVAL;
+    const double cap = (double)kTwo42;
+    for (int j = 0; j < TAS_LEVELS; j++) {
+        const double w = (double)k * std::ldexp(1.0, j);  // quantized signal k 2^j
+        const double b = -log1mexp(gamma * w) / gamma;     // b_gamma(w) in tokens
+        const double us = tau_us * b;
+        out[j] = us >= cap ? kTwo42 : (int64_t)std::llround(us);
+    }
+    return TAS_OK;
+}
+
+size_t tas_workspace_bytes(const tas_traces *t, const tas_params *p) {
+    if (!shape_ok(t) || !p || !engine_ok(p)) return 0;
+    int32_t lc, sc;
+    if (!caps(t, p, &lc, &sc)) return 0;
+    Layout L;
+    layout(t, p, lc, sc, &L);
+    return L.total;
+}
+
+int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_bytes,
+               tas_ctx **out) {
+    if (!out) return TAS_EINVAL;
+    *out = nullptr;
+    if (!shape_ok(t) || !p || !engine_ok(p)) return TAS_EINVAL;
+    int32_t lc, sc;
+    if (!caps(t, p, &lc, &sc)) return TAS_EINVAL;
+    const int32_t N = t->n_req;
+    const size_t tn = (size_t)t->n_traces * (size_t)N;
+    // traces: sorted, in range; P, D >= 1; P + D < 2^24
+    for (size_t i = 0; i < tn; i++) {
+        const int64_t a = t->arrival_us[i];
+        const int32_t P = t->prompt[i], D = t->decode[i];
+        if (a < 0 || a >= kTwo41 || P < 1 || D < 1 || (int64_t)P + D >= (int64_t(1) << 24))
+            return TAS_EINVAL;
+        if (i % (size_t)N && a < t->arrival_us[i - 1]) return TAS_EINVAL;
+    }
+    for (int32_t i = 0; i < p->n_inst; i++) {
+        int rc = check_setting(p->inst[i], t->n_traces);
+        if (rc) return rc;
+    }
+    for (size_t i = 0; i < tn; i++) {
+        const int64_t need = ((int64_t)t->prompt[i] + t->decode[i] - 1 + p->block_tokens - 1) /
+                             p->block_tokens;
+        if (need > p->kv_blocks) return TAS_EINFEASIBLE;
+    }
+    Layout L;
+    layout(t, p, lc, sc, &L);
+    if (!d_ws || ws_bytes < L.total || ((uintptr_t)d_ws & 255u)) return TAS_ENOMEM;
+
+    tas_ctx *c = new (std::nothrow) tas_ctx();
+    if (!c) return TAS_ENOMEM;
+    c->n_traces = t->n_traces, c->n_req = N, c->n_inst = p->n_inst;
+    c->list_cap = lc, c->spill_cap = sc;
+    c->lds_bytes = tas::lds_bytes_for(lc);
+    c->settings.resize((size_t)p->n_inst);
+    for (int32_t i = 0; i < p->n_inst; i++) {
+        const tas_setting &s = p->inst[i];
+        tas::DevSetting &d = c->settings[(size_t)i];
+        std::memset(&d, 0, sizeof d);
+        d.trace = s.trace, d.policy = s.policy, d.k = s.policy == TAS_BOOST ? s.k : 1;
+        d.memguard = s.policy == TAS_BOOST ? s.memguard : 0;
+        d.delta = s.policy == TAS_BOOST ? s.delta_us : 0;
+        if (s.policy == TAS_BOOST) {
+            if (s.table_given) std::memcpy(d.bt, s.boost_us, sizeof d.bt);
+            else tas_boost_table(s.gamma, s.k, p->tau_us, d.bt);
+        }
+    }
+    char *ws = (char *)d_ws;
+    bool ok = hipMemcpy(ws + L.arrival, t->arrival_us, tn * 8, hipMemcpyHostToDevice) == hipSuccess &&
+              hipMemcpy(ws + L.prompt, t->prompt, tn * 4, hipMemcpyHostToDevice) == hipSuccess &&
+              hipMemcpy(ws + L.decode, t->decode, tn * 4, hipMemcpyHostToDevice) == hipSuccess;
+    if (ok && p->n_inst > 0)
+        ok = hipMemcpy(ws + L.settings, c->settings.data(),
+                       c->settings.size() * sizeof(tas::DevSetting),
+                       hipMemcpyHostToDevice) == hipSuccess;
+    if (!ok) {
+        delete c;
+        return TAS_EHIP;
+    }
+    tas::SimArgs &a = c->args;
+    a.arrival = (const int64_t *)(ws + L.arrival);
+    a.prompt = (const int32_t *)(ws + L.prompt);
+    a.decode = (const int32_t *)(ws + L.decode);
+    a.inst = (const tas::DevSetting *)(ws + L.settings);
+    a.tfirst = (int64_t *)(ws + L.tfirst);
+    a.tlast = (int64_t *)(ws + L.tlast);
+    a.tbtw = (uint32_t *)(ws + L.tbtw);
+    a.ttft = (uint32_t *)(ws + L.ttft);
+    a.ttlt = (uint32_t *)(ws + L.ttlt);
+    a.tbtmax = (uint32_t *)(ws + L.tbtmax);
+    a.counters = (int64_t *)(ws + L.counters);
+    a.status = (int32_t *)(ws + L.status);
+    a.spill = (tas::Rec *)(ws + L.spill);
+    a.ovf = (tas::Rec *)(ws + L.ovf);
+    a.max_iters = p->max_iters;
+    a.n_req = N, a.n_inst = p->n_inst;
+    a.M = p->max_seqs, a.T = p->max_tokens, a.c = p->chunk, a.Kb = p->kv_blocks;
+    a.bs = p->block_tokens, a.base = p->iter_base_us, a.tok = p->iter_tok_us;
+    a.div = p->iter_ctx_div, a.list_cap = lc, a.spill_cap = sc;
+    *out = c;
+    return TAS_OK;
+}
+
+int tas_run(tas_ctx *c, void *stream) {
+    if (!c) return TAS_EINVAL;
+    c->last_stream = (hipStream_t)stream;
+    return tas_launch_sim(c->args, c->lds_bytes, stream) ? TAS_EHIP : TAS_OK;
+}
+
+int tas_percentiles(tas_ctx *c, uint32_t *d_out, void *stream) {
+    if (!c || !d_out) return TAS_EINVAL;
+    c->last_stream = (hipStream_t)stream;
+    return tas_launch_pctl(c->args.ttft, c->args.ttlt, c->args.tbtmax, c->n_inst, c->n_req, d_out,
+                           stream)
+               ? TAS_EHIP
+               : TAS_OK;
+}
+
+int tas_latencies(tas_ctx *c, uint32_t *d_ttft, uint32_t *d_ttlt, uint32_t *d_tbtmax,
+                  void *stream) {
+    if (!c) return TAS_EINVAL;
+    c->last_stream = (hipStream_t)stream;
+    const size_t bytes = (size_t)c->n_inst * (size_t)c->n_req * 4;
+    const uint32_t *src[3] = {c->args.ttft, c->args.ttlt, c->args.tbtmax};
+    uint32_t *dst[3] = {d_ttft, d_ttlt, d_tbtmax};
+    for (int m = 0; m < 3; m++)
+        if (dst[m] && bytes &&
+            hipMemcpyAsync(dst[m], src[m], bytes, hipMemcpyDeviceToDevice,
+                           (hipStream_t)stream) != hipSuccess)
+            return TAS_EHIP;
+    return TAS_OK;
+}
+
+int tas_counters(tas_ctx *c, int64_t *d_out, void *stream) {
+    if (!c || !d_out) return TAS_EINVAL;
+    c->last_stream = (hipStream_t)stream;
+    if (c->n_inst == 0) return TAS_OK;
+    return hipMemcpyAsync(d_out, c->args.counters, (size_t)c->n_inst * 64,
+                          hipMemcpyDeviceToDevice, (hipStream_t)stream) == hipSuccess
+               ? TAS_OK
+               : TAS_EHIP;
+}
+
+int tas_instance_status(tas_ctx *c, int32_t *d_out, void *stream) {
+    if (!c || !d_out) return TAS_EINVAL;
+    c->last_stream = (hipStream_t)stream;
+    if (c->n_inst == 0) return TAS_OK;
+    return hipMemcpyAsync(d_out, c->args.status, (size_t)c->n_inst * 4, hipMemcpyDeviceToDevice,
+                          (hipStream_t)stream) == hipSuccess
+               ? TAS_OK
+               : TAS_EHIP;
+}
+
+int tas_status(tas_ctx *c) {
+    if (!c) return TAS_EINVAL;
+    if (hipStreamSynchronize(c->last_stream) != hipSuccess) return TAS_EHIP;
+    if (c->n_inst == 0) return TAS_OK;
+    std::vector<int32_t> st((size_t)c->n_inst);
+    if (hipMemcpy(st.data(), c->args.status, st.size() * 4, hipMemcpyDeviceToHost) != hipSuccess)
+        return TAS_EHIP;
+    for (int32_t v : st)
+        if (v) return v;
+    return TAS_OK;
+}
+
+void tas_destroy(tas_ctx *c) { delete c; }
+
+int tas_instance_table(const tas_ctx *c, int32_t inst, int64_t *out) {
+    if (!c || !out || inst < 0 || inst >= c->n_inst) return TAS_EINVAL;
+    std::memcpy(out, c->settings[(size_t)inst].bt, sizeof(int64_t) * TAS_LEVELS);
+    return TAS_OK;
+}
+
+int32_t tas_list_cap(const tas_ctx *c) { return c ? c->list_cap : 0; }
+
+const char *tas_strerror(int code) {
+    switch (code) {
+    case TAS_OK: return "ok";
+    case TAS_EINVAL: return "invalid argument";
+    case TAS_EINFEASIBLE: return "a request needs more KV blocks than the budget";
+    case TAS_ENOMEM: return "workspace too small or misaligned";
+    case TAS_EHIP: return "HIP runtime error";
+    case TAS_EOVERFLOW: return "a latency exceeds 2^32-1 microseconds";
+    case TAS_ELIVELOCK: return "an instance exceeded max_iters";
+    case TAS_ESTATE: return "internal consistency check failed";
+    case TAS_ECAPACITY: return "an instance outgrew its candidate-list or spill capacity";
+    default: return "unknown error";
+    }
+}
+
+}  // extern "C"

@@ -1,0 +1,73 @@
+// tas_internal.h - device-side layouts shared by the host ABI and the kernels.
+#pragma once
+#include <stdint.h>
+
+namespace tas {
+
+constexpr int kWave = 64;
+constexpr int kLevels = 24;
+constexpr int kStage = 64;              // staging slots behind the candidate list
+constexpr int64_t kKeyOff = int64_t(1) << 42;
+constexpr int kIdxBits = 21;            // packed key = (key + 2^42) << 21 | idx
+constexpr uint64_t kIdxMask = (uint64_t(1) << kIdxBits) - 1;
+
+// Policy parameters of one instance, as the kernel reads them.
+struct DevSetting {
+    int32_t trace;
+    int32_t policy;
+    int32_t k;
+    int32_t memguard;
+    int64_t delta;
+    int64_t bt[kLevels];  // boost in us per MemGuard level (non-increasing)
+};
+
+// A candidate-list record as it is parked in HBM (spilled waiting entries and
+// the overflow of a large re-sort). 40 bytes.
+struct Rec {
+    uint64_t pk;   // packed (key, idx)
+    int64_t tl;    // time of the last emitted token (absolute us)
+    int32_t w;     // signal: prompt + emitted tokens
+    int32_t left;  // tokens still to emit
+    int32_t kv;    // tokens with resident KV
+    uint32_t gs;   // flags, guard and level (see the kernel)
+    uint32_t tbt;  // max inter-token gap so far (us, saturating)
+    uint32_t pad;
+};
+
+struct SimArgs {
+    const int64_t *arrival;  // [n_traces][n_req]
+    const int32_t *prompt;
+    const int32_t *decode;
+    const DevSetting *inst;  // [n_inst]
+    int64_t *tfirst;         // [n_inst][n_req] absolute time of the first token
+    int64_t *tlast;          // [n_inst][n_req] absolute time of the last token
+    uint32_t *tbtw;          // [n_inst][n_req] max gap (working copy)
+    uint32_t *ttft;          // [n_inst][n_req] outputs, relative to arrival
+    uint32_t *ttlt;
+    uint32_t *tbtmax;
+    int64_t *counters;       // [n_inst][8]
+    int32_t *status;         // [n_inst]
+    Rec *spill;              // [n_inst][spill_cap]
+    Rec *ovf;                // [n_inst][list_cap]
+    int64_t max_iters;
+    int32_t n_req;
+    int32_t n_inst;
+    int32_t M, T, c, Kb, bs, base, tok, div;
+    int32_t list_cap;
+    int32_t spill_cap;
+};
+
+// Dynamic LDS bytes per workgroup for a list capacity.
+inline int64_t lds_bytes_for(int32_t list_cap) {
+    const int64_t cap = int64_t(list_cap) + kStage;
+    // pk, tl (8 B) + w, left, kv, gs, tbt, nn (4 B) per slot; boost table;
+    // 256-bin histogram; a few scalars
+    return cap * (8 + 8 + 6 * 4) + kLevels * 8 + 256 * 4 + 64;
+}
+
+}  // namespace tas
+
+// Launchers implemented next to the kernels.
+int tas_launch_sim(const tas::SimArgs &a, int64_t lds_bytes, void *stream);
+int tas_launch_pctl(const uint32_t *ttft, const uint32_t *ttlt, const uint32_t *tbtmax,
+                    int32_t n_inst, int32_t n_req, uint32_t *out, void *stream);

@@ -1,0 +1,104 @@
+// tas_pctl.hip - nearest-rank percentiles of the per-request latencies.
+//
+// For every instance and metric (TTFT, TTLT, max inter-token gap) the value
+// at sorted position ceil(q*n/100) - 1 for q in {50, 90, 99}: the empirical
+// t_p = inf{t : Fbar(t) <= (100-p)/100} (arXiv 2606.18431, Phase 4).
+//
+// One 256-thread workgroup per (instance, metric) runs an exact radix select
+// over the 32-bit values, 8 bits per pass, most significant digit first; the
+// three ranks share each pass over the data (one LDS histogram per rank; the
+// first pass, where no prefix is fixed yet, needs only one). Integer work
+// bound by HBM reads: 4 passes x 4 bytes per value.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tas_internal.h"
+
+namespace tas {
+namespace {
+
+constexpr int kThreads = 256;
+
+__global__ __launch_bounds__(kThreads) void pctl_kernel(const uint32_t *ttft, const uint32_t *ttlt,
+                                                        const uint32_t *tbt, int n_inst, int n,
+                                                        uint32_t *out) {
+    __shared__ uint32_t hist[3][256];
+    __shared__ uint32_t pre[3];
+    __shared__ int rk[3];
+    const int b = blockIdx.x;
+    const int inst = b / 3, metric = b % 3;
+    if (inst >= n_inst) return;
+    const uint32_t *v =
+        (metric == 0 ? ttft : metric == 1 ? ttlt : tbt) + (size_t)inst * (size_t)n;
+    const int tid = threadIdx.x;
+    if (tid < 3) {
+        const int q = tid == 0 ? 50 : tid == 1 ? 90 : 99;
+        rk[tid] = (int)(((int64_t)q * n + 99) / 100);
+        pre[tid] = 0;
+    }
+    for (int pass = 0; pass < 4; pass++) {
+        const int sh = 24 - 8 * pass;
+        for (int j = tid; j < 3 * 256; j += kThreads) (&hist[0][0])[j] = 0;
+        __syncthreads();
+        const uint32_t p0 = pre[0], p1 = pre[1], p2 = pre[2];
+        for (int i = tid; i < n; i += kThreads) {
+            const uint32_t x = v[i];
+            const uint32_t d = (x >> sh) & 255u;
+            if (pass == 0) {
+                atomicAdd(&hist[0][d], 1u);
+            } else {
+                const uint32_t hx = x >> (sh + 8);
+                if (hx == (p0 >> (sh + 8))) atomicAdd(&hist[0][d], 1u);
+                if (hx == (p1 >> (sh + 8))) atomicAdd(&hist[1][d], 1u);
+                if (hx == (p2 >> (sh + 8))) atomicAdd(&hist[2][d], 1u);
+            }
+        }
+        __syncthreads();
+        const int wv = tid >> 6, ln = tid & 63;
+        if (wv < 3) {
+            const uint32_t *h = pass == 0 ? hist[0] : hist[wv];
+            const int h0 = (int)h[4 * ln], h1 = (int)h[4 * ln + 1], h2 = (int)h[4 * ln + 2],
+                      h3 = (int)h[4 * ln + 3];
+            const int s = h0 + h1 + h2 + h3;
+            int inc = s;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const int y = __shfl_up(inc, o);
+                if (ln >= o) inc += y;
+            }
+            const int exc = inc - s;
+            const int r = rk[wv];
+            const uint64_t m = __ballot(exc < r && r <= inc);
+            if (m) {
+                const int src = __ffsll((unsigned long long)m) - 1;
+                int rr = r - __shfl(exc, src);
+                const int b0 = __shfl(h0, src), b1 = __shfl(h1, src), b2 = __shfl(h2, src);
+                int bin = 4 * src;
+                if (rr > b0) {
+                    rr -= b0, bin++;
+                    if (rr > b1) {
+                        rr -= b1, bin++;
+                        if (rr > b2) rr -= b2, bin++;
+                    }
+                }
+                if (ln == 0) {
+                    pre[wv] |= (uint32_t)bin << sh;
+                    rk[wv] = rr;
+                }
+            }
+        }
+        __syncthreads();
+    }
+    if (tid < 3) out[(size_t)inst * 9 + metric * 3 + tid] = pre[tid];
+}
+
+}  // namespace
+}  // namespace tas
+
+int tas_launch_pctl(const uint32_t *ttft, const uint32_t *ttlt, const uint32_t *tbtmax,
+                    int32_t n_inst, int32_t n_req, uint32_t *out, void *stream) {
+    if (n_inst <= 0) return 0;
+    hipLaunchKernelGGL(tas::pctl_kernel, dim3((unsigned)(3 * n_inst)), dim3(tas::kThreads), 0,
+                       (hipStream_t)stream, ttft, ttlt, tbtmax, n_inst, n_req, out);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}

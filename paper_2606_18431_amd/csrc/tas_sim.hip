@@ -1,0 +1,933 @@
+// tas_sim.hip - the iteration-level serving simulation, one wavefront per
+// instance (one trace x one policy setting), for gfx950.
+//
+// What each iteration computes (arXiv 2606.18431, Algorithm 1 with gamma
+// fixed; Phase 2 unified key and hysteresis; Phase 3 MemGuard):
+//   1. arrivals with a_i <= t join the waiting set;
+//   2. every waiting or resident request has a key; candidates are taken in
+//      ascending (key, idx) order;
+//   3. greedy batch formation under max_seqs, max_tokens and the KV budget;
+//      when the KV budget is exceeded the worst eligible resident outside the
+//      batch is evicted (recompute preemption); a resident candidate with no
+//      eligible victim forces out the worst other resident or itself; a
+//      waiting candidate that does not fit closes admissions;
+//   4. the step costs base + tok*sum(n) + floor(sum(kv+n)/div) us; tokens are
+//      emitted, first/last token times and the max inter-token gap recorded.
+//
+// Design (MI355X): instances are independent, so one 64-lane wavefront owns
+// one instance and needs no workgroup barrier. The active requests live in
+// LDS as one array sorted by the packed key (key + 2^42) << 21 | idx, with
+// their state in structure-of-arrays form, so the batch-formation pass is a
+// sequence of 64-wide chunks with wavefront prefix sums (token budget, KV
+// blocks, sequence count) and a ballot to find the first candidate that does
+// not fit; only that candidate takes the sequential eviction path. Keys of
+// waiting requests never change (MemGuard recomputes a key only when the
+// quantized signal moves, Phase 3), so the list is repaired incrementally:
+// finished entries are compacted out, entries whose key moved are extracted
+// and merged back. Waiting requests beyond the on-chip capacity spill to HBM
+// with the invariant that every spilled key exceeds every waiting key on
+// chip; a radix select over the spill refills the list.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tas_internal.h"
+
+namespace tas {
+namespace {
+
+#define DEV __device__ __forceinline__
+
+// record flag word (gs)
+constexpr uint32_t G_GUARD = 0x1fu;      // MemGuard level at the latest dispatch
+constexpr uint32_t G_RES = 1u << 5;      // resident: holds KV
+constexpr uint32_t G_FIRST = 1u << 6;    // first token emitted
+constexpr uint32_t G_INB = 1u << 7;      // in this iteration's batch
+constexpr uint32_t G_EVI = 1u << 8;      // evicted during this iteration
+constexpr uint32_t G_DONE = 1u << 9;     // completed
+constexpr uint32_t G_DIRTY = 1u << 10;   // key moved: re-insert
+constexpr uint32_t G_MARK = 1u << 11;    // selected for spilling
+constexpr int G_LVL_SHIFT = 12;          // current MemGuard level (5 bits)
+constexpr uint32_t G_LVL = 0x1fu << G_LVL_SHIFT;
+
+enum { S_OK = 0, S_EOVERFLOW = -5, S_ELIVELOCK = -6, S_ESTATE = -7, S_ECAPACITY = -8 };
+enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2 };
+
+// ------------------------------------------------------------ wave helpers
+
+DEV int lane() { return (int)__lane_id(); }
+DEV uint64_t ballot(bool p) { return (uint64_t)__ballot(p); }
+DEV int popc(uint64_t m) { return __popcll(m); }
+DEV int mbcnt(uint64_t m) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+DEV int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+DEV int rl(int x, int l) { return __builtin_amdgcn_readlane(x, l); }
+DEV uint64_t rlu(uint64_t x, int l) {
+    uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, l);
+    uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+DEV int64_t rl64(int64_t x, int l) { return (int64_t)rlu((uint64_t)x, l); }
+DEV uint64_t uniu(uint64_t x) { return rlu(x, __builtin_amdgcn_readfirstlane(lane())); }
+DEV void wsync() { __syncthreads(); }
+
+DEV int scan_add(int x) {
+    const int l = lane();
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        int y = __shfl_up(x, o);
+        if (l >= o) x += y;
+    }
+    return x;
+}
+DEV int wsum(int x) {
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    return uni(x);
+}
+DEV int wmin(int x) {
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) x = min(x, __shfl_xor(x, o));
+    return uni(x);
+}
+DEV uint64_t wmaxu(uint64_t x) {
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        uint64_t y = (uint64_t)__shfl_xor((unsigned long long)x, o);
+        x = y > x ? y : x;
+    }
+    return uniu(x);
+}
+DEV uint64_t wminu(uint64_t x) {
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        uint64_t y = (uint64_t)__shfl_xor((unsigned long long)x, o);
+        x = y < x ? y : x;
+    }
+    return uniu(x);
+}
+DEV uint64_t scan_maxu(uint64_t x) {
+    const int l = lane();
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        uint64_t y = (uint64_t)__shfl_up((unsigned long long)x, o);
+        if (l >= o && y > x) x = y;
+    }
+    return x;
+}
+
+// ------------------------------------------------------------ keys
+
+DEV uint64_t pack(int64_t key, int idx) {
+    return ((uint64_t)(key + kKeyOff) << kIdxBits) | (uint64_t)(uint32_t)idx;
+}
+DEV int64_t key_of(uint64_t pk) { return (int64_t)(pk >> kIdxBits) - kKeyOff; }
+DEV int idx_of(uint64_t pk) { return (int)(pk & kIdxMask); }
+
+// MemGuard level floor(log2(max(w,k)/k)) capped at 23, without a division:
+// with e = floor(log2 w) - floor(log2 k), the level is e when w >= k 2^e and
+// e - 1 otherwise (Eq. memguard_level).
+DEV int level_of(int w, int k, int lk) {
+    if (w < k) return 0;
+    int e = (31 - __clz(w)) - lk;
+    int L = ((w >> e) >= k) ? e : e - 1;
+    return L < kLevels - 1 ? L : kLevels - 1;
+}
+
+// ------------------------------------------------------------ LDS layout
+
+struct Lds {
+    uint64_t *pk;
+    int64_t *tl;
+    int64_t *bt;
+    int32_t *w, *left, *kv, *nn;
+    uint32_t *gs, *tbt, *hist;
+};
+
+struct R {  // one candidate-list record in registers
+    uint64_t pk = 0;
+    int64_t tl = 0;
+    int w = 0, left = 0, kv = 0;
+    uint32_t gs = 0, tbt = 0;
+};
+
+DEV void ldr(const Lds &S, int i, R &x) {
+    x.pk = S.pk[i];
+    x.tl = S.tl[i];
+    x.w = S.w[i];
+    x.left = S.left[i];
+    x.kv = S.kv[i];
+    x.gs = S.gs[i];
+    x.tbt = S.tbt[i];
+}
+DEV void str(const Lds &S, int i, const R &x) {
+    S.pk[i] = x.pk;
+    S.tl[i] = x.tl;
+    S.w[i] = x.w;
+    S.left[i] = x.left;
+    S.kv[i] = x.kv;
+    S.gs[i] = x.gs;
+    S.tbt[i] = x.tbt;
+}
+DEV R from_rec(const Rec &r) {
+    R x;
+    x.pk = r.pk, x.tl = r.tl, x.w = r.w, x.left = r.left, x.kv = r.kv, x.gs = r.gs, x.tbt = r.tbt;
+    return x;
+}
+DEV Rec to_rec(const R &x) {
+    Rec r;
+    r.pk = x.pk, r.tl = x.tl, r.w = x.w, r.left = x.left, r.kv = x.kv, r.gs = x.gs, r.tbt = x.tbt;
+    r.pad = 0;
+    return r;
+}
+DEV R shfl_rec(const R &x, int src) {
+    R y;
+    y.pk = (uint64_t)__shfl((unsigned long long)x.pk, src);
+    y.tl = (int64_t)__shfl((long long)x.tl, src);
+    y.w = __shfl(x.w, src);
+    y.left = __shfl(x.left, src);
+    y.kv = __shfl(x.kv, src);
+    y.gs = (uint32_t)__shfl((int)x.gs, src);
+    y.tbt = (uint32_t)__shfl((int)x.tbt, src);
+    return y;
+}
+
+// ------------------------------------------------------------ the simulator
+
+template <int POL>
+struct Sim {
+    const SimArgs &A;
+    Lds S;
+    // instance constants
+    int inst, N, M, T, c, Kb, bs, bs_shift, base, tok, div, k, lk, memguard, lcap, scap;
+    int64_t delta, max_iters;
+    const int64_t *arr;
+    const int32_t *Pp, *Dp;
+    int64_t *tfirst, *tlast;
+    uint32_t *tbtw;
+    Rec *spill, *ovf;
+    // state
+    int64_t t;
+    int U, L, nW, spill_n, next, pf, completed, status;
+    uint64_t spill_min;
+    int64_t pa;
+    int pP, pD;
+    int64_t iters, reqiters, tokens, ev_vol, ev_forced, maxU, idle;
+    // per-iteration formation results
+    int cnt, used, hi;
+    int64_t sum_ctx;
+
+    DEV Sim(const SimArgs &a, const DevSetting &st, int i, unsigned char *smem) : A(a) {
+        inst = i;
+        N = a.n_req, M = a.M, T = a.T, c = a.c, Kb = a.Kb, bs = a.bs;
+        base = a.base, tok = a.tok, div = a.div, lcap = a.list_cap, scap = a.spill_cap;
+        bs_shift = (bs & (bs - 1)) == 0 ? (31 - __clz(bs)) : -1;
+        k = st.k > 0 ? st.k : 1;
+        lk = 31 - __clz(k);
+        memguard = st.memguard;
+        delta = st.delta;
+        max_iters = a.max_iters;
+        const size_t toff = (size_t)st.trace * (size_t)N;
+        arr = a.arrival + toff, Pp = a.prompt + toff, Dp = a.decode + toff;
+        const size_t ioff = (size_t)i * (size_t)N;
+        tfirst = a.tfirst + ioff, tlast = a.tlast + ioff, tbtw = a.tbtw + ioff;
+        spill = a.spill + (size_t)i * (size_t)scap;
+        ovf = a.ovf + (size_t)i * (size_t)lcap;
+        const int cap = lcap + kStage;
+        size_t o = 0;
+        S.pk = (uint64_t *)(smem + o), o += (size_t)cap * 8;
+        S.tl = (int64_t *)(smem + o), o += (size_t)cap * 8;
+        S.bt = (int64_t *)(smem + o), o += kLevels * 8;
+        S.w = (int32_t *)(smem + o), o += (size_t)cap * 4;
+        S.left = (int32_t *)(smem + o), o += (size_t)cap * 4;
+        S.kv = (int32_t *)(smem + o), o += (size_t)cap * 4;
+        S.nn = (int32_t *)(smem + o), o += (size_t)cap * 4;
+        S.gs = (uint32_t *)(smem + o), o += (size_t)cap * 4;
+        S.tbt = (uint32_t *)(smem + o), o += (size_t)cap * 4;
+        S.hist = (uint32_t *)(smem + o);
+        for (int j = lane(); j < kLevels; j += kWave) S.bt[j] = st.bt[j];
+        t = 0;
+        U = L = nW = spill_n = next = pf = completed = status = 0;
+        spill_min = ~0ull;
+        iters = reqiters = tokens = ev_vol = ev_forced = maxU = idle = 0;
+        cnt = used = hi = 0;
+        sum_ctx = 0;
+        wsync();
+    }
+
+    DEV void fail(int code) {
+        if (status == 0) status = code;
+    }
+    DEV int blocks(int x) const { return bs_shift >= 0 ? (x + bs - 1) >> bs_shift : (x + bs - 1) / bs; }
+
+    // ---------------------------------------------------------- arrivals
+
+    DEV void load_pf() {
+        const int r = pf + lane();
+        if (r < N) {
+            pa = arr[r], pP = Pp[r], pD = Dp[r];
+        } else {
+            pa = INT64_MAX, pP = 1, pD = 1;
+        }
+    }
+
+    DEV R new_record(int idx, int64_t a, int P, int D) const {
+        R x;
+        x.w = P, x.left = D, x.kv = 0, x.tl = 0, x.tbt = 0;
+        int64_t key;
+        uint32_t lvl = 0;
+        if (POL == P_FCFS) {
+            key = a;
+        } else if (POL == P_SRPT) {
+            key = (int64_t)P + D - 1;
+        } else {
+            lvl = (uint32_t)level_of(P, k, lk);
+            key = a - S.bt[lvl];
+        }
+        x.gs = lvl << G_LVL_SHIFT;
+        x.pk = pack(key, idx);
+        return x;
+    }
+
+    // Arrivals with a <= t join the waiting set, up to 64 per round.
+    DEV void take_arrivals() {
+        for (int round = 0; round <= (N >> 6) + 1 && status == 0; round++) {
+            int off = next - pf;
+            if (off >= kWave) {
+                pf = next;
+                load_pf();
+                off = 0;
+            }
+            const int r = pf + lane();
+            const bool arrive = lane() >= off && r < N && pa <= t;
+            const int n_arr = popc(ballot(arrive));
+            if (n_arr == 0) return;
+            R x = new_record(r, pa, pP, pD);
+            R y = shfl_rec(x, min(off + lane(), kWave - 1));
+            nW += n_arr;
+            next += n_arr;
+            add_entries(y, n_arr);
+            if (off + n_arr < kWave) return;
+        }
+    }
+
+    // ---------------------------------------------------------- list edits
+
+    // Merge K records held by lanes [0, K) into the sorted list.
+    // Requires L + K <= lcap + kStage.
+    DEV void merge_new(const R &x, int K) {
+        if (K <= 0) return;
+        const bool act = lane() < K;
+        int lo = 0, hi_ = L;
+        if (act) {
+            for (int s = 0; s < 32 && lo < hi_; s++) {
+                int mid = (lo + hi_) >> 1;
+                if (S.pk[mid] < x.pk) lo = mid + 1;
+                else hi_ = mid;
+            }
+        }
+        const int pos = lo;
+        int rn = 0;
+        for (int j = 0; j < K; j++) {
+            uint64_t y = rlu(x.pk, j);
+            rn += (act && y < x.pk) ? 1 : 0;
+        }
+        const int minpos = wmin(act ? pos : INT32_MAX);
+        if (L > 0) {
+            for (int b = ((L - 1) >> 6) << 6; b >= 0 && b + kWave > minpos; b -= kWave) {
+                const int r = b + lane();
+                const bool mv = r >= minpos && r < L;
+                R y;
+                if (mv) ldr(S, r, y);
+                int sh = 0;
+                for (int j = 0; j < K; j++) sh += (rl(pos, j) <= r) ? 1 : 0;
+                wsync();
+                if (mv && sh) str(S, r + sh, y);
+                wsync();
+            }
+        }
+        if (act) str(S, pos + rn, x);
+        wsync();
+        L += K;
+    }
+
+    // Remove marked entries at ranks >= from (stable).
+    DEV void compact_marked(int from) {
+        int out = from;
+        for (int b = (from >> 6) << 6; b < L; b += kWave) {
+            const int r = b + lane();
+            const bool v = r >= from && r < L;
+            R y;
+            if (v) ldr(S, r, y);
+            const bool keep = v && !(y.gs & G_MARK);
+            const uint64_t km = ballot(keep);
+            wsync();
+            if (keep) {
+                const int d = out + mbcnt(km);
+                if (d != r) str(S, d, y);
+            }
+            wsync();
+            out += popc(km);
+        }
+        L = out;
+    }
+
+    // Spill the L - lcap largest waiting entries to HBM.
+    DEV void spill_excess() {
+        const int E = L - lcap;
+        if (E <= 0) return;
+        if (spill_n + E > scap) {
+            fail(S_ECAPACITY);
+            return;
+        }
+        int found = 0, lowest = L;
+        for (int b = ((L - 1) >> 6) << 6; b >= 0 && found < E; b -= kWave) {
+            const int r = b + lane();
+            const bool isw = r < L && !(S.gs[r] & G_RES);
+            const uint64_t m = ballot(isw);
+            const int above = popc(m) - mbcnt(m) - 1;
+            const bool take = isw && above < E - found;
+            if (take) {
+                R y;
+                ldr(S, r, y);
+                spill[spill_n + found + above] = to_rec(y);
+                S.gs[r] = y.gs | G_MARK;
+            }
+            const uint64_t tm = ballot(take);
+            found += popc(tm);
+            if (tm) lowest = b + (__ffsll((unsigned long long)tm) - 1);
+        }
+        wsync();
+        if (found < E) {
+            fail(S_ECAPACITY);
+            return;
+        }
+        const uint64_t mn = uniu(S.pk[lowest]);
+        spill_min = (spill_n == 0 || mn < spill_min) ? mn : spill_min;
+        spill_n += E;
+        nW -= E;
+        compact_marked(lowest);
+    }
+
+    // Add K records (lanes [0, K)) to the list; waiting ones whose key exceeds
+    // the spill's minimum go straight to the spill. L <= lcap on entry.
+    DEV void add_entries(R y, int K) {
+        if (spill_n > 0) {
+            const bool toS = lane() < K && !(y.gs & G_RES) && y.pk > spill_min;
+            const uint64_t sm = ballot(toS);
+            const int ns = popc(sm);
+            if (ns) {
+                if (spill_n + ns > scap) {
+                    fail(S_ECAPACITY);
+                    return;
+                }
+                if (toS) spill[spill_n + mbcnt(sm)] = to_rec(y);
+                spill_n += ns;
+                nW -= ns;
+                const uint64_t km = ballot(lane() < K && !toS);
+                if (lane() < K && !toS) str(S, lcap + mbcnt(km), y);
+                wsync();
+                K -= ns;
+                if (lane() < K) ldr(S, lcap + lane(), y);
+                wsync();
+            }
+        }
+        if (K > 0) merge_new(y, K);
+        if (L > lcap) spill_excess();
+    }
+
+    // The want-th smallest spilled key (radix select, 8 bits per pass).
+    DEV uint64_t select_kth(int want) {
+        uint64_t prefix = 0;
+        int rank = want;
+        for (int d = 7; d >= 0; d--) {
+            for (int j = lane(); j < 256; j += kWave) S.hist[j] = 0;
+            wsync();
+            const int sh = 8 * d;
+            for (int rd = 0; rd < spill_n; rd += kWave) {
+                const int i = rd + lane();
+                if (i < spill_n) {
+                    const uint64_t key = spill[i].pk;
+                    const bool match = (d == 7) || ((key >> (sh + 8)) == (prefix >> (sh + 8)));
+                    if (match) atomicAdd(&S.hist[(key >> sh) & 255u], 1u);
+                }
+            }
+            wsync();
+            const int l4 = 4 * lane();
+            const int h0 = (int)S.hist[l4], h1 = (int)S.hist[l4 + 1], h2 = (int)S.hist[l4 + 2],
+                      h3 = (int)S.hist[l4 + 3];
+            const int s = h0 + h1 + h2 + h3;
+            const int inc = scan_add(s);
+            const int exc = inc - s;
+            const uint64_t hm = ballot(exc < rank && rank <= inc);
+            if (hm == 0) {
+                fail(S_ESTATE);
+                return 0;
+            }
+            const int ln = __ffsll((unsigned long long)hm) - 1;
+            int rr = rank - rl(exc, ln);
+            const int b0 = rl(h0, ln), b1 = rl(h1, ln), b2 = rl(h2, ln);
+            int bin = 4 * ln;
+            if (rr > b0) {
+                rr -= b0, bin++;
+                if (rr > b1) {
+                    rr -= b1, bin++;
+                    if (rr > b2) rr -= b2, bin++;
+                }
+            }
+            prefix |= (uint64_t)bin << sh;
+            rank = rr;
+            wsync();
+        }
+        return prefix;
+    }
+
+    // Bring the smallest spilled entries back on chip.
+    DEV void refill() {
+        const int room = lcap - L;
+        const int want = min(spill_n, room);
+        if (want <= 0) return;
+        const uint64_t theta = want < spill_n ? select_kth(want) : ~0ull;
+        if (status) return;
+        int wr = 0, got = 0;
+        uint64_t newmin = ~0ull;
+        const int n0 = spill_n;
+        for (int rd = 0; rd < n0; rd += kWave) {
+            const int i = rd + lane();
+            const bool v = i < n0;
+            Rec s;
+            if (v) s = spill[i];
+            const bool sel = v && s.pk <= theta;
+            const bool keep = v && !sel;
+            const uint64_t km = ballot(keep), sm = ballot(sel);
+            if (keep) {
+                const int d = wr + mbcnt(km);
+                if (d != i) spill[d] = s;
+                if (s.pk < newmin) newmin = s.pk;
+            }
+            wr += popc(km);
+            const int ks = popc(sm);
+            if (ks) {
+                if (sel) str(S, lcap + mbcnt(sm), from_rec(s));
+                wsync();
+                R x;
+                if (lane() < ks) ldr(S, lcap + lane(), x);
+                wsync();
+                merge_new(x, ks);
+                got += ks;
+            }
+        }
+        if (got != want) fail(S_ESTATE);
+        spill_n = wr;
+        nW += got;
+        spill_min = wminu(newmin);
+    }
+
+    // ---------------------------------------------------------- formation
+
+    // Highest rank > q holding a resident outside the batch that may be
+    // evicted for candidate q (voluntary: MemGuard and hysteresis apply).
+    DEV int find_victim(int q, uint64_t pkq, bool voluntary) {
+        const int64_t keyq = key_of(pkq);
+        const int idxq = idx_of(pkq);
+        for (int b = ((L - 1) >> 6) << 6; b >= 0 && b + kWave - 1 > q; b -= kWave) {
+            const int r = b + lane();
+            bool e = false;
+            if (r > q && r < L) {
+                const uint32_t g = S.gs[r];
+                e = (g & G_RES) && !(g & G_INB);
+                if (POL == P_BOOST && voluntary && e) {
+                    if (memguard) e = ((g >> G_LVL_SHIFT) & 31u) > (g & G_GUARD);
+                    if (e && delta > 0) {
+                        const uint64_t pv = S.pk[r];
+                        const int64_t kd = key_of(pv) - delta;
+                        e = kd > keyq || (kd == keyq && idx_of(pv) > idxq);
+                    }
+                }
+            }
+            const uint64_t m = ballot(e);
+            if (m) return b + 63 - __clzll((unsigned long long)m);
+        }
+        return -1;
+    }
+
+    DEV void do_evict(int v) {
+        const int kvv = uni(S.kv[v]);
+        wsync();
+        if (lane() == 0) {
+            const uint32_t g = S.gs[v];
+            S.kv[v] = 0;
+            S.gs[v] = (g & ~G_RES) | G_EVI | (POL == P_SRPT ? G_DIRTY : 0u);
+        }
+        wsync();
+        U -= blocks(kvv);
+        nW++;
+        hi = max(hi, v + 1);
+    }
+
+    DEV void admit_one(int q, uint32_t g, int n, int du, int kvv) {
+        const bool res = (g & G_RES) != 0;
+        if (lane() == 0) {
+            S.nn[q] = n;
+            uint32_t g2 = g | G_INB;
+            if (!res) g2 = (g2 & ~G_GUARD) | G_RES | ((g >> G_LVL_SHIFT) & 31u);
+            S.gs[q] = g2;
+        }
+        wsync();
+        cnt++;
+        used += n;
+        U += du;
+        sum_ctx += kvv + n;
+        if (!res) nW--;
+    }
+
+    // Candidate q did not fit: evictions, or closing admissions.
+    DEV void slow_path(int q, bool &closed) {
+        const uint32_t g = (uint32_t)uni((int)S.gs[q]);
+        const int w = uni(S.w[q]);
+        const int kvv = uni(S.kv[q]);
+        const uint64_t pkq = uniu(S.pk[q]);
+        const bool res = (g & G_RES) != 0;
+        const int n = min(min(w - kvv, c), T - used);
+        const int du = blocks(kvv + n) - blocks(kvv);
+        for (int it = 0; it <= L + 1; it++) {
+            if (U + du <= Kb) {
+                admit_one(q, g, n, du, kvv);
+                return;
+            }
+            int v = find_victim(q, pkq, true);
+            if (v >= 0) {
+                do_evict(v);
+                ev_vol++;
+                continue;
+            }
+            if (res) {
+                v = find_victim(q, pkq, false);
+                if (v >= 0) {
+                    do_evict(v);
+                    ev_forced++;
+                    continue;
+                }
+                do_evict(q);
+                ev_forced++;
+                return;
+            }
+            closed = true;
+            return;
+        }
+        fail(S_ESTATE);
+    }
+
+    DEV void formation() {
+        cnt = 0, used = 0, hi = 0;
+        sum_ctx = 0;
+        bool closed = false;
+        int p = 0;
+        for (int guard = 0; guard <= 2 * L + 2 && p < L && cnt < M && used < T; guard++) {
+            const int r = p + lane();
+            const bool valid = r < L;
+            const uint32_t g = valid ? S.gs[r] : 0u;
+            const int w = valid ? S.w[r] : 0;
+            const int kvv = valid ? S.kv[r] : 0;
+            const bool res = (g & G_RES) != 0;
+            const bool cand = valid && !(g & G_EVI) && (res || !closed);
+            const int m = cand ? min(w - kvv, c) : 0;
+            const int ci = scan_add(cand ? 1 : 0);
+            const int mi = scan_add(m);
+            const int cb = cnt + ci - (cand ? 1 : 0);
+            const int ub = used + mi - m;
+            const bool adm = cand && cb < M && ub < T;
+            const int n = adm ? min(m, T - ub) : 0;
+            const int du = adm ? blocks(kvv + n) - blocks(kvv) : 0;
+            const int dui = scan_add(du);
+            const bool fit = U + dui <= Kb;
+            const uint64_t bad = ballot(adm && !fit);
+            const uint64_t am = ballot(adm);
+            const uint64_t okm =
+                bad ? (am & ((1ull << (__ffsll((unsigned long long)bad) - 1)) - 1ull)) : am;
+            const bool ok = ((okm >> lane()) & 1ull) != 0;
+            if (ok) {
+                S.nn[r] = n;
+                uint32_t g2 = g | G_INB;
+                if (!res) g2 = (g2 & ~G_GUARD) | G_RES | ((g >> G_LVL_SHIFT) & 31u);
+                S.gs[r] = g2;
+            }
+            if (okm) {
+                cnt += popc(okm);
+                used += wsum(ok ? n : 0);
+                U += wsum(ok ? du : 0);
+                sum_ctx += wsum(ok ? kvv + n : 0);
+                nW -= popc(ballot(ok && !res));
+            }
+            wsync();
+            if (bad) {
+                const int q = p + __ffsll((unsigned long long)bad) - 1;
+                slow_path(q, closed);
+                if (status) return;
+                p = q + 1;
+            } else {
+                p += kWave;
+            }
+        }
+        hi = max(hi, min(p, L));
+    }
+
+    // ---------------------------------------------------------- execute
+
+    // Returns the lowest rank whose key or presence changed (INT32_MAX if none).
+    DEV int emission(int64_t t_end) {
+        int lo = INT32_MAX, ufree = 0, ndone = 0;
+        bool bad_idx = false;
+        for (int b = 0; b < hi; b += kWave) {
+            const int r = b + lane();
+            const uint32_t g = r < hi ? S.gs[r] : 0u;
+            bool chg = false;
+            if (g & G_INB) {
+                R x;
+                ldr(S, r, x);
+                x.kv += S.nn[r];
+                const int idx = idx_of(x.pk);
+                if (idx >= N) bad_idx = true;
+                if (x.kv == x.w && idx < N) {
+                    x.w++;
+                    x.left--;
+                    if (!(x.gs & G_FIRST)) {
+                        x.gs |= G_FIRST;
+                        tfirst[idx] = t_end;
+                    } else {
+                        const int64_t gap = t_end - x.tl;
+                        const uint32_t gp = gap > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)gap;
+                        if (gp > x.tbt) x.tbt = gp;
+                    }
+                    x.tl = t_end;
+                    if (x.left == 0) {
+                        x.gs = (x.gs | G_DONE) & ~G_RES;
+                        ufree += blocks(x.kv);
+                        x.kv = 0;
+                        tlast[idx] = t_end;
+                        tbtw[idx] = x.tbt;
+                        chg = true;
+                        ndone++;
+                    } else if (POL == P_BOOST) {
+                        const int lo_ = (int)((x.gs >> G_LVL_SHIFT) & 31u);
+                        const int ln = level_of(x.w, k, lk);
+                        if (ln != lo_) {
+                            const int64_t key = key_of(x.pk) + S.bt[lo_] - S.bt[ln];
+                            x.pk = pack(key, idx);
+                            x.gs = (x.gs & ~G_LVL) | ((uint32_t)ln << G_LVL_SHIFT) | G_DIRTY;
+                            chg = true;
+                        }
+                    }
+                }
+                if (POL == P_SRPT && !(x.gs & G_DONE)) {
+                    x.pk = pack((int64_t)x.w + x.left - 1 - x.kv, idx);
+                    chg = true;
+                }
+                x.gs &= ~G_INB;
+                str(S, r, x);
+            } else if (g & G_EVI) {
+                if (POL == P_SRPT) {
+                    const uint64_t pk = S.pk[r];
+                    S.pk[r] = pack((int64_t)S.w[r] + S.left[r] - 1, idx_of(pk));
+                    chg = true;
+                }
+                S.gs[r] = g & ~G_EVI;
+            }
+            if (chg && r < lo) lo = r;
+        }
+        wsync();
+        if (ballot(bad_idx)) fail(S_ESTATE);
+        U -= wsum(ufree);
+        completed += wsum(ndone);
+        return wmin(lo);
+    }
+
+    // Compact out finished entries from rank `from` on; extract entries whose
+    // key moved (flagged, or below the running maximum) into the staging
+    // slots and, beyond 64, the HBM overflow. Returns the number extracted.
+    DEV int compact_extract(int from) {
+        const int start = (from >> 6) << 6;
+        uint64_t pmax = start > 0 ? uniu(S.pk[start - 1]) : 0ull;
+        int out = start, nx = 0;
+        for (int b = start; b < L; b += kWave) {
+            const int r = b + lane();
+            const bool v = r < L;
+            R y;
+            if (v) ldr(S, r, y);
+            const bool dead = v && (y.gs & G_DONE);
+            const bool dirty = v && (y.gs & G_DIRTY);
+            const uint64_t val = (v && !dead && !dirty) ? y.pk : 0ull;
+            const uint64_t inc = scan_maxu(val);
+            uint64_t exc = (uint64_t)__shfl_up((unsigned long long)inc, 1);
+            if (lane() == 0) exc = 0;
+            if (pmax > exc) exc = pmax;
+            const bool ext = v && !dead && (dirty || y.pk < exc);
+            const bool keep = v && !dead && !ext;
+            const uint64_t km = ballot(keep), xm = ballot(ext);
+            wsync();
+            if (keep) {
+                const int d = out + mbcnt(km);
+                if (d != r) str(S, d, y);
+            }
+            if (ext) {
+                y.gs &= ~G_DIRTY;
+                const int xi = nx + mbcnt(xm);
+                if (xi < kStage) str(S, lcap + xi, y);
+                else ovf[xi - kStage] = to_rec(y);
+            }
+            wsync();
+            const uint64_t cm = wmaxu(val);
+            if (cm > pmax) pmax = cm;
+            out += popc(km);
+            nx += popc(xm);
+        }
+        L = out;
+        return nx;
+    }
+
+    DEV void maintenance(int lo_mod) {
+        if (lo_mod < L) {
+            const int nx = compact_extract(lo_mod);
+            const int k0 = min(nx, kStage);
+            R x;
+            if (lane() < k0) ldr(S, lcap + lane(), x);
+            wsync();
+            add_entries(x, k0);
+            for (int b = kStage; b < nx && status == 0; b += kStage) {
+                const int kb = min(nx - b, kStage);
+                if (lane() < kb) x = from_rec(ovf[b - kStage + lane()]);
+                add_entries(x, kb);
+            }
+        }
+        if (status == 0) take_arrivals();
+    }
+
+    // ---------------------------------------------------------- driver
+
+    DEV void run() {
+        load_pf();
+        take_arrivals();
+        for (;;) {
+            if (status) break;
+            if (L == 0) {
+                if (spill_n > 0) {
+                    refill();
+                    if (status) break;
+                    if (L == 0) {
+                        fail(S_ESTATE);
+                        break;
+                    }
+                    continue;
+                }
+                if (next >= N) break;
+                int off = next - pf;
+                if (off >= kWave) {
+                    pf = next;
+                    load_pf();
+                    off = 0;
+                }
+                const int64_t an = rl64(pa, off);
+                idle += an - t;
+                t = an;
+                take_arrivals();
+                continue;
+            }
+            if (spill_n > 0 && nW < M) {
+                refill();
+                if (status) break;
+                if (spill_n > 0 && nW < M) {
+                    fail(S_ECAPACITY);
+                    break;
+                }
+            }
+            formation();
+            if (status) break;
+            if (cnt == 0) {
+                fail(S_ESTATE);
+                break;
+            }
+            if (U > maxU) maxU = U;
+            const int64_t dt = (int64_t)base + (int64_t)tok * used + sum_ctx / div;
+            const int64_t t_end = t + dt;
+            const int lo_mod = emission(t_end);
+            t = t_end;
+            iters++;
+            reqiters += cnt;
+            tokens += used;
+            if (iters > max_iters) {
+                fail(S_ELIVELOCK);
+                break;
+            }
+            maintenance(lo_mod);
+        }
+        finish();
+    }
+
+    DEV void finish() {
+        if (status == 0 && completed != N) fail(S_ESTATE);
+        if (status == 0) {
+            const size_t ioff = (size_t)inst * (size_t)N;
+            bool bad = false;
+            for (int b = 0; b < N; b += kWave) {
+                const int i = b + lane();
+                if (i < N) {
+                    const int64_t a = arr[i];
+                    const int64_t f = tfirst[i] - a, l = tlast[i] - a;
+                    if (f < 0 || f > 0xFFFFFFFFll || l < 0 || l > 0xFFFFFFFFll) bad = true;
+                    A.ttft[ioff + i] = (uint32_t)f;
+                    A.ttlt[ioff + i] = (uint32_t)l;
+                    A.tbtmax[ioff + i] = tbtw[i];
+                }
+            }
+            if (ballot(bad)) fail(S_EOVERFLOW);
+        }
+        if (lane() == 0) {
+            int64_t *cn = A.counters + (size_t)inst * 8;
+            cn[0] = iters, cn[1] = reqiters, cn[2] = tokens, cn[3] = ev_vol;
+            cn[4] = ev_forced, cn[5] = t, cn[6] = maxU, cn[7] = idle;
+            A.status[inst] = status;
+        }
+    }
+};
+
+__global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int inst = blockIdx.x;
+    if (inst >= a.n_inst) return;
+    const DevSetting &st = a.inst[inst];
+    switch (st.policy) {
+    case P_FCFS: {
+        Sim<P_FCFS> s(a, st, inst, smem);
+        s.run();
+        break;
+    }
+    case P_SRPT: {
+        Sim<P_SRPT> s(a, st, inst, smem);
+        s.run();
+        break;
+    }
+    default: {
+        Sim<P_BOOST> s(a, st, inst, smem);
+        s.run();
+        break;
+    }
+    }
+}
+
+}  // namespace
+}  // namespace tas
+
+int tas_launch_sim(const tas::SimArgs &a, int64_t lds_bytes, void *stream) {
+    if (a.n_inst <= 0) return 0;
+    hipStream_t s = (hipStream_t)stream;
+    if (lds_bytes > 65536) {
+        if (hipFuncSetAttribute((const void *)tas::sim_kernel,
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lds_bytes) != hipSuccess)
+            return -4;
+    }
+    hipLaunchKernelGGL(tas::sim_kernel, dim3((unsigned)a.n_inst), dim3(64), (size_t)lds_bytes, s,
+                       a);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}

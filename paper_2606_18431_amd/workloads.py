@@ -63,7 +63,7 @@ class Engine:
     iter_base_us: int = 5000
     iter_tok_us: int = 2
     iter_ctx_div: int = 100
-    max_iters: int = 1 << 40
+    max_iters: int = 4_000_000  # ends a runaway instance with a livelock error
     tau_us: float = 5000.0  # microseconds per token of boost (one decode step)
 
 

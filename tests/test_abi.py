@@ -1,0 +1,146 @@
+"""The C-ABI library on the host: it loads, exports every symbol that
+include/tas.h declares, builds the same boost tables as the oracle, and rejects
+invalid inputs before touching the GPU (no compute calls here)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_18431_amd import tas
+from paper_2606_18431_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "tas.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"\b(tas_[a-z_]+)\s*\(", src)
+    return sorted(set(names))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = tas.lib()
+    names = declared_functions()
+    assert len(names) == 13
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(tas.EXPORTS) <= set(names)
+
+
+def test_struct_layouts_match_header():
+    assert ctypes.sizeof(tas.tas_setting) == 232
+    assert ctypes.sizeof(tas.tas_params) == 72
+    assert ctypes.sizeof(tas.tas_traces) == 32
+
+
+@pytest.mark.parametrize("k", [1, 7, 16, 256])
+def test_boost_table_matches_oracle(k):
+    """Both sides evaluate the gamma-Boost curve on the host in fp64; the tables
+    (the only floating-point step of the path) agree bit for bit."""
+    for g in np.concatenate([np.geomspace(1e-6, 2.0, 60), 10.0 ** np.linspace(-5, -1, 31)]):
+        for tau in (5000.0, 1234.5):
+            assert np.array_equal(tas.tas_boost_table(g, k, tau), oracle.boost_table(g, k, tau))
+
+
+def test_boost_table_rejects():
+    for g, k, tau in [(0.0, 1, 5000.0), (-1.0, 1, 5000.0), (1e-3, 0, 5000.0), (1e-3, 1, 0.0),
+                      (float("nan"), 1, 5000.0), (float("inf"), 1, 5000.0)]:
+        with pytest.raises(tas.TasError):
+            tas.tas_boost_table(g, k, tau)
+
+
+def small():
+    return W.make(1, n_traces=2, n_settings=6, n_req=50)
+
+
+def create_rc(w, settings=None, engine=None, ws_bytes=None, **kw):
+    t, keep_t = tas.make_traces(w.arrival_us, w.prompt, w.decode)
+    p, keep_p = tas.make_params(engine or w.engine, w.settings if settings is None else settings,
+                                **kw)
+    need = tas.tas_workspace_bytes(t, p)
+    ctx = ctypes.c_void_p()
+    # a fake, aligned, non-null device address: every rejection below happens
+    # before the first HIP call, so it is never dereferenced
+    addr = 1 << 40
+    rc = tas.lib().tas_create(ctypes.byref(t), ctypes.byref(p), addr,
+                              need if ws_bytes is None else ws_bytes, ctypes.byref(ctx))
+    assert not ctx.value
+    return rc, need
+
+
+def test_workspace_bytes_and_nomem():
+    w = small()
+    rc, need = create_rc(w, ws_bytes=1)
+    assert need > 0 and rc == tas.TAS_ENOMEM
+
+
+def test_rejects_invalid_traces():
+    w = small()
+    bad = small()
+    bad.arrival_us[0, 5] = bad.arrival_us[0, 4] - 1  # unsorted
+    assert create_rc(bad)[0] == tas.TAS_EINVAL
+    bad = small()
+    bad.prompt[1, 3] = 0
+    assert create_rc(bad)[0] == tas.TAS_EINVAL
+    bad = small()
+    bad.decode[1, 3] = 0
+    assert create_rc(bad)[0] == tas.TAS_EINVAL
+    bad = small()
+    bad.arrival_us[0, 0] = -1
+    assert create_rc(bad)[0] == tas.TAS_EINVAL
+    bad = small()
+    bad.arrival_us[1, -1] = 1 << 41
+    assert create_rc(bad)[0] == tas.TAS_EINVAL
+    bad = small()
+    bad.prompt[0, 0], bad.decode[0, 0] = 1 << 23, 1 << 23
+    assert create_rc(bad)[0] == tas.TAS_EINVAL
+    assert w.n_req > 0
+
+
+def test_rejects_invalid_settings():
+    w = small()
+    cases = []
+    s = w.settings.copy(); s[0]["trace"] = 5; cases.append(s)
+    s = w.settings.copy(); s[0]["policy"] = 3; cases.append(s)
+    s = w.settings.copy(); s[0]["memguard"] = 1; cases.append(s)          # FCFS with MemGuard
+    s = w.settings.copy(); s[1]["delta_us"] = 10; cases.append(s)         # SRPT with delta
+    s = w.settings.copy(); s[2]["k"] = 0; cases.append(s)
+    s = w.settings.copy(); s[2]["delta_us"] = -1; cases.append(s)
+    s = w.settings.copy(); s[2]["gamma"] = 0.0; cases.append(s)
+    s = w.settings.copy(); s[2]["table_given"] = 1; s[2]["boost_us"][:] = np.arange(24); cases.append(s)
+    s = w.settings.copy(); s[2]["table_given"] = 1; s[2]["boost_us"][:] = -1; cases.append(s)
+    s = w.settings.copy(); s[2]["table_given"] = 1; s[2]["boost_us"][0] = (1 << 42) + 1; cases.append(s)
+    for s in cases:
+        assert create_rc(w, settings=s)[0] == tas.TAS_EINVAL
+
+
+def test_rejects_invalid_engine():
+    w = small()
+    for kw in (dict(max_seqs=0), dict(chunk=0), dict(chunk=10000, max_tokens=8192),
+               dict(kv_blocks=0), dict(block_tokens=0), dict(iter_base_us=0),
+               dict(iter_ctx_div=0), dict(max_iters=0), dict(tau_us=0.0)):
+        e = W.Engine(**{**W.Engine().__dict__, **kw})
+        assert create_rc(w, engine=e)[0] == tas.TAS_EINVAL
+        t, _ = tas.make_traces(w.arrival_us, w.prompt, w.decode)
+        p, _ = tas.make_params(e, w.settings)
+        assert tas.tas_workspace_bytes(t, p) == 0
+    # candidate list too small for the batch cap, or beyond the LDS limit
+    assert create_rc(w, list_cap=64)[0] == tas.TAS_EINVAL
+    assert create_rc(w, list_cap=1 << 16)[0] == tas.TAS_EINVAL
+
+
+def test_rejects_infeasible_request():
+    w = small()
+    w.prompt[0, 0] = 4000
+    w.decode[0, 0] = 4000
+    e = W.Engine(kv_blocks=400)  # 7999 tokens need 500 blocks
+    assert create_rc(w, engine=e)[0] == tas.TAS_EINFEASIBLE
+
+
+def test_strerror_covers_codes():
+    for code in range(-8, 1):
+        assert tas.tas_strerror(code) != "unknown error"

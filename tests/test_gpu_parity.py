@@ -1,0 +1,187 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Every comparison is element by element and exact: the whole path is integer
+arithmetic (the only floating-point step, the boost table, is checked equal
+on the host). Inputs are the seeded workloads; sizes span many 64-wide chunks
+and ragged tails, plus the degenerate cases.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_18431_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def gpu_run(w, **kw):
+    from paper_2606_18431_amd import tas
+
+    print(f"[gpu] {w.name} traces={w.n_traces} inst={w.n_inst} n_req={w.n_req} {kw}", flush=True)
+    sim = tas.Simulation(w, **kw)
+    sim.step()
+    out = sim.results()
+    out["tables"] = np.stack([sim.table(i) for i in range(w.n_inst)]) if w.n_inst else None
+    sim.close()
+    return out
+
+
+def assert_parity(w, g, o, inst=None):
+    inst = range(w.n_inst) if inst is None else inst
+    for i in inst:
+        assert g["status"][i] == o["status"][i] == 0, (i, g["status"][i], o["status"][i])
+        for key in ("ttft", "ttlt", "tbtmax"):
+            if not np.array_equal(g[key][i], o[key][i]):
+                bad = np.nonzero(g[key][i] != o[key][i])[0]
+                raise AssertionError(f"inst {i} {key}: {len(bad)} differ, first idx {bad[0]}: "
+                                     f"gpu {g[key][i][bad[0]]} oracle {o[key][i][bad[0]]}")
+        assert np.array_equal(g["counters"][i], o["counters"][i]), (i, g["counters"][i],
+                                                                    o["counters"][i])
+        assert np.array_equal(g["pct"][i], o["pct"][i]), (i, g["pct"][i], o["pct"][i])
+
+
+def test_boost_tables_equal(torch):
+    w = W.make(1, n_traces=1, n_settings=64, n_req=64)
+    g = gpu_run(w)
+    assert np.array_equal(g["tables"], oracle.tables(w.settings, w.engine.tau_us))
+
+
+GOLD = json.load(open(os.path.join(HERE, "golden", "hand_worked.json")))["cases"]
+
+
+@pytest.mark.parametrize("case", GOLD, ids=[c["name"] for c in GOLD])
+def test_hand_worked_on_gpu(torch, case):
+    e = W.Engine(**case["engine"])
+    tb = case.get("table")
+    s = W.setting(0, case["policy"], k=case.get("k", 1), memguard=case.get("memguard", 0),
+                  delta_us=case.get("delta_us", 0), table=tb if tb is not None else None)
+    w = W.Workload(case["name"], np.array([case["arrival"]], np.int64),
+                   np.array([case["prompt"]], np.int32), np.array([case["decode"]], np.int32),
+                   e, np.stack([s]))
+    g = gpu_run(w)
+    assert g["rc"] == 0
+    assert g["ttft"][0].tolist() == case["ttft"]
+    assert g["ttlt"][0].tolist() == case["ttlt"]
+    assert g["tbtmax"][0].tolist() == case["tbtmax"]
+    assert g["counters"][0].tolist() == case["counters"]
+
+
+@pytest.mark.parametrize("cfg,n_traces,n_settings,n_req", [
+    (0, 1, 8, 1000),      # the tiny workload, full size
+    (1, 2, 8, 3000),
+    (2, 2, 8, 3000),      # KV pressure: many evictions
+    (3, 2, 8, 5000),      # bursts and a length shift
+    (4, 1, 8, 6000),      # max_seqs 256, 16384-token budget
+])
+def test_parity_reduced_configs(torch, cfg, n_traces, n_settings, n_req):
+    w = W.make(cfg, n_traces=n_traces, n_settings=n_settings, n_req=n_req)
+    o = oracle.run(w)
+    assert o["rc"] == 0
+    g = gpu_run(w)
+    assert_parity(w, g, o)
+
+
+@pytest.mark.parametrize("cfg,list_cap", [(2, 128), (4, 320), (3, 128)])
+def test_parity_with_spill(torch, cfg, list_cap):
+    """A small on-chip list forces the HBM spill, refill and radix-select paths."""
+    w = W.make(cfg, n_traces=1, n_settings=8, n_req=4000)
+    o = oracle.run(w)
+    g = gpu_run(w, list_cap=list_cap)
+    assert_parity(w, g, o)
+
+
+def edge_workload(arrival, prompt, decode, engine, policies=None):
+    a = np.asarray(arrival, np.int64)[None]
+    p = np.asarray(prompt, np.int32)[None]
+    d = np.asarray(decode, np.int32)[None]
+    sets = policies or [W.setting(0, W.FCFS), W.setting(0, W.SRPT),
+                        W.setting(0, W.BOOST, gamma=1e-3, **W.UNIBOOST),
+                        W.setting(0, W.BOOST, gamma=1e-3, **W.VANILLA)]
+    return W.Workload("edge", a, p, d, engine, np.stack(sets))
+
+
+EDGES = {
+    "one_request": ([0], [5], [1], W.Engine()),
+    "two_requests_same_time": ([7, 7], [100, 3], [4, 9], W.Engine(max_seqs=1)),
+    "all_at_zero": (np.zeros(300), np.full(300, 40), np.arange(1, 301) % 17 + 1,
+                    W.Engine(max_seqs=16, kv_blocks=64, chunk=32, max_tokens=256)),
+    "all_decode_one": (np.arange(200) * 100, np.full(200, 33), np.ones(200),
+                       W.Engine(max_seqs=8, kv_blocks=40)),
+    "prompt_one": (np.arange(150) * 3000, np.ones(150), np.full(150, 20), W.Engine(max_seqs=4)),
+    "long_prompts_many_chunks": (np.arange(80) * 20000, np.full(80, 4000), np.full(80, 3),
+                                 W.Engine(max_seqs=4, chunk=512, max_tokens=1024, kv_blocks=600)),
+    "kv_exactly_one_request": (np.zeros(40), np.full(40, 16), np.full(40, 17),
+                               W.Engine(max_seqs=64, kv_blocks=2, block_tokens=16)),
+    "block_size_one": (np.arange(120) * 500, np.full(120, 7), np.full(120, 9),
+                       W.Engine(max_seqs=8, kv_blocks=60, block_tokens=1, chunk=5,
+                                max_tokens=12)),
+    "non_power_of_two_block": (np.arange(120) * 900, np.full(120, 50), np.full(120, 30),
+                               W.Engine(max_seqs=8, kv_blocks=40, block_tokens=12, chunk=40,
+                                        max_tokens=100)),
+    "idle_gaps": (np.array([0, 10 ** 9, 2 * 10 ** 9, 2 * 10 ** 9 + 1]), [10, 20, 30, 40],
+                  [3, 3, 3, 3], W.Engine()),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EDGES))
+def test_edge_cases(torch, name):
+    a, p, d, e = EDGES[name]
+    w = edge_workload(a, p, d, e)
+    o = oracle.run(w)
+    assert o["rc"] == 0
+    g = gpu_run(w)
+    assert_parity(w, g, o)
+
+
+def test_more_than_64_arrivals_at_once(torch):
+    a = np.concatenate([np.zeros(150), np.full(200, 50_000)])
+    w = edge_workload(a, np.full(350, 20), np.full(350, 5),
+                      W.Engine(max_seqs=32, kv_blocks=200, chunk=64, max_tokens=512))
+    o = oracle.run(w)
+    assert_parity(w, gpu_run(w), o)
+
+
+def test_error_livelock(torch):
+    w = edge_workload([0, 0], [16, 16], [50, 50], W.Engine(max_iters=10))
+    g = gpu_run(w)
+    assert g["rc"] == -6 and np.all(g["status"] == -6)
+
+
+def test_error_overflow(torch):
+    w = edge_workload([0], [1], [900_000], W.Engine(kv_blocks=1 << 20),
+                      policies=[W.setting(0, W.FCFS)])
+    g = gpu_run(w)
+    assert g["rc"] == -5
+
+
+def test_error_spill_capacity(torch):
+    """A spill too small to hold the waiting queue is reported, not hidden."""
+    w = W.make(2, n_traces=1, n_settings=4, n_req=3000)
+    g = gpu_run(w, list_cap=128, spill_cap=16)
+    assert g["rc"] == -8 and np.any(g["status"] == -8)
+
+
+def test_deterministic_and_order_independent(torch):
+    w = W.make(2, n_traces=2, n_settings=6, n_req=2500)
+    g1 = gpu_run(w)
+    g2 = gpu_run(w)
+    for key in ("ttft", "ttlt", "tbtmax", "counters", "pct"):
+        assert np.array_equal(g1[key], g2[key])
+    perm = np.random.default_rng(1).permutation(w.n_inst)
+    g3 = gpu_run(w.subset(perm))
+    for key in ("ttft", "ttlt", "tbtmax", "counters", "pct"):
+        assert np.array_equal(g3[key], g1[key][perm])
