@@ -102,7 +102,7 @@ typedef struct {
 typedef struct {
     int32_t max_seqs;      /* sequences per iteration, >= 1                    */
     int32_t max_tokens;    /* tokens per iteration, >= chunk                   */
-    int32_t chunk;         /* prefill chunk, >= 1                              */
+    int32_t chunk;         /* prefill chunk, 1 <= chunk <= 32767               */
     int32_t kv_blocks;     /* KV budget in blocks, >= 1                        */
     int32_t block_tokens;  /* tokens per KV block, >= 1                        */
     int32_t iter_base_us;  /* iteration cost: base + tok*sum(n)                */
@@ -110,8 +110,10 @@ typedef struct {
     int32_t iter_ctx_div;  /*   ctx_div >= 1                                   */
     int64_t max_iters;     /* per-instance iteration limit (TAS_ELIVELOCK)     */
     double tau_us;         /* microseconds per token of boost, > 0             */
-    int32_t list_cap;      /* on-chip candidate entries per instance; 0 picks
-                              a default from max_seqs                          */
+    int32_t list_cap;      /* on-chip candidate entries per instance, in
+                              [max_seqs + 64, 4032]; 0 picks max_seqs + 192
+                              rounded up to 64. More residents than this at
+                              once is TAS_ECAPACITY                            */
     int32_t spill_cap;     /* waiting entries per instance kept in HBM beyond
                               the on-chip list; 0 = n_req                      */
     int32_t n_inst;
@@ -134,7 +136,7 @@ size_t tas_workspace_bytes(const tas_traces *traces, const tas_params *params);
  * range; policy unknown; k < 1 (BOOST); delta < 0; memguard or delta nonzero
  * for FCFS/SRPT; gamma <= 0 without table_given (BOOST); an explicit table not
  * non-increasing or outside [0, 2^42]; chunk > max_tokens; any engine limit
- * < 1; tau <= 0; list_cap too small for max_seqs or above the LDS limit.
+ * < 1; chunk > 32767; tau <= 0; list_cap < max_seqs + 64 or > 4032.
  * TAS_EINFEASIBLE if ceil((P + D - 1) / block_tokens) > kv_blocks for some
  * request. TAS_ENOMEM if ws_bytes is too small. TAS_EHIP if a copy fails. */
 int tas_create(const tas_traces *traces, const tas_params *params, void *d_ws, size_t ws_bytes,

@@ -35,14 +35,17 @@ struct Layout {
         status, spill, ovf, total;
 };
 
+// Room for the residents (about max_seqs; more when the token budget pauses
+// many of them) plus a window of waiting entries.
 int32_t default_list_cap(int32_t max_seqs) {
-    int64_t lc = (int64_t)max_seqs + std::max<int64_t>(2 * (int64_t)max_seqs, 256);
+    int64_t lc = (int64_t)max_seqs + 192;
     lc = (lc + 63) / 64 * 64;
     return (int32_t)lc;
 }
 
 bool engine_ok(const tas_params *p) {
     return p->max_seqs >= 1 && p->max_tokens >= 1 && p->chunk >= 1 && p->chunk <= p->max_tokens &&
+           p->chunk <= tas::kMaxChunk &&
            p->kv_blocks >= 1 && p->block_tokens >= 1 && p->iter_base_us >= 1 &&
            p->iter_tok_us >= 0 && p->iter_ctx_div >= 1 && p->max_iters >= 1 &&
            p->tau_us > 0.0 && std::isfinite(p->tau_us) && p->n_inst >= 0 &&
@@ -57,7 +60,7 @@ bool shape_ok(const tas_traces *t) {
 // Effective capacities; false if invalid.
 bool caps(const tas_traces *t, const tas_params *p, int32_t *lc, int32_t *sc) {
     int32_t l = p->list_cap ? p->list_cap : default_list_cap(p->max_seqs);
-    if ((int64_t)l < (int64_t)p->max_seqs + 64) return false;
+    if ((int64_t)l < (int64_t)p->max_seqs + 64 || l > tas::kMaxListCap) return false;
     if (tas::lds_bytes_for(l) > kMaxLds) return false;
     int32_t s = p->spill_cap ? p->spill_cap : t->n_req;
     *lc = l;
@@ -82,7 +85,7 @@ bool layout(const tas_traces *t, const tas_params *p, int32_t lc, int32_t sc, La
     L->counters = o, o = align256(o + (size_t)p->n_inst * 8 * 8);
     L->status = o, o = align256(o + (size_t)p->n_inst * 4);
     L->spill = o, o = align256(o + (size_t)p->n_inst * (size_t)sc * sizeof(tas::Rec));
-    L->ovf = o, o = align256(o + (size_t)p->n_inst * (size_t)lc * sizeof(tas::Rec));
+    L->ovf = o, o = align256(o + (size_t)p->n_inst * (size_t)(lc + tas::kStage) * sizeof(tas::Rec));
     L->total = o;
     return true;
 }

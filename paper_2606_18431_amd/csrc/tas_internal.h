@@ -22,16 +22,15 @@ struct DevSetting {
 };
 
 // A candidate-list record as it is parked in HBM (spilled waiting entries and
-// the overflow of a large re-sort). 40 bytes.
+// the overflow of a large re-sort). 32 bytes.
 struct Rec {
     uint64_t pk;   // packed (key, idx)
-    int64_t tl;    // time of the last emitted token (absolute us)
     int32_t w;     // signal: prompt + emitted tokens
     int32_t left;  // tokens still to emit
     int32_t kv;    // tokens with resident KV
-    uint32_t gs;   // flags, guard and level (see the kernel)
+    uint32_t gs;   // flags, guard, level and this iteration's chunk (see the kernel)
     uint32_t tbt;  // max inter-token gap so far (us, saturating)
-    uint32_t pad;
+    uint32_t tl;   // time of the last emitted token, modulo 2^32 (us)
 };
 
 struct SimArgs {
@@ -48,7 +47,7 @@ struct SimArgs {
     int64_t *counters;       // [n_inst][8]
     int32_t *status;         // [n_inst]
     Rec *spill;              // [n_inst][spill_cap]
-    Rec *ovf;                // [n_inst][list_cap]
+    Rec *ovf;                // [n_inst][list_cap + 64]
     int64_t max_iters;
     int32_t n_req;
     int32_t n_inst;
@@ -59,11 +58,15 @@ struct SimArgs {
 
 // Dynamic LDS bytes per workgroup for a list capacity.
 inline int64_t lds_bytes_for(int32_t list_cap) {
-    const int64_t cap = int64_t(list_cap) + kStage;
-    // pk, tl (8 B) + w, left, kv, gs, tbt, nn (4 B) per slot; boost table;
+    const int64_t cap = int64_t(list_cap) + 2 * kStage;  // list, its overflow region, staging
+    // pk (8 B) + w, left, kv, gs, tbt, tl (4 B) per slot; boost table;
     // 256-bin histogram; a few scalars
-    return cap * (8 + 8 + 6 * 4) + kLevels * 8 + 256 * 4 + 64;
+    return cap * (8 + 6 * 4) + kLevels * 8 + 256 * 4 + 64;
 }
+constexpr int kMaxChunk = (1 << 15) - 1;  // the chunk size lives in 15 bits of the flag word
+// At most 64 chunks of 64 entries (list + overflow region): chunk bitmaps are
+// 64-bit and per-chunk masks live one chunk per lane.
+constexpr int kMaxListCap = 64 * 64 - kStage;
 
 }  // namespace tas
 

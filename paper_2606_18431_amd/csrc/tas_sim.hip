@@ -18,15 +18,16 @@
 // one instance and needs no workgroup barrier. The active requests live in
 // LDS as one array sorted by the packed key (key + 2^42) << 21 | idx, with
 // their state in structure-of-arrays form, so the batch-formation pass is a
-// sequence of 64-wide chunks with wavefront prefix sums (token budget, KV
-// blocks, sequence count) and a ballot to find the first candidate that does
-// not fit; only that candidate takes the sequential eviction path. Keys of
+// sequence of 64-wide chunks with DPP prefix sums (token budget, KV blocks,
+// sequence count) and a ballot to find the first candidate that does not
+// fit; only that candidate takes the sequential eviction path. Keys of
 // waiting requests never change (MemGuard recomputes a key only when the
 // quantized signal moves, Phase 3), so the list is repaired incrementally:
-// finished entries are compacted out, entries whose key moved are extracted
-// and merged back. Waiting requests beyond the on-chip capacity spill to HBM
-// with the invariant that every spilled key exceeds every waiting key on
-// chip; a radix select over the spill refills the list.
+// finished entries stay behind as holes until a compaction pass, entries whose
+// key moved are extracted and merged back. Waiting requests beyond the
+// on-chip capacity spill to HBM with the invariant that every spilled key
+// exceeds every waiting key on chip; a radix select over the spill refills
+// the list.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -43,11 +44,14 @@ constexpr uint32_t G_RES = 1u << 5;      // resident: holds KV
 constexpr uint32_t G_FIRST = 1u << 6;    // first token emitted
 constexpr uint32_t G_INB = 1u << 7;      // in this iteration's batch
 constexpr uint32_t G_EVI = 1u << 8;      // evicted during this iteration
-constexpr uint32_t G_DONE = 1u << 9;     // completed
+constexpr uint32_t G_DONE = 1u << 9;     // completed: a hole until compaction
 constexpr uint32_t G_DIRTY = 1u << 10;   // key moved: re-insert
 constexpr uint32_t G_MARK = 1u << 11;    // selected for spilling
 constexpr int G_LVL_SHIFT = 12;          // current MemGuard level (5 bits)
 constexpr uint32_t G_LVL = 0x1fu << G_LVL_SHIFT;
+constexpr int G_N_SHIFT = 17;            // tokens scheduled this iteration (15 bits)
+constexpr uint32_t G_LOW = (1u << G_N_SHIFT) - 1;
+constexpr int kHoleLimit = 16;           // compact once this many holes accumulate
 
 enum { S_OK = 0, S_EOVERFLOW = -5, S_ELIVELOCK = -6, S_ESTATE = -7, S_ECAPACITY = -8 };
 enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2 };
@@ -57,6 +61,8 @@ enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2 };
 DEV int lane() { return (int)__lane_id(); }
 DEV uint64_t ballot(bool p) { return (uint64_t)__ballot(p); }
 DEV int popc(uint64_t m) { return __popcll(m); }
+DEV int ffs0(uint64_t m) { return __ffsll((unsigned long long)m) - 1; }
+DEV int fls0(uint64_t m) { return 63 - __clzll((unsigned long long)m); }
 DEV int mbcnt(uint64_t m) {
     return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
                                           __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
@@ -70,52 +76,73 @@ DEV uint64_t rlu(uint64_t x, int l) {
 }
 DEV int64_t rl64(int64_t x, int l) { return (int64_t)rlu((uint64_t)x, l); }
 DEV uint64_t uniu(uint64_t x) { return rlu(x, __builtin_amdgcn_readfirstlane(lane())); }
-DEV void wsync() { __syncthreads(); }
+// One wavefront is the whole workgroup and its LDS operations execute in
+// issue order, so ordering LDS traffic between lanes only needs the compiler
+// not to move memory operations across this point.
+DEV void wsync() { __asm__ volatile("" ::: "memory"); }
+// Before reading back HBM this wavefront wrote (spill, overflow, timestamps).
+DEV void hbm_fence() { __builtin_amdgcn_s_waitcnt(0); __asm__ volatile("" ::: "memory"); }
 
+// DPP lane moves (GFX9 encodings): row_shr:n shifts within 16-lane rows,
+// row_bcast:15 / :31 carry a row's last lane into the next row(s), wave_shr:1
+// shifts across the whole wavefront. Disabled or out-of-range lanes take `old`.
+constexpr int kShr1 = 0x111, kShr2 = 0x112, kShr4 = 0x114, kShr8 = 0x118;
+constexpr int kBc15 = 0x142, kBc31 = 0x143, kWShr1 = 0x138;
+
+template <int CTRL, int RM = 0xf>
+DEV int dpp(int old, int x) {
+    return __builtin_amdgcn_update_dpp(old, x, CTRL, RM, 0xf, false);
+}
+template <int CTRL, int RM = 0xf>
+DEV uint64_t dppu(uint64_t old, uint64_t x) {
+    const uint32_t lo = (uint32_t)dpp<CTRL, RM>((int)(uint32_t)old, (int)(uint32_t)x);
+    const uint32_t hi = (uint32_t)dpp<CTRL, RM>((int)(uint32_t)(old >> 32), (int)(uint32_t)(x >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// inclusive prefix sum over the wavefront
 DEV int scan_add(int x) {
-    const int l = lane();
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        int y = __shfl_up(x, o);
-        if (l >= o) x += y;
-    }
+    x += dpp<kShr1>(0, x);
+    x += dpp<kShr2>(0, x);
+    x += dpp<kShr4>(0, x);
+    x += dpp<kShr8>(0, x);
+    x += dpp<kBc15, 0xa>(0, x);
+    x += dpp<kBc31, 0xc>(0, x);
     return x;
 }
-DEV int wsum(int x) {
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) x += __shfl_xor(x, o);
-    return uni(x);
-}
+DEV int wsum(int x) { return rl(scan_add(x), 63); }
 DEV int wmin(int x) {
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) x = min(x, __shfl_xor(x, o));
-    return uni(x);
-}
-DEV uint64_t wmaxu(uint64_t x) {
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) {
-        uint64_t y = (uint64_t)__shfl_xor((unsigned long long)x, o);
-        x = y > x ? y : x;
-    }
-    return uniu(x);
-}
-DEV uint64_t wminu(uint64_t x) {
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) {
-        uint64_t y = (uint64_t)__shfl_xor((unsigned long long)x, o);
-        x = y < x ? y : x;
-    }
-    return uniu(x);
+    x = min(x, dpp<kShr1>(INT32_MAX, x));
+    x = min(x, dpp<kShr2>(INT32_MAX, x));
+    x = min(x, dpp<kShr4>(INT32_MAX, x));
+    x = min(x, dpp<kShr8>(INT32_MAX, x));
+    x = min(x, dpp<kBc15, 0xa>(INT32_MAX, x));
+    x = min(x, dpp<kBc31, 0xc>(INT32_MAX, x));
+    return rl(x, 63);
 }
 DEV uint64_t scan_maxu(uint64_t x) {
-    const int l = lane();
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        uint64_t y = (uint64_t)__shfl_up((unsigned long long)x, o);
-        if (l >= o && y > x) x = y;
-    }
+    uint64_t y;
+    y = dppu<kShr1>(0ull, x), x = y > x ? y : x;
+    y = dppu<kShr2>(0ull, x), x = y > x ? y : x;
+    y = dppu<kShr4>(0ull, x), x = y > x ? y : x;
+    y = dppu<kShr8>(0ull, x), x = y > x ? y : x;
+    y = dppu<kBc15, 0xa>(0ull, x), x = y > x ? y : x;
+    y = dppu<kBc31, 0xc>(0ull, x), x = y > x ? y : x;
     return x;
 }
+DEV uint64_t scan_minu(uint64_t x) {
+    uint64_t y;
+    y = dppu<kShr1>(~0ull, x), x = y < x ? y : x;
+    y = dppu<kShr2>(~0ull, x), x = y < x ? y : x;
+    y = dppu<kShr4>(~0ull, x), x = y < x ? y : x;
+    y = dppu<kShr8>(~0ull, x), x = y < x ? y : x;
+    y = dppu<kBc15, 0xa>(~0ull, x), x = y < x ? y : x;
+    y = dppu<kBc31, 0xc>(~0ull, x), x = y < x ? y : x;
+    return x;
+}
+DEV uint64_t wminu(uint64_t x) { return rlu(scan_minu(x), 63); }
+// the value of the previous lane (lane 0 gets `fill`)
+DEV uint64_t prev_lane_u64(uint64_t x, uint64_t fill) { return dppu<kWShr1>(fill, x); }
 
 // ------------------------------------------------------------ keys
 
@@ -130,8 +157,8 @@ DEV int idx_of(uint64_t pk) { return (int)(pk & kIdxMask); }
 // e - 1 otherwise (Eq. memguard_level).
 DEV int level_of(int w, int k, int lk) {
     if (w < k) return 0;
-    int e = (31 - __clz(w)) - lk;
-    int L = ((w >> e) >= k) ? e : e - 1;
+    const int e = (31 - __clz(w)) - lk;
+    const int L = ((w >> e) >= k) ? e : e - 1;
     return L < kLevels - 1 ? L : kLevels - 1;
 }
 
@@ -139,59 +166,57 @@ DEV int level_of(int w, int k, int lk) {
 
 struct Lds {
     uint64_t *pk;
-    int64_t *tl;
     int64_t *bt;
-    int32_t *w, *left, *kv, *nn;
-    uint32_t *gs, *tbt, *hist;
+    int32_t *w, *left, *kv;
+    uint32_t *gs, *tbt, *tl, *hist;
 };
 
 struct R {  // one candidate-list record in registers
     uint64_t pk = 0;
-    int64_t tl = 0;
     int w = 0, left = 0, kv = 0;
-    uint32_t gs = 0, tbt = 0;
+    uint32_t gs = 0, tbt = 0, tl = 0;
 };
 
 DEV void ldr(const Lds &S, int i, R &x) {
     x.pk = S.pk[i];
-    x.tl = S.tl[i];
     x.w = S.w[i];
     x.left = S.left[i];
     x.kv = S.kv[i];
     x.gs = S.gs[i];
     x.tbt = S.tbt[i];
+    x.tl = S.tl[i];
 }
 DEV void str(const Lds &S, int i, const R &x) {
     S.pk[i] = x.pk;
-    S.tl[i] = x.tl;
     S.w[i] = x.w;
     S.left[i] = x.left;
     S.kv[i] = x.kv;
     S.gs[i] = x.gs;
     S.tbt[i] = x.tbt;
+    S.tl[i] = x.tl;
 }
 DEV R from_rec(const Rec &r) {
     R x;
-    x.pk = r.pk, x.tl = r.tl, x.w = r.w, x.left = r.left, x.kv = r.kv, x.gs = r.gs, x.tbt = r.tbt;
+    x.pk = r.pk, x.w = r.w, x.left = r.left, x.kv = r.kv, x.gs = r.gs, x.tbt = r.tbt, x.tl = r.tl;
     return x;
 }
 DEV Rec to_rec(const R &x) {
     Rec r;
-    r.pk = x.pk, r.tl = x.tl, r.w = x.w, r.left = x.left, r.kv = x.kv, r.gs = x.gs, r.tbt = x.tbt;
-    r.pad = 0;
+    r.pk = x.pk, r.w = x.w, r.left = x.left, r.kv = x.kv, r.gs = x.gs, r.tbt = x.tbt, r.tl = x.tl;
     return r;
 }
 DEV R shfl_rec(const R &x, int src) {
     R y;
     y.pk = (uint64_t)__shfl((unsigned long long)x.pk, src);
-    y.tl = (int64_t)__shfl((long long)x.tl, src);
     y.w = __shfl(x.w, src);
     y.left = __shfl(x.left, src);
     y.kv = __shfl(x.kv, src);
     y.gs = (uint32_t)__shfl((int)x.gs, src);
     y.tbt = (uint32_t)__shfl((int)x.tbt, src);
+    y.tl = (uint32_t)__shfl((int)x.tl, src);
     return y;
 }
+DEV bool is_waiting(uint32_t g) { return (g & (G_RES | G_DONE)) == 0; }
 
 // ------------------------------------------------------------ the simulator
 
@@ -201,6 +226,7 @@ struct Sim {
     Lds S;
     // instance constants
     int inst, N, M, T, c, Kb, bs, bs_shift, base, tok, div, k, lk, memguard, lcap, scap;
+    int sb;  // first staging slot: the list may use [0, lcap + kStage) during formation
     int64_t delta, max_iters;
     const int64_t *arr;
     const int32_t *Pp, *Dp;
@@ -209,14 +235,20 @@ struct Sim {
     Rec *spill, *ovf;
     // state
     int64_t t;
-    int U, L, nW, spill_n, next, pf, completed, status;
+    int U, L, nW, nR, n_holes, lo_hole, spill_n, next, pf, completed, status;
     uint64_t spill_min;
     int64_t pa;
     int pP, pD;
     int64_t iters, reqiters, tokens, ev_vol, ev_forced, maxU, idle;
     // per-iteration formation results
-    int cnt, used, hi;
+    int cnt, used;
     int64_t sum_ctx;
+    uint64_t emit_chunks;  // 64-entry chunks holding batch members or evictions
+    bool emit_all;         // ranks moved during formation: visit every chunk
+    // victim masks, lane c = chunk c: residents outside the batch, and those a
+    // voluntary eviction may take (MemGuard); valid for chunks >= vm_from
+    uint64_t vm_res, vm_ev;
+    int vm_from;
 
     DEV Sim(const SimArgs &a, const DevSetting &st, int i, unsigned char *smem) : A(a) {
         inst = i;
@@ -233,26 +265,31 @@ struct Sim {
         const size_t ioff = (size_t)i * (size_t)N;
         tfirst = a.tfirst + ioff, tlast = a.tlast + ioff, tbtw = a.tbtw + ioff;
         spill = a.spill + (size_t)i * (size_t)scap;
-        ovf = a.ovf + (size_t)i * (size_t)lcap;
-        const int cap = lcap + kStage;
+        ovf = a.ovf + (size_t)i * (size_t)(lcap + kStage);
+        sb = lcap + kStage;
+        const int cap = lcap + 2 * kStage;
         size_t o = 0;
         S.pk = (uint64_t *)(smem + o), o += (size_t)cap * 8;
-        S.tl = (int64_t *)(smem + o), o += (size_t)cap * 8;
         S.bt = (int64_t *)(smem + o), o += kLevels * 8;
         S.w = (int32_t *)(smem + o), o += (size_t)cap * 4;
         S.left = (int32_t *)(smem + o), o += (size_t)cap * 4;
         S.kv = (int32_t *)(smem + o), o += (size_t)cap * 4;
-        S.nn = (int32_t *)(smem + o), o += (size_t)cap * 4;
         S.gs = (uint32_t *)(smem + o), o += (size_t)cap * 4;
         S.tbt = (uint32_t *)(smem + o), o += (size_t)cap * 4;
+        S.tl = (uint32_t *)(smem + o), o += (size_t)cap * 4;
         S.hist = (uint32_t *)(smem + o);
         for (int j = lane(); j < kLevels; j += kWave) S.bt[j] = st.bt[j];
         t = 0;
-        U = L = nW = spill_n = next = pf = completed = status = 0;
+        U = L = nW = nR = n_holes = spill_n = next = pf = completed = status = 0;
+        lo_hole = INT32_MAX;
         spill_min = ~0ull;
         iters = reqiters = tokens = ev_vol = ev_forced = maxU = idle = 0;
-        cnt = used = hi = 0;
+        cnt = used = 0;
         sum_ctx = 0;
+        emit_chunks = 0;
+        emit_all = false;
+        vm_res = vm_ev = 0;
+        vm_from = INT32_MAX;
         wsync();
     }
 
@@ -274,7 +311,7 @@ struct Sim {
 
     DEV R new_record(int idx, int64_t a, int P, int D) const {
         R x;
-        x.w = P, x.left = D, x.kv = 0, x.tl = 0, x.tbt = 0;
+        x.w = P, x.left = D;
         int64_t key;
         uint32_t lvl = 0;
         if (POL == P_FCFS) {
@@ -303,8 +340,8 @@ struct Sim {
             const bool arrive = lane() >= off && r < N && pa <= t;
             const int n_arr = popc(ballot(arrive));
             if (n_arr == 0) return;
-            R x = new_record(r, pa, pP, pD);
-            R y = shfl_rec(x, min(off + lane(), kWave - 1));
+            const R x = new_record(r, pa, pP, pD);
+            const R y = off ? shfl_rec(x, min(off + lane(), kWave - 1)) : x;
             nW += n_arr;
             next += n_arr;
             add_entries(y, n_arr);
@@ -314,53 +351,64 @@ struct Sim {
 
     // ---------------------------------------------------------- list edits
 
+    // Number of list entries with pk < x (x wave-uniform): the last key of
+    // every 64-entry chunk, then one chunk. Requires L <= 64 * 64.
+    DEV int lower_bound(uint64_t x) const {
+        if (L == 0) return 0;
+        const int nch = (L + kWave - 1) >> 6;
+        const int probe = min(lane() * kWave + kWave - 1, L - 1);
+        const uint64_t cm = lane() < nch ? S.pk[probe] : ~0ull;
+        const int c0 = popc(ballot(lane() < nch && cm < x));
+        if (c0 >= nch) return L;
+        const int r = c0 * kWave + lane();
+        const uint64_t v = r < L ? S.pk[r] : ~0ull;
+        return c0 * kWave + popc(ballot(r < L && v < x));
+    }
+
     // Merge K records held by lanes [0, K) into the sorted list.
-    // Requires L + K <= lcap + kStage.
+    // Requires L + K <= lcap + kStage (the list's overflow region).
     DEV void merge_new(const R &x, int K) {
         if (K <= 0) return;
         const bool act = lane() < K;
-        int lo = 0, hi_ = L;
-        if (act) {
-            for (int s = 0; s < 32 && lo < hi_; s++) {
-                int mid = (lo + hi_) >> 1;
-                if (S.pk[mid] < x.pk) lo = mid + 1;
-                else hi_ = mid;
-            }
-        }
-        const int pos = lo;
         int rn = 0;
-        for (int j = 0; j < K; j++) {
-            uint64_t y = rlu(x.pk, j);
-            rn += (act && y < x.pk) ? 1 : 0;
-        }
-        const int minpos = wmin(act ? pos : INT32_MAX);
-        if (L > 0) {
+        for (int j = 0; j < K; j++) rn += (act && rlu(x.pk, j) < x.pk) ? 1 : 0;
+        const uint64_t xmin = wminu(act ? x.pk : ~0ull);
+        const int minpos = lower_bound(xmin);
+        int pos_in = 0;  // lane j < K: list entries at ranks >= minpos smaller than x_j
+        if (minpos < L) {
             for (int b = ((L - 1) >> 6) << 6; b >= 0 && b + kWave > minpos; b -= kWave) {
                 const int r = b + lane();
                 const bool mv = r >= minpos && r < L;
-                R y;
-                if (mv) ldr(S, r, y);
+                const uint64_t pr = mv ? S.pk[r] : ~0ull;
                 int sh = 0;
-                for (int j = 0; j < K; j++) sh += (rl(pos, j) <= r) ? 1 : 0;
+                for (int j = 0; j < K; j++) {
+                    const uint64_t xj = rlu(x.pk, j);
+                    sh += (mv && xj < pr) ? 1 : 0;
+                    const int cj = popc(ballot(mv && pr < xj));
+                    if (lane() == j) pos_in += cj;
+                }
+                const bool go = mv && sh > 0;
+                R y;
+                if (go) ldr(S, r, y);
                 wsync();
-                if (mv && sh) str(S, r + sh, y);
+                if (go) str(S, r + sh, y);
                 wsync();
             }
         }
-        if (act) str(S, pos + rn, x);
+        if (act) str(S, minpos + pos_in + rn, x);
         wsync();
         L += K;
     }
 
-    // Remove marked entries at ranks >= from (stable).
-    DEV void compact_marked(int from) {
+    // Remove the entries whose flags intersect `mask`, from rank `from` on.
+    DEV void compact_remove(int from, uint32_t mask) {
         int out = from;
         for (int b = (from >> 6) << 6; b < L; b += kWave) {
             const int r = b + lane();
             const bool v = r >= from && r < L;
             R y;
             if (v) ldr(S, r, y);
-            const bool keep = v && !(y.gs & G_MARK);
+            const bool keep = v && !(y.gs & mask);
             const uint64_t km = ballot(keep);
             wsync();
             if (keep) {
@@ -373,8 +421,18 @@ struct Sim {
         L = out;
     }
 
-    // Spill the L - lcap largest waiting entries to HBM.
+    DEV void drop_holes() {
+        if (n_holes == 0) return;
+        compact_remove(lo_hole, G_DONE);
+        n_holes = 0;
+        lo_hole = INT32_MAX;
+    }
+
+    // Keep at most lcap entries: drop holes, then spill the largest waiting
+    // entries to HBM.
     DEV void spill_excess() {
+        if (L <= lcap) return;
+        drop_holes();
         const int E = L - lcap;
         if (E <= 0) return;
         if (spill_n + E > scap) {
@@ -384,7 +442,7 @@ struct Sim {
         int found = 0, lowest = L;
         for (int b = ((L - 1) >> 6) << 6; b >= 0 && found < E; b -= kWave) {
             const int r = b + lane();
-            const bool isw = r < L && !(S.gs[r] & G_RES);
+            const bool isw = r < L && is_waiting(S.gs[r]);
             const uint64_t m = ballot(isw);
             const int above = popc(m) - mbcnt(m) - 1;
             const bool take = isw && above < E - found;
@@ -396,7 +454,7 @@ struct Sim {
             }
             const uint64_t tm = ballot(take);
             found += popc(tm);
-            if (tm) lowest = b + (__ffsll((unsigned long long)tm) - 1);
+            if (tm) lowest = b + ffs0(tm);
         }
         wsync();
         if (found < E) {
@@ -407,14 +465,14 @@ struct Sim {
         spill_min = (spill_n == 0 || mn < spill_min) ? mn : spill_min;
         spill_n += E;
         nW -= E;
-        compact_marked(lowest);
+        compact_remove(lowest, G_MARK);
     }
 
     // Add K records (lanes [0, K)) to the list; waiting ones whose key exceeds
     // the spill's minimum go straight to the spill. L <= lcap on entry.
     DEV void add_entries(R y, int K) {
         if (spill_n > 0) {
-            const bool toS = lane() < K && !(y.gs & G_RES) && y.pk > spill_min;
+            const bool toS = lane() < K && is_waiting(y.gs) && y.pk > spill_min;
             const uint64_t sm = ballot(toS);
             const int ns = popc(sm);
             if (ns) {
@@ -426,10 +484,10 @@ struct Sim {
                 spill_n += ns;
                 nW -= ns;
                 const uint64_t km = ballot(lane() < K && !toS);
-                if (lane() < K && !toS) str(S, lcap + mbcnt(km), y);
+                if (lane() < K && !toS) str(S, sb + mbcnt(km), y);
                 wsync();
                 K -= ns;
-                if (lane() < K) ldr(S, lcap + lane(), y);
+                if (lane() < K) ldr(S, sb + lane(), y);
                 wsync();
             }
         }
@@ -439,6 +497,7 @@ struct Sim {
 
     // The want-th smallest spilled key (radix select, 8 bits per pass).
     DEV uint64_t select_kth(int want) {
+        hbm_fence();
         uint64_t prefix = 0;
         int rank = want;
         for (int d = 7; d >= 0; d--) {
@@ -465,7 +524,7 @@ struct Sim {
                 fail(S_ESTATE);
                 return 0;
             }
-            const int ln = __ffsll((unsigned long long)hm) - 1;
+            const int ln = ffs0(hm);
             int rr = rank - rl(exc, ln);
             const int b0 = rl(h0, ln), b1 = rl(h1, ln), b2 = rl(h2, ln);
             int bin = 4 * ln;
@@ -483,13 +542,18 @@ struct Sim {
         return prefix;
     }
 
-    // Bring the smallest spilled entries back on chip.
+    // Bring the smallest spilled entries back on chip (as many as fit).
     DEV void refill() {
-        const int room = lcap - L;
+        drop_holes();
+        refill_into(lcap - L);
+    }
+
+    DEV void refill_into(int room) {
         const int want = min(spill_n, room);
         if (want <= 0) return;
         const uint64_t theta = want < spill_n ? select_kth(want) : ~0ull;
         if (status) return;
+        hbm_fence();
         int wr = 0, got = 0;
         uint64_t newmin = ~0ull;
         const int n0 = spill_n;
@@ -509,10 +573,10 @@ struct Sim {
             wr += popc(km);
             const int ks = popc(sm);
             if (ks) {
-                if (sel) str(S, lcap + mbcnt(sm), from_rec(s));
+                if (sel) str(S, sb + mbcnt(sm), from_rec(s));
                 wsync();
                 R x;
-                if (lane() < ks) ldr(S, lcap + lane(), x);
+                if (lane() < ks) ldr(S, sb + lane(), x);
                 wsync();
                 merge_new(x, ks);
                 got += ks;
@@ -526,30 +590,47 @@ struct Sim {
 
     // ---------------------------------------------------------- formation
 
+    // Victim masks for chunks [c0, nch): one LDS read and two ballots per
+    // chunk, kept one chunk per lane.
+    DEV void build_victim_masks(int c0) {
+        const int nch = (L + kWave - 1) >> 6;
+        for (int c = c0; c < nch && c < vm_from; c++) {
+            const int r = c * kWave + lane();
+            const uint32_t g = r < L ? S.gs[r] : 0u;
+            const bool rs = (g & G_RES) && !(g & G_INB);
+            bool ev = rs;
+            if (POL == P_BOOST && memguard) ev = rs && ((g >> G_LVL_SHIFT) & 31u) > (g & G_GUARD);
+            const uint64_t m1 = ballot(rs), m2 = ballot(ev);
+            if (lane() == c) vm_res = m1, vm_ev = m2;
+        }
+        vm_from = min(vm_from, c0);
+    }
+
+    // Highest rank > q set in the per-chunk mask vm, or -1.
+    DEV int top_above(uint64_t vm, int q) const {
+        const int qc = q >> 6, qb = q & 63;
+        uint64_t m = vm;
+        if (lane() < qc) m = 0;
+        else if (lane() == qc) m &= qb == 63 ? 0ull : (~0ull << (qb + 1));
+        const uint64_t nz = ballot(m != 0);
+        if (!nz) return -1;
+        const int ch = fls0(nz);
+        return ch * kWave + fls0(rlu(m, ch));
+    }
+
     // Highest rank > q holding a resident outside the batch that may be
     // evicted for candidate q (voluntary: MemGuard and hysteresis apply).
+    // The list is sorted, so the highest such rank is the worst (key, idx).
     DEV int find_victim(int q, uint64_t pkq, bool voluntary) {
-        const int64_t keyq = key_of(pkq);
-        const int idxq = idx_of(pkq);
-        for (int b = ((L - 1) >> 6) << 6; b >= 0 && b + kWave - 1 > q; b -= kWave) {
-            const int r = b + lane();
-            bool e = false;
-            if (r > q && r < L) {
-                const uint32_t g = S.gs[r];
-                e = (g & G_RES) && !(g & G_INB);
-                if (POL == P_BOOST && voluntary && e) {
-                    if (memguard) e = ((g >> G_LVL_SHIFT) & 31u) > (g & G_GUARD);
-                    if (e && delta > 0) {
-                        const uint64_t pv = S.pk[r];
-                        const int64_t kd = key_of(pv) - delta;
-                        e = kd > keyq || (kd == keyq && idx_of(pv) > idxq);
-                    }
-                }
-            }
-            const uint64_t m = ballot(e);
-            if (m) return b + 63 - __clzll((unsigned long long)m);
+        if (vm_from > (q >> 6)) build_victim_masks(q >> 6);
+        const int v = top_above(voluntary ? vm_ev : vm_res, q);
+        if (POL == P_BOOST && voluntary && v >= 0 && delta > 0) {
+            // the worst eligible key fails the hysteresis test => all fail
+            const uint64_t pv = uniu(S.pk[v]);
+            const int64_t kd = key_of(pv) - delta, kq = key_of(pkq);
+            if (!(kd > kq || (kd == kq && idx_of(pv) > idx_of(pkq)))) return -1;
         }
-        return -1;
+        return v;
     }
 
     DEV void do_evict(int v) {
@@ -563,14 +644,18 @@ struct Sim {
         wsync();
         U -= blocks(kvv);
         nW++;
-        hi = max(hi, v + 1);
+        nR--;
+        emit_chunks |= 1ull << (v >> 6);
+        if ((v >> 6) >= vm_from && lane() == (v >> 6)) {
+            vm_res &= ~(1ull << (v & 63));
+            vm_ev &= ~(1ull << (v & 63));
+        }
     }
 
     DEV void admit_one(int q, uint32_t g, int n, int du, int kvv) {
         const bool res = (g & G_RES) != 0;
         if (lane() == 0) {
-            S.nn[q] = n;
-            uint32_t g2 = g | G_INB;
+            uint32_t g2 = (g & G_LOW) | G_INB | ((uint32_t)n << G_N_SHIFT);
             if (!res) g2 = (g2 & ~G_GUARD) | G_RES | ((g >> G_LVL_SHIFT) & 31u);
             S.gs[q] = g2;
         }
@@ -579,11 +664,13 @@ struct Sim {
         used += n;
         U += du;
         sum_ctx += kvv + n;
-        if (!res) nW--;
+        if (!res) nW--, nR++;
+        emit_chunks |= 1ull << (q >> 6);
     }
 
-    // Candidate q did not fit: evictions, or closing admissions.
-    DEV void slow_path(int q, bool &closed) {
+    // Candidate q did not fit: evictions, or closing admissions. r_ahead
+    // counts residents at ranks > q.
+    DEV void slow_path(int q, bool &closed, int &r_ahead) {
         const uint32_t g = (uint32_t)uni((int)S.gs[q]);
         const int w = uni(S.w[q]);
         const int kvv = uni(S.kv[q]);
@@ -599,6 +686,7 @@ struct Sim {
             int v = find_victim(q, pkq, true);
             if (v >= 0) {
                 do_evict(v);
+                r_ahead--;
                 ev_vol++;
                 continue;
             }
@@ -606,6 +694,7 @@ struct Sim {
                 v = find_victim(q, pkq, false);
                 if (v >= 0) {
                     do_evict(v);
+                    r_ahead--;
                     ev_forced++;
                     continue;
                 }
@@ -619,19 +708,57 @@ struct Sim {
         fail(S_ESTATE);
     }
 
+    // Spilled entries come next in the candidate order (formation reached
+    // the first on-chip key above the spill's minimum with admissions open):
+    // bring the smallest of them on chip. Every entry below rank p has been
+    // processed and keeps its rank; every on-chip waiting key is below p.
+    DEV void mid_refill(int p) {
+        if (n_holes > 0) {
+            const int from = max(p, lo_hole);
+            const int L0 = L;
+            compact_remove(from, G_DONE);
+            n_holes -= L0 - L;
+            if (n_holes == 0) lo_hole = INT32_MAX;
+        }
+        const int room = lcap + kStage - L;  // may use the overflow region
+        if (room <= 0) {
+            fail(S_ECAPACITY);
+            return;
+        }
+        refill_into(room);
+        vm_from = INT32_MAX;  // ranks moved: rebuild the victim masks on demand
+        vm_res = vm_ev = 0;
+        emit_all = true;
+    }
+
     DEV void formation() {
-        cnt = 0, used = 0, hi = 0;
+        cnt = 0, used = 0;
         sum_ctx = 0;
+        emit_chunks = 0;
+        emit_all = false;
+        vm_from = INT32_MAX;
+        vm_res = vm_ev = 0;
         bool closed = false;
+        int r_ahead = nR;  // residents at ranks >= p
         int p = 0;
-        for (int guard = 0; guard <= 2 * L + 2 && p < L && cnt < M && used < T; guard++) {
+        int bstar = spill_n > 0 ? lower_bound(spill_min) : INT32_MAX;
+        for (int guard = 0; guard < (1 << 22); guard++) {
+            if (cnt >= M || used >= T || (closed && r_ahead <= 0)) break;
+            if (!closed && p >= bstar) {  // bstar <= L: spilled entries come next
+                mid_refill(p);
+                if (status) return;
+                bstar = spill_n > 0 ? lower_bound(spill_min) : INT32_MAX;
+                continue;
+            }
+            if (p >= L) break;
+            const int end = closed ? L : min(L, bstar);
             const int r = p + lane();
-            const bool valid = r < L;
+            const bool valid = r < end;
             const uint32_t g = valid ? S.gs[r] : 0u;
             const int w = valid ? S.w[r] : 0;
             const int kvv = valid ? S.kv[r] : 0;
             const bool res = (g & G_RES) != 0;
-            const bool cand = valid && !(g & G_EVI) && (res || !closed);
+            const bool cand = valid && !(g & (G_EVI | G_DONE)) && (res || !closed);
             const int m = cand ? min(w - kvv, c) : 0;
             const int ci = scan_add(cand ? 1 : 0);
             const int mi = scan_add(m);
@@ -641,52 +768,66 @@ struct Sim {
             const int n = adm ? min(m, T - ub) : 0;
             const int du = adm ? blocks(kvv + n) - blocks(kvv) : 0;
             const int dui = scan_add(du);
+            const int kvi = scan_add(adm ? kvv : 0);
             const bool fit = U + dui <= Kb;
             const uint64_t bad = ballot(adm && !fit);
             const uint64_t am = ballot(adm);
-            const uint64_t okm =
-                bad ? (am & ((1ull << (__ffsll((unsigned long long)bad) - 1)) - 1ull)) : am;
+            const uint64_t okm = bad ? (am & ((1ull << ffs0(bad)) - 1ull)) : am;
             const bool ok = ((okm >> lane()) & 1ull) != 0;
             if (ok) {
-                S.nn[r] = n;
-                uint32_t g2 = g | G_INB;
+                uint32_t g2 = (g & G_LOW) | G_INB | ((uint32_t)n << G_N_SHIFT);
                 if (!res) g2 = (g2 & ~G_GUARD) | G_RES | ((g >> G_LVL_SHIFT) & 31u);
                 S.gs[r] = g2;
             }
             if (okm) {
+                const int last = fls0(okm);
+                const int used_new = rl(ub + n, last);
+                const int nadm_w = popc(ballot(ok && !res));
                 cnt += popc(okm);
-                used += wsum(ok ? n : 0);
-                U += wsum(ok ? du : 0);
-                sum_ctx += wsum(ok ? kvv + n : 0);
-                nW -= popc(ballot(ok && !res));
+                sum_ctx += rl(kvi, last) + (used_new - used);
+                used = used_new;
+                U += rl(dui, last);
+                nW -= nadm_w;
+                nR += nadm_w;
+                emit_chunks |= (1ull << ((p + ffs0(okm)) >> 6)) | (1ull << ((p + last) >> 6));
             }
+            const uint64_t resm = ballot(valid && res);
             wsync();
             if (bad) {
-                const int q = p + __ffsll((unsigned long long)bad) - 1;
-                slow_path(q, closed);
+                const int ql = ffs0(bad);
+                // residents among lanes [0, ql] are passed (q included if resident);
+                // waiting entries admitted in this chunk sit below q
+                r_ahead -= popc(resm & (ql == 63 ? ~0ull : ((2ull << ql) - 1ull)));
+                slow_path(p + ql, closed, r_ahead);
                 if (status) return;
-                p = q + 1;
+                p = p + ql + 1;
             } else {
-                p += kWave;
+                r_ahead -= popc(resm);
+                p = min(p + kWave, end);
             }
         }
-        hi = max(hi, min(p, L));
     }
 
     // ---------------------------------------------------------- execute
 
-    // Returns the lowest rank whose key or presence changed (INT32_MAX if none).
+    // Returns the lowest rank whose key moved (INT32_MAX if none).
     DEV int emission(int64_t t_end) {
-        int lo = INT32_MAX, ufree = 0, ndone = 0;
+        int lo = INT32_MAX, ufree = 0, ndone = 0, lohole = INT32_MAX;
         bool bad_idx = false;
-        for (int b = 0; b < hi; b += kWave) {
+        const uint32_t t32 = (uint32_t)t_end;
+        const int nch = (L + kWave - 1) >> 6;
+        uint64_t todo = emit_all ? (nch >= 64 ? ~0ull : ((1ull << nch) - 1ull)) : emit_chunks;
+        while (todo) {
+            const int b = ffs0(todo) * kWave;
+            todo &= todo - 1;
             const int r = b + lane();
-            const uint32_t g = r < hi ? S.gs[r] : 0u;
+            const uint32_t g = r < L ? S.gs[r] : 0u;
             bool chg = false;
             if (g & G_INB) {
                 R x;
                 ldr(S, r, x);
-                x.kv += S.nn[r];
+                x.kv += (int)(x.gs >> G_N_SHIFT);
+                x.gs &= G_LOW & ~G_INB;
                 const int idx = idx_of(x.pk);
                 if (idx >= N) bad_idx = true;
                 if (x.kv == x.w && idx < N) {
@@ -696,19 +837,18 @@ struct Sim {
                         x.gs |= G_FIRST;
                         tfirst[idx] = t_end;
                     } else {
-                        const int64_t gap = t_end - x.tl;
-                        const uint32_t gp = gap > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)gap;
+                        const uint32_t gp = t32 - x.tl;  // gaps beyond 2^32 overflow TTLT too
                         if (gp > x.tbt) x.tbt = gp;
                     }
-                    x.tl = t_end;
+                    x.tl = t32;
                     if (x.left == 0) {
                         x.gs = (x.gs | G_DONE) & ~G_RES;
                         ufree += blocks(x.kv);
                         x.kv = 0;
                         tlast[idx] = t_end;
                         tbtw[idx] = x.tbt;
-                        chg = true;
                         ndone++;
+                        if (r < lohole) lohole = r;
                     } else if (POL == P_BOOST) {
                         const int lo_ = (int)((x.gs >> G_LVL_SHIFT) & 31u);
                         const int ln = level_of(x.w, k, lk);
@@ -724,7 +864,6 @@ struct Sim {
                     x.pk = pack((int64_t)x.w + x.left - 1 - x.kv, idx);
                     chg = true;
                 }
-                x.gs &= ~G_INB;
                 str(S, r, x);
             } else if (g & G_EVI) {
                 if (POL == P_SRPT) {
@@ -738,14 +877,21 @@ struct Sim {
         }
         wsync();
         if (ballot(bad_idx)) fail(S_ESTATE);
-        U -= wsum(ufree);
-        completed += wsum(ndone);
+        const int nd = wsum(ndone);
+        if (nd) {
+            U -= wsum(ufree);
+            completed += nd;
+            nR -= nd;
+            n_holes += nd;
+            lo_hole = min(lo_hole, wmin(lohole));
+        }
         return wmin(lo);
     }
 
-    // Compact out finished entries from rank `from` on; extract entries whose
-    // key moved (flagged, or below the running maximum) into the staging
-    // slots and, beyond 64, the HBM overflow. Returns the number extracted.
+    // From rank `from` on: remove holes; extract entries whose key moved
+    // (flagged, or below the running maximum of the entries kept before them)
+    // into the staging slots and, beyond 64, the HBM overflow. Returns the
+    // number extracted. No holes lie below `from`.
     DEV int compact_extract(int from) {
         const int start = (from >> 6) << 6;
         uint64_t pmax = start > 0 ? uniu(S.pk[start - 1]) : 0ull;
@@ -759,8 +905,7 @@ struct Sim {
             const bool dirty = v && (y.gs & G_DIRTY);
             const uint64_t val = (v && !dead && !dirty) ? y.pk : 0ull;
             const uint64_t inc = scan_maxu(val);
-            uint64_t exc = (uint64_t)__shfl_up((unsigned long long)inc, 1);
-            if (lane() == 0) exc = 0;
+            uint64_t exc = prev_lane_u64(inc, 0ull);
             if (pmax > exc) exc = pmax;
             const bool ext = v && !dead && (dirty || y.pk < exc);
             const bool keep = v && !dead && !ext;
@@ -773,31 +918,37 @@ struct Sim {
             if (ext) {
                 y.gs &= ~G_DIRTY;
                 const int xi = nx + mbcnt(xm);
-                if (xi < kStage) str(S, lcap + xi, y);
+                if (xi < kStage) str(S, sb + xi, y);
                 else ovf[xi - kStage] = to_rec(y);
             }
             wsync();
-            const uint64_t cm = wmaxu(val);
+            const uint64_t cm = rlu(inc, 63);
             if (cm > pmax) pmax = cm;
             out += popc(km);
             nx += popc(xm);
         }
         L = out;
+        n_holes = 0;
+        lo_hole = INT32_MAX;
         return nx;
     }
 
     DEV void maintenance(int lo_mod) {
-        if (lo_mod < L) {
-            const int nx = compact_extract(lo_mod);
-            const int k0 = min(nx, kStage);
-            R x;
-            if (lane() < k0) ldr(S, lcap + lane(), x);
-            wsync();
-            add_entries(x, k0);
-            for (int b = kStage; b < nx && status == 0; b += kStage) {
-                const int kb = min(nx - b, kStage);
-                if (lane() < kb) x = from_rec(ovf[b - kStage + lane()]);
-                add_entries(x, kb);
+        if (lo_mod < L || n_holes >= kHoleLimit || L > lcap) {
+            const int nx = compact_extract(min(min(lo_mod, lo_hole), L));
+            if (nx > kStage) hbm_fence();
+            if (L > lcap) spill_excess();  // a refill during formation used the overflow region
+            if (nx > 0 && status == 0) {
+                const int k0 = min(nx, kStage);
+                R x;
+                if (lane() < k0) ldr(S, sb + lane(), x);
+                wsync();
+                add_entries(x, k0);
+                for (int b = kStage; b < nx && status == 0; b += kStage) {
+                    const int kb = min(nx - b, kStage);
+                    if (lane() < kb) x = from_rec(ovf[b - kStage + lane()]);
+                    add_entries(x, kb);
+                }
             }
         }
         if (status == 0) take_arrivals();
@@ -810,11 +961,11 @@ struct Sim {
         take_arrivals();
         for (;;) {
             if (status) break;
-            if (L == 0) {
+            if (nW + nR == 0) {
                 if (spill_n > 0) {
                     refill();
                     if (status) break;
-                    if (L == 0) {
+                    if (nW + nR == 0) {
                         fail(S_ESTATE);
                         break;
                     }
@@ -832,14 +983,6 @@ struct Sim {
                 t = an;
                 take_arrivals();
                 continue;
-            }
-            if (spill_n > 0 && nW < M) {
-                refill();
-                if (status) break;
-                if (spill_n > 0 && nW < M) {
-                    fail(S_ECAPACITY);
-                    break;
-                }
             }
             formation();
             if (status) break;
@@ -865,6 +1008,7 @@ struct Sim {
     }
 
     DEV void finish() {
+        hbm_fence();
         if (status == 0 && completed != N) fail(S_ESTATE);
         if (status == 0) {
             const size_t ioff = (size_t)inst * (size_t)N;

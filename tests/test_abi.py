@@ -121,6 +121,7 @@ def test_rejects_invalid_settings():
 def test_rejects_invalid_engine():
     w = small()
     for kw in (dict(max_seqs=0), dict(chunk=0), dict(chunk=10000, max_tokens=8192),
+               dict(chunk=40000, max_tokens=65536),
                dict(kv_blocks=0), dict(block_tokens=0), dict(iter_base_us=0),
                dict(iter_ctx_div=0), dict(max_iters=0), dict(tau_us=0.0)):
         e = W.Engine(**{**W.Engine().__dict__, **kw})
@@ -130,6 +131,7 @@ def test_rejects_invalid_engine():
         assert tas.tas_workspace_bytes(t, p) == 0
     # candidate list too small for the batch cap, or beyond the LDS limit
     assert create_rc(w, list_cap=64)[0] == tas.TAS_EINVAL
+    assert create_rc(w, list_cap=4033)[0] == tas.TAS_EINVAL
     assert create_rc(w, list_cap=1 << 16)[0] == tas.TAS_EINVAL
 
 
