@@ -80,6 +80,8 @@ def main():
     ap.add_argument("--traces", type=int, default=None, help="shrink the sweep (testing)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
     ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
+    ap.add_argument("--list-cap", type=int, default=0,
+                    help="on-chip candidate list per instance (0: the library default)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this path runs on one GPU; --gpus {args.gpus} is not supported "
@@ -98,7 +100,7 @@ def main():
     name = f"{W.NAMES[args.workload]}: {w.n_traces} traces x {w.meta['n_settings']} settings x " \
            f"{w.n_req} requests"
     print(f"[bench] building {name}", file=sys.stderr, flush=True)
-    sim = tas.Simulation(w, device=dev)
+    sim = tas.Simulation(w, device=dev, list_cap=args.list_cap)
     stream = torch.cuda.current_stream()
 
     for i in range(args.warmup):

@@ -111,13 +111,16 @@ typedef struct {
     int64_t max_iters;     /* per-instance iteration limit (TAS_ELIVELOCK)     */
     double tau_us;         /* microseconds per token of boost, > 0             */
     int32_t list_cap;      /* on-chip candidate entries per instance, in
-                              [max_seqs + 64, 4032]; 0 picks max_seqs + 192
-                              rounded up to 64. More residents than this at
-                              once is TAS_ECAPACITY                            */
+                              [max_seqs + 64, 4032]; 0 picks max_seqs + 128
+                              rounded up to 64                                 */
     int32_t spill_cap;     /* waiting entries per instance kept in HBM beyond
                               the on-chip list; 0 = n_req                      */
     int32_t n_inst;
-    int32_t reserved;
+    int32_t retry_cap;     /* an instance that holds more residents than
+                              list_cap reruns from scratch with this larger
+                              list (tas_run enqueues the second pass); 0 picks
+                              min(4032, max(2048, 4 list_cap)). Beyond it:
+                              TAS_ECAPACITY                                    */
     const tas_setting *inst; /* [n_inst]                                       */
 } tas_params;
 
@@ -143,8 +146,8 @@ int tas_create(const tas_traces *traces, const tas_params *params, void *d_ws, s
                tas_ctx **out);
 
 /* Enqueue the simulation of every instance on `stream` (one workgroup per
- * instance). Per-request latencies, counters and errors land in the
- * workspace. */
+ * instance), followed by the retry pass for instances that outgrew list_cap.
+ * Per-request latencies, counters and errors land in the workspace. */
 int tas_run(tas_ctx *ctx, void *stream);
 
 /* Enqueue the nearest-rank percentile reduction: d_out DEVICE uint32

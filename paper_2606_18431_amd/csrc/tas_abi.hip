@@ -15,8 +15,8 @@
 #include "tas_internal.h"
 
 struct tas_ctx {
-    int32_t n_traces = 0, n_req = 0, n_inst = 0, list_cap = 0, spill_cap = 0;
-    int64_t lds_bytes = 0;
+    int32_t n_traces = 0, n_req = 0, n_inst = 0, list_cap = 0, spill_cap = 0, retry_cap = 0;
+    int64_t lds_bytes = 0, lds_retry = 0;
     tas::SimArgs args{};
     std::vector<tas::DevSetting> settings;
     hipStream_t last_stream = nullptr;
@@ -35,12 +35,17 @@ struct Layout {
         status, spill, ovf, total;
 };
 
-// Room for the residents (about max_seqs; more when the token budget pauses
-// many of them) plus a window of waiting entries.
+// First pass: room for about max_seqs residents plus a window of waiting
+// entries, small enough for several instances per compute unit. Instances
+// that hold more residents than that rerun in a second pass with a large list.
 int32_t default_list_cap(int32_t max_seqs) {
-    int64_t lc = (int64_t)max_seqs + 192;
+    int64_t lc = (int64_t)max_seqs + 128;
     lc = (lc + 63) / 64 * 64;
-    return (int32_t)lc;
+    return (int32_t)std::min<int64_t>(lc, tas::kMaxListCap);
+}
+int32_t default_retry_cap(int32_t list_cap) {
+    return (int32_t)std::min<int64_t>(std::max<int64_t>(4 * (int64_t)list_cap, 2048),
+                                      tas::kMaxListCap);
 }
 
 bool engine_ok(const tas_params *p) {
@@ -57,18 +62,21 @@ bool shape_ok(const tas_traces *t) {
            t->prompt && t->decode;
 }
 
-// Effective capacities; false if invalid.
-bool caps(const tas_traces *t, const tas_params *p, int32_t *lc, int32_t *sc) {
-    int32_t l = p->list_cap ? p->list_cap : default_list_cap(p->max_seqs);
+// Effective capacities; false if invalid. *rc == *lc means no second pass.
+bool caps(const tas_traces *t, const tas_params *p, int32_t *lc, int32_t *rc, int32_t *sc) {
+    const int32_t l = p->list_cap ? p->list_cap : default_list_cap(p->max_seqs);
     if ((int64_t)l < (int64_t)p->max_seqs + 64 || l > tas::kMaxListCap) return false;
     if (tas::lds_bytes_for(l) > kMaxLds) return false;
-    int32_t s = p->spill_cap ? p->spill_cap : t->n_req;
+    int32_t r = p->retry_cap ? p->retry_cap : default_retry_cap(l);
+    if (r < l) r = l;
+    if (r > tas::kMaxListCap || tas::lds_bytes_for(r) > kMaxLds) return false;
     *lc = l;
-    *sc = s;
+    *rc = r;
+    *sc = p->spill_cap ? p->spill_cap : t->n_req;
     return true;
 }
 
-bool layout(const tas_traces *t, const tas_params *p, int32_t lc, int32_t sc, Layout *L) {
+bool layout(const tas_traces *t, const tas_params *p, int32_t rc, int32_t sc, Layout *L) {
     const size_t tn = (size_t)t->n_traces * (size_t)t->n_req;
     const size_t in = (size_t)p->n_inst * (size_t)t->n_req;
     size_t o = 0;
@@ -85,7 +93,7 @@ bool layout(const tas_traces *t, const tas_params *p, int32_t lc, int32_t sc, La
     L->counters = o, o = align256(o + (size_t)p->n_inst * 8 * 8);
     L->status = o, o = align256(o + (size_t)p->n_inst * 4);
     L->spill = o, o = align256(o + (size_t)p->n_inst * (size_t)sc * sizeof(tas::Rec));
-    L->ovf = o, o = align256(o + (size_t)p->n_inst * (size_t)(lc + tas::kStage) * sizeof(tas::Rec));
+    L->ovf = o, o = align256(o + (size_t)p->n_inst * (size_t)(rc + tas::kStage) * sizeof(tas::Rec));
     L->total = o;
     return true;
 }
@@ -132,10 +140,10 @@ int tas_boost_table(double gamma, int32_t k, double tau_us, int64_t *out) {
 
 size_t tas_workspace_bytes(const tas_traces *t, const tas_params *p) {
     if (!shape_ok(t) || !p || !engine_ok(p)) return 0;
-    int32_t lc, sc;
-    if (!caps(t, p, &lc, &sc)) return 0;
+    int32_t lc, rc, sc;
+    if (!caps(t, p, &lc, &rc, &sc)) return 0;
     Layout L;
-    layout(t, p, lc, sc, &L);
+    layout(t, p, rc, sc, &L);
     return L.total;
 }
 
@@ -144,8 +152,8 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     if (!out) return TAS_EINVAL;
     *out = nullptr;
     if (!shape_ok(t) || !p || !engine_ok(p)) return TAS_EINVAL;
-    int32_t lc, sc;
-    if (!caps(t, p, &lc, &sc)) return TAS_EINVAL;
+    int32_t lc, rc, sc;
+    if (!caps(t, p, &lc, &rc, &sc)) return TAS_EINVAL;
     const int32_t N = t->n_req;
     const size_t tn = (size_t)t->n_traces * (size_t)N;
     // traces: sorted, in range; P, D >= 1; P + D < 2^24
@@ -166,14 +174,15 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
         if (need > p->kv_blocks) return TAS_EINFEASIBLE;
     }
     Layout L;
-    layout(t, p, lc, sc, &L);
+    layout(t, p, rc, sc, &L);
     if (!d_ws || ws_bytes < L.total || ((uintptr_t)d_ws & 255u)) return TAS_ENOMEM;
 
     tas_ctx *c = new (std::nothrow) tas_ctx();
     if (!c) return TAS_ENOMEM;
     c->n_traces = t->n_traces, c->n_req = N, c->n_inst = p->n_inst;
-    c->list_cap = lc, c->spill_cap = sc;
+    c->list_cap = lc, c->spill_cap = sc, c->retry_cap = rc;
     c->lds_bytes = tas::lds_bytes_for(lc);
+    c->lds_retry = tas::lds_bytes_for(rc);
     c->settings.resize((size_t)p->n_inst);
     for (int32_t i = 0; i < p->n_inst; i++) {
         const tas_setting &s = p->inst[i];
@@ -219,6 +228,7 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     a.M = p->max_seqs, a.T = p->max_tokens, a.c = p->chunk, a.Kb = p->kv_blocks;
     a.bs = p->block_tokens, a.base = p->iter_base_us, a.tok = p->iter_tok_us;
     a.div = p->iter_ctx_div, a.list_cap = lc, a.spill_cap = sc;
+    a.ovf_stride = rc + tas::kStage, a.retry = 0;
     *out = c;
     return TAS_OK;
 }
@@ -226,7 +236,14 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
 int tas_run(tas_ctx *c, void *stream) {
     if (!c) return TAS_EINVAL;
     c->last_stream = (hipStream_t)stream;
-    return tas_launch_sim(c->args, c->lds_bytes, stream) ? TAS_EHIP : TAS_OK;
+    if (tas_launch_sim(c->args, c->lds_bytes, stream)) return TAS_EHIP;
+    if (c->retry_cap > c->list_cap) {  // rerun instances that outgrew the small list
+        tas::SimArgs a2 = c->args;
+        a2.list_cap = c->retry_cap;
+        a2.retry = 1;
+        if (tas_launch_sim(a2, c->lds_retry, stream)) return TAS_EHIP;
+    }
+    return TAS_OK;
 }
 
 int tas_percentiles(tas_ctx *c, uint32_t *d_out, void *stream) {

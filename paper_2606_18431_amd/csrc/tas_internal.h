@@ -47,13 +47,15 @@ struct SimArgs {
     int64_t *counters;       // [n_inst][8]
     int32_t *status;         // [n_inst]
     Rec *spill;              // [n_inst][spill_cap]
-    Rec *ovf;                // [n_inst][list_cap + 64]
+    Rec *ovf;                // [n_inst][ovf_stride]
     int64_t max_iters;
     int32_t n_req;
     int32_t n_inst;
     int32_t M, T, c, Kb, bs, base, tok, div;
     int32_t list_cap;
     int32_t spill_cap;
+    int32_t ovf_stride;  // records per instance in `ovf` (largest list + 64)
+    int32_t retry;       // second pass: only instances whose first pass ran out of list
 };
 
 // Dynamic LDS bytes per workgroup for a list capacity.

@@ -164,11 +164,16 @@ DEV int level_of(int w, int k, int lk) {
 
 // ------------------------------------------------------------ LDS layout
 
+// LDS holds the candidate list as three parallel arrays: a 16-byte quad
+// {gs, w, kv, left} (what formation reads, one 128-bit load per lane), the
+// packed key (searches and merges) and {tbt, tl} (emission only). Strides of
+// 16 and 8 bytes keep the 64 lanes of one access on distinct banks.
 struct Lds {
-    uint64_t *pk;
+    uint4 *q;
+    uint64_t *k;
+    uint2 *tt;
     int64_t *bt;
-    int32_t *w, *left, *kv;
-    uint32_t *gs, *tbt, *tl, *hist;
+    uint32_t *hist;
 };
 
 struct R {  // one candidate-list record in registers
@@ -178,22 +183,16 @@ struct R {  // one candidate-list record in registers
 };
 
 DEV void ldr(const Lds &S, int i, R &x) {
-    x.pk = S.pk[i];
-    x.w = S.w[i];
-    x.left = S.left[i];
-    x.kv = S.kv[i];
-    x.gs = S.gs[i];
-    x.tbt = S.tbt[i];
-    x.tl = S.tl[i];
+    const uint4 q = S.q[i];
+    const uint2 t = S.tt[i];
+    x.gs = q.x, x.w = (int)q.y, x.kv = (int)q.z, x.left = (int)q.w;
+    x.pk = S.k[i];
+    x.tbt = t.x, x.tl = t.y;
 }
 DEV void str(const Lds &S, int i, const R &x) {
-    S.pk[i] = x.pk;
-    S.w[i] = x.w;
-    S.left[i] = x.left;
-    S.kv[i] = x.kv;
-    S.gs[i] = x.gs;
-    S.tbt[i] = x.tbt;
-    S.tl[i] = x.tl;
+    S.q[i] = make_uint4(x.gs, (uint32_t)x.w, (uint32_t)x.kv, (uint32_t)x.left);
+    S.k[i] = x.pk;
+    S.tt[i] = make_uint2(x.tbt, x.tl);
 }
 DEV R from_rec(const Rec &r) {
     R x;
@@ -220,12 +219,14 @@ DEV bool is_waiting(uint32_t g) { return (g & (G_RES | G_DONE)) == 0; }
 
 // ------------------------------------------------------------ the simulator
 
-template <int POL>
+// POL: policy. BSH: log2 of the KV block size when it is a power of two
+// (the common 16-token block gets its own instantiation), -1 otherwise.
+template <int POL, int BSH>
 struct Sim {
     const SimArgs &A;
     Lds S;
     // instance constants
-    int inst, N, M, T, c, Kb, bs, bs_shift, base, tok, div, k, lk, memguard, lcap, scap;
+    int inst, N, M, T, c, Kb, bs, base, tok, div, k, lk, memguard, lcap, scap;
     int sb;  // first staging slot: the list may use [0, lcap + kStage) during formation
     int64_t delta, max_iters;
     const int64_t *arr;
@@ -245,16 +246,17 @@ struct Sim {
     int64_t sum_ctx;
     uint64_t emit_chunks;  // 64-entry chunks holding batch members or evictions
     bool emit_all;         // ranks moved during formation: visit every chunk
-    // victim masks, lane c = chunk c: residents outside the batch, and those a
-    // voluntary eviction may take (MemGuard); valid for chunks >= vm_from
+    // victim masks, lane c = chunk c: residents, and those a voluntary
+    // eviction may take (MemGuard). Kept across iterations: bits change in
+    // place on admission, eviction and completion; any edit that moves ranks
+    // clears vm_ok and the next victim search rebuilds them.
     uint64_t vm_res, vm_ev;
-    int vm_from;
+    bool vm_ok;
 
     DEV Sim(const SimArgs &a, const DevSetting &st, int i, unsigned char *smem) : A(a) {
         inst = i;
         N = a.n_req, M = a.M, T = a.T, c = a.c, Kb = a.Kb, bs = a.bs;
         base = a.base, tok = a.tok, div = a.div, lcap = a.list_cap, scap = a.spill_cap;
-        bs_shift = (bs & (bs - 1)) == 0 ? (31 - __clz(bs)) : -1;
         k = st.k > 0 ? st.k : 1;
         lk = 31 - __clz(k);
         memguard = st.memguard;
@@ -265,18 +267,14 @@ struct Sim {
         const size_t ioff = (size_t)i * (size_t)N;
         tfirst = a.tfirst + ioff, tlast = a.tlast + ioff, tbtw = a.tbtw + ioff;
         spill = a.spill + (size_t)i * (size_t)scap;
-        ovf = a.ovf + (size_t)i * (size_t)(lcap + kStage);
+        ovf = a.ovf + (size_t)i * (size_t)a.ovf_stride;
         sb = lcap + kStage;
         const int cap = lcap + 2 * kStage;
         size_t o = 0;
-        S.pk = (uint64_t *)(smem + o), o += (size_t)cap * 8;
+        S.q = (uint4 *)(smem + o), o += (size_t)cap * 16;
+        S.k = (uint64_t *)(smem + o), o += (size_t)cap * 8;
+        S.tt = (uint2 *)(smem + o), o += (size_t)cap * 8;
         S.bt = (int64_t *)(smem + o), o += kLevels * 8;
-        S.w = (int32_t *)(smem + o), o += (size_t)cap * 4;
-        S.left = (int32_t *)(smem + o), o += (size_t)cap * 4;
-        S.kv = (int32_t *)(smem + o), o += (size_t)cap * 4;
-        S.gs = (uint32_t *)(smem + o), o += (size_t)cap * 4;
-        S.tbt = (uint32_t *)(smem + o), o += (size_t)cap * 4;
-        S.tl = (uint32_t *)(smem + o), o += (size_t)cap * 4;
         S.hist = (uint32_t *)(smem + o);
         for (int j = lane(); j < kLevels; j += kWave) S.bt[j] = st.bt[j];
         t = 0;
@@ -289,14 +287,17 @@ struct Sim {
         emit_chunks = 0;
         emit_all = false;
         vm_res = vm_ev = 0;
-        vm_from = INT32_MAX;
+        vm_ok = false;
         wsync();
     }
 
     DEV void fail(int code) {
         if (status == 0) status = code;
     }
-    DEV int blocks(int x) const { return bs_shift >= 0 ? (x + bs - 1) >> bs_shift : (x + bs - 1) / bs; }
+    DEV int blocks(int x) const {
+        if (BSH >= 0) return (x + (1 << BSH) - 1) >> BSH;
+        return (x + bs - 1) / bs;
+    }
 
     // ---------------------------------------------------------- arrivals
 
@@ -357,11 +358,11 @@ struct Sim {
         if (L == 0) return 0;
         const int nch = (L + kWave - 1) >> 6;
         const int probe = min(lane() * kWave + kWave - 1, L - 1);
-        const uint64_t cm = lane() < nch ? S.pk[probe] : ~0ull;
+        const uint64_t cm = lane() < nch ? S.k[probe] : ~0ull;
         const int c0 = popc(ballot(lane() < nch && cm < x));
         if (c0 >= nch) return L;
         const int r = c0 * kWave + lane();
-        const uint64_t v = r < L ? S.pk[r] : ~0ull;
+        const uint64_t v = r < L ? S.k[r] : ~0ull;
         return c0 * kWave + popc(ballot(r < L && v < x));
     }
 
@@ -379,7 +380,7 @@ struct Sim {
             for (int b = ((L - 1) >> 6) << 6; b >= 0 && b + kWave > minpos; b -= kWave) {
                 const int r = b + lane();
                 const bool mv = r >= minpos && r < L;
-                const uint64_t pr = mv ? S.pk[r] : ~0ull;
+                const uint64_t pr = mv ? S.k[r] : ~0ull;
                 int sh = 0;
                 for (int j = 0; j < K; j++) {
                     const uint64_t xj = rlu(x.pk, j);
@@ -388,6 +389,7 @@ struct Sim {
                     if (lane() == j) pos_in += cj;
                 }
                 const bool go = mv && sh > 0;
+                if (ballot(go)) vm_ok = false;
                 R y;
                 if (go) ldr(S, r, y);
                 wsync();
@@ -402,6 +404,7 @@ struct Sim {
 
     // Remove the entries whose flags intersect `mask`, from rank `from` on.
     DEV void compact_remove(int from, uint32_t mask) {
+        vm_ok = false;
         int out = from;
         for (int b = (from >> 6) << 6; b < L; b += kWave) {
             const int r = b + lane();
@@ -442,7 +445,7 @@ struct Sim {
         int found = 0, lowest = L;
         for (int b = ((L - 1) >> 6) << 6; b >= 0 && found < E; b -= kWave) {
             const int r = b + lane();
-            const bool isw = r < L && is_waiting(S.gs[r]);
+            const bool isw = r < L && is_waiting(S.q[r].x);
             const uint64_t m = ballot(isw);
             const int above = popc(m) - mbcnt(m) - 1;
             const bool take = isw && above < E - found;
@@ -450,7 +453,7 @@ struct Sim {
                 R y;
                 ldr(S, r, y);
                 spill[spill_n + found + above] = to_rec(y);
-                S.gs[r] = y.gs | G_MARK;
+                S.q[r].x = y.gs | G_MARK;
             }
             const uint64_t tm = ballot(take);
             found += popc(tm);
@@ -461,7 +464,7 @@ struct Sim {
             fail(S_ECAPACITY);
             return;
         }
-        const uint64_t mn = uniu(S.pk[lowest]);
+        const uint64_t mn = uniu(S.k[lowest]);
         spill_min = (spill_n == 0 || mn < spill_min) ? mn : spill_min;
         spill_n += E;
         nW -= E;
@@ -590,20 +593,38 @@ struct Sim {
 
     // ---------------------------------------------------------- formation
 
-    // Victim masks for chunks [c0, nch): one LDS read and two ballots per
-    // chunk, kept one chunk per lane.
-    DEV void build_victim_masks(int c0) {
+    // Victim masks for the whole list: one LDS read and two ballots per chunk.
+    // Batch members below the candidate are excluded by rank (victims lie
+    // above it, where nothing is in the batch yet), so the masks ignore INB.
+    DEV void build_victim_masks() {
         const int nch = (L + kWave - 1) >> 6;
-        for (int c = c0; c < nch && c < vm_from; c++) {
+        vm_res = vm_ev = 0;
+        for (int c = 0; c < nch; c++) {
             const int r = c * kWave + lane();
-            const uint32_t g = r < L ? S.gs[r] : 0u;
-            const bool rs = (g & G_RES) && !(g & G_INB);
+            const uint32_t g = r < L ? S.q[r].x : 0u;
+            const bool rs = (g & G_RES) != 0;
             bool ev = rs;
             if (POL == P_BOOST && memguard) ev = rs && ((g >> G_LVL_SHIFT) & 31u) > (g & G_GUARD);
             const uint64_t m1 = ballot(rs), m2 = ballot(ev);
             if (lane() == c) vm_res = m1, vm_ev = m2;
         }
-        vm_from = min(vm_from, c0);
+        vm_ok = true;
+    }
+
+    // A request at rank r became resident (dispatch: MemGuard keeps it
+    // non-evictable until its level moves) or stopped being one.
+    DEV void vm_set(int r, bool resident) {
+        if (!vm_ok) return;
+        const uint64_t bit = 1ull << (r & 63);
+        if (lane() == (r >> 6)) {
+            if (resident) {
+                vm_res |= bit;
+                if (!(POL == P_BOOST && memguard)) vm_ev |= bit;
+            } else {
+                vm_res &= ~bit;
+                vm_ev &= ~bit;
+            }
+        }
     }
 
     // Highest rank > q set in the per-chunk mask vm, or -1.
@@ -622,11 +643,11 @@ struct Sim {
     // evicted for candidate q (voluntary: MemGuard and hysteresis apply).
     // The list is sorted, so the highest such rank is the worst (key, idx).
     DEV int find_victim(int q, uint64_t pkq, bool voluntary) {
-        if (vm_from > (q >> 6)) build_victim_masks(q >> 6);
+        if (!vm_ok) build_victim_masks();
         const int v = top_above(voluntary ? vm_ev : vm_res, q);
         if (POL == P_BOOST && voluntary && v >= 0 && delta > 0) {
             // the worst eligible key fails the hysteresis test => all fail
-            const uint64_t pv = uniu(S.pk[v]);
+            const uint64_t pv = uniu(S.k[v]);
             const int64_t kd = key_of(pv) - delta, kq = key_of(pkq);
             if (!(kd > kq || (kd == kq && idx_of(pv) > idx_of(pkq)))) return -1;
         }
@@ -634,22 +655,20 @@ struct Sim {
     }
 
     DEV void do_evict(int v) {
-        const int kvv = uni(S.kv[v]);
+        const uint4 qv = S.q[v];
+        const int kvv = uni((int)qv.z);
+        const uint32_t g = (uint32_t)uni((int)qv.x);
         wsync();
         if (lane() == 0) {
-            const uint32_t g = S.gs[v];
-            S.kv[v] = 0;
-            S.gs[v] = (g & ~G_RES) | G_EVI | (POL == P_SRPT ? G_DIRTY : 0u);
+            S.q[v].x = (g & ~G_RES) | G_EVI | (POL == P_SRPT ? G_DIRTY : 0u);
+            S.q[v].z = 0;
         }
         wsync();
         U -= blocks(kvv);
         nW++;
         nR--;
         emit_chunks |= 1ull << (v >> 6);
-        if ((v >> 6) >= vm_from && lane() == (v >> 6)) {
-            vm_res &= ~(1ull << (v & 63));
-            vm_ev &= ~(1ull << (v & 63));
-        }
+        vm_set(v, false);
     }
 
     DEV void admit_one(int q, uint32_t g, int n, int du, int kvv) {
@@ -657,24 +676,28 @@ struct Sim {
         if (lane() == 0) {
             uint32_t g2 = (g & G_LOW) | G_INB | ((uint32_t)n << G_N_SHIFT);
             if (!res) g2 = (g2 & ~G_GUARD) | G_RES | ((g >> G_LVL_SHIFT) & 31u);
-            S.gs[q] = g2;
+            S.q[q].x = g2;
         }
         wsync();
         cnt++;
         used += n;
         U += du;
         sum_ctx += kvv + n;
-        if (!res) nW--, nR++;
+        if (!res) {
+            nW--, nR++;
+            vm_set(q, true);
+        }
         emit_chunks |= 1ull << (q >> 6);
     }
 
     // Candidate q did not fit: evictions, or closing admissions. r_ahead
     // counts residents at ranks > q.
     DEV void slow_path(int q, bool &closed, int &r_ahead) {
-        const uint32_t g = (uint32_t)uni((int)S.gs[q]);
-        const int w = uni(S.w[q]);
-        const int kvv = uni(S.kv[q]);
-        const uint64_t pkq = uniu(S.pk[q]);
+        const uint4 qq = S.q[q];
+        const uint32_t g = (uint32_t)uni((int)qq.x);
+        const int w = uni((int)qq.y);
+        const int kvv = uni((int)qq.z);
+        const uint64_t pkq = uniu(S.k[q]);
         const bool res = (g & G_RES) != 0;
         const int n = min(min(w - kvv, c), T - used);
         const int du = blocks(kvv + n) - blocks(kvv);
@@ -726,8 +749,6 @@ struct Sim {
             return;
         }
         refill_into(room);
-        vm_from = INT32_MAX;  // ranks moved: rebuild the victim masks on demand
-        vm_res = vm_ev = 0;
         emit_all = true;
     }
 
@@ -736,8 +757,6 @@ struct Sim {
         sum_ctx = 0;
         emit_chunks = 0;
         emit_all = false;
-        vm_from = INT32_MAX;
-        vm_res = vm_ev = 0;
         bool closed = false;
         int r_ahead = nR;  // residents at ranks >= p
         int p = 0;
@@ -754,9 +773,11 @@ struct Sim {
             const int end = closed ? L : min(L, bstar);
             const int r = p + lane();
             const bool valid = r < end;
-            const uint32_t g = valid ? S.gs[r] : 0u;
-            const int w = valid ? S.w[r] : 0;
-            const int kvv = valid ? S.kv[r] : 0;
+            uint4 qr = make_uint4(0u, 0u, 0u, 0u);
+            if (valid) qr = S.q[r];
+            const uint32_t g = qr.x;
+            const int w = (int)qr.y;
+            const int kvv = (int)qr.z;
             const bool res = (g & G_RES) != 0;
             const bool cand = valid && !(g & (G_EVI | G_DONE)) && (res || !closed);
             const int m = cand ? min(w - kvv, c) : 0;
@@ -777,7 +798,7 @@ struct Sim {
             if (ok) {
                 uint32_t g2 = (g & G_LOW) | G_INB | ((uint32_t)n << G_N_SHIFT);
                 if (!res) g2 = (g2 & ~G_GUARD) | G_RES | ((g >> G_LVL_SHIFT) & 31u);
-                S.gs[r] = g2;
+                S.q[r].x = g2;
             }
             if (okm) {
                 const int last = fls0(okm);
@@ -789,6 +810,15 @@ struct Sim {
                 U += rl(dui, last);
                 nW -= nadm_w;
                 nR += nadm_w;
+                if (vm_ok && nadm_w) {  // dispatched waiting entries become residents
+                    const uint64_t nm = ballot(ok && !res);
+                    // lanes of this chunk land in aligned chunks p>>6 and (p>>6)+1
+                    const int c0 = p >> 6, sh = p & 63;
+                    const uint64_t lo = nm << sh, hi = sh ? (nm >> (64 - sh)) : 0ull;
+                    const bool ev_too = !(POL == P_BOOST && memguard);
+                    if (lane() == c0) vm_res |= lo, vm_ev |= ev_too ? lo : 0ull;
+                    if (lane() == c0 + 1) vm_res |= hi, vm_ev |= ev_too ? hi : 0ull;
+                }
                 emit_chunks |= (1ull << ((p + ffs0(okm)) >> 6)) | (1ull << ((p + last) >> 6));
             }
             const uint64_t resm = ballot(valid && res);
@@ -821,8 +851,8 @@ struct Sim {
             const int b = ffs0(todo) * kWave;
             todo &= todo - 1;
             const int r = b + lane();
-            const uint32_t g = r < L ? S.gs[r] : 0u;
-            bool chg = false;
+            const uint32_t g = r < L ? S.q[r].x : 0u;
+            bool chg = false, fin = false;
             if (g & G_INB) {
                 R x;
                 ldr(S, r, x);
@@ -848,6 +878,7 @@ struct Sim {
                         tlast[idx] = t_end;
                         tbtw[idx] = x.tbt;
                         ndone++;
+                        fin = true;
                         if (r < lohole) lohole = r;
                     } else if (POL == P_BOOST) {
                         const int lo_ = (int)((x.gs >> G_LVL_SHIFT) & 31u);
@@ -867,13 +898,15 @@ struct Sim {
                 str(S, r, x);
             } else if (g & G_EVI) {
                 if (POL == P_SRPT) {
-                    const uint64_t pk = S.pk[r];
-                    S.pk[r] = pack((int64_t)S.w[r] + S.left[r] - 1, idx_of(pk));
+                    const uint4 qe = S.q[r];
+                    S.k[r] = pack((int64_t)(int)qe.y + (int)qe.w - 1, idx_of(S.k[r]));
                     chg = true;
                 }
-                S.gs[r] = g & ~G_EVI;
+                S.q[r].x = g & ~G_EVI;
             }
             if (chg && r < lo) lo = r;
+            const uint64_t fm = ballot(fin);
+            if (fm && vm_ok && lane() == (b >> 6)) vm_res &= ~fm, vm_ev &= ~fm;
         }
         wsync();
         if (ballot(bad_idx)) fail(S_ESTATE);
@@ -893,8 +926,9 @@ struct Sim {
     // into the staging slots and, beyond 64, the HBM overflow. Returns the
     // number extracted. No holes lie below `from`.
     DEV int compact_extract(int from) {
+        vm_ok = false;
         const int start = (from >> 6) << 6;
-        uint64_t pmax = start > 0 ? uniu(S.pk[start - 1]) : 0ull;
+        uint64_t pmax = start > 0 ? uniu(S.k[start - 1]) : 0ull;
         int out = start, nx = 0;
         for (int b = start; b < L; b += kWave) {
             const int r = b + lane();
@@ -1035,28 +1069,35 @@ struct Sim {
     }
 };
 
-__global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int inst = blockIdx.x;
-    if (inst >= a.n_inst) return;
-    const DevSetting &st = a.inst[inst];
+template <int BSH>
+DEV void run_instance(const SimArgs &a, const DevSetting &st, int inst, unsigned char *smem) {
     switch (st.policy) {
     case P_FCFS: {
-        Sim<P_FCFS> s(a, st, inst, smem);
+        Sim<P_FCFS, BSH> s(a, st, inst, smem);
         s.run();
         break;
     }
     case P_SRPT: {
-        Sim<P_SRPT> s(a, st, inst, smem);
+        Sim<P_SRPT, BSH> s(a, st, inst, smem);
         s.run();
         break;
     }
     default: {
-        Sim<P_BOOST> s(a, st, inst, smem);
+        Sim<P_BOOST, BSH> s(a, st, inst, smem);
         s.run();
         break;
     }
     }
+}
+
+__global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int inst = blockIdx.x;
+    if (inst >= a.n_inst) return;
+    if (a.retry && a.status[inst] != S_ECAPACITY) return;
+    const DevSetting &st = a.inst[inst];
+    if (a.bs == 16) run_instance<4>(a, st, inst, smem);
+    else run_instance<-1>(a, st, inst, smem);
 }
 
 }  // namespace

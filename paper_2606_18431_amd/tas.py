@@ -51,7 +51,7 @@ class tas_params(ctypes.Structure):
                 ("iter_tok_us", ctypes.c_int32), ("iter_ctx_div", ctypes.c_int32),
                 ("max_iters", ctypes.c_int64), ("tau_us", ctypes.c_double),
                 ("list_cap", ctypes.c_int32), ("spill_cap", ctypes.c_int32),
-                ("n_inst", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("n_inst", ctypes.c_int32), ("retry_cap", ctypes.c_int32),
                 ("inst", ctypes.c_void_p)]
 
 
@@ -136,13 +136,13 @@ def make_traces(arrival_us: np.ndarray, prompt: np.ndarray, decode: np.ndarray):
 
 
 def make_params(engine: W.Engine, settings: np.ndarray, list_cap: int = 0, spill_cap: int = 0,
-                max_iters: int | None = None):
+                max_iters: int | None = None, retry_cap: int = 0):
     """tas_params for an engine and a SETTING_DTYPE array; returns (struct, keepalive)."""
     s = np.ascontiguousarray(settings, W.SETTING_DTYPE)
     p = tas_params(engine.max_seqs, engine.max_tokens, engine.chunk, engine.kv_blocks,
                    engine.block_tokens, engine.iter_base_us, engine.iter_tok_us,
                    engine.iter_ctx_div, int(engine.max_iters if max_iters is None else max_iters),
-                   float(engine.tau_us), int(list_cap), int(spill_cap), len(s), 0,
+                   float(engine.tau_us), int(list_cap), int(spill_cap), len(s), int(retry_cap),
                    s.ctypes.data if len(s) else None)
     return p, s
 
@@ -213,14 +213,14 @@ class Simulation:
     """One workload on one GPU: workspace, outputs and the C-ABI calls."""
 
     def __init__(self, w: W.Workload, device="cuda", list_cap: int = 0, spill_cap: int = 0,
-                 max_iters: int | None = None):
+                 max_iters: int | None = None, retry_cap: int = 0):
         import torch
 
         self.w = w
         self.torch = torch
         self._tr, self._keep_t = make_traces(w.arrival_us, w.prompt, w.decode)
         self._pa, self._keep_p = make_params(w.engine, w.settings, list_cap, spill_cap,
-                                             max_iters)
+                                             max_iters, retry_cap)
         self.ws_bytes = tas_workspace_bytes(self._tr, self._pa)
         if self.ws_bytes == 0:
             raise TasError(TAS_EINVAL, "tas_workspace_bytes")

@@ -114,19 +114,34 @@ def test_parity_with_minimum_list(torch):
     assert_parity(w, g, o)
 
 
-def test_residents_beyond_list_fail_loudly(torch):
-    """Least-attained-service order with everyone arriving at once pauses
-    old residents behind fresh arrivals until more requests hold KV than the
-    on-chip list can hold: the instance reports TAS_ECAPACITY (the oracle has
-    no such limit and finishes)."""
-    n = 200
+def las_burst_workload(n=200):
+    """Least-attained-service order with everyone arriving at once pauses old
+    residents behind fresh arrivals, so more requests hold KV than max_seqs."""
     tb = [(23 - j) * 10 ** 11 for j in range(24)]
-    w = edge_workload(np.zeros(n), np.ones(n), np.full(n, 50),
-                      W.Engine(max_seqs=8, kv_blocks=4096, chunk=64, max_tokens=512),
-                      policies=[W.setting(0, W.BOOST, k=1, table=tb)])
-    assert oracle.run(w)["rc"] == 0
+    return edge_workload(np.zeros(n), np.ones(n), np.full(n, 50),
+                         W.Engine(max_seqs=8, kv_blocks=4096, chunk=64, max_tokens=512),
+                         policies=[W.setting(0, W.BOOST, k=1, table=tb),
+                                   W.setting(0, W.FCFS)])
+
+
+def test_residents_beyond_list_are_retried_exactly(torch):
+    """An instance whose residents outgrow the first-pass list reruns from
+    scratch in the second pass with the large list: exact results."""
+    w = las_burst_workload()
+    o = oracle.run(w)
+    assert o["rc"] == 0
     g = gpu_run(w, list_cap=72)
+    assert_parity(w, g, o)
+
+
+def test_residents_beyond_both_lists_fail_loudly(torch):
+    """Without room in the retry list either, the instance reports
+    TAS_ECAPACITY instead of a wrong schedule; the others are exact."""
+    w = las_burst_workload()
+    o = oracle.run(w)
+    g = gpu_run(w, list_cap=72, retry_cap=72)
     assert g["rc"] == -8 and g["status"][0] == -8
+    assert_parity(w, g, o, inst=[1])
 
 
 def edge_workload(arrival, prompt, decode, engine, policies=None):
@@ -196,7 +211,7 @@ def test_error_overflow(torch):
 def test_error_spill_capacity(torch):
     """A spill too small to hold the waiting queue is reported, not hidden."""
     w = W.make(2, n_traces=1, n_settings=4, n_req=3000)
-    g = gpu_run(w, list_cap=128, spill_cap=16)
+    g = gpu_run(w, list_cap=128, spill_cap=16, retry_cap=128)
     assert g["rc"] == -8 and np.any(g["status"] == -8)
 
 
