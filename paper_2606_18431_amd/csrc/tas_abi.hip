@@ -228,6 +228,7 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     a.M = p->max_seqs, a.T = p->max_tokens, a.c = p->chunk, a.Kb = p->kv_blocks;
     a.bs = p->block_tokens, a.base = p->iter_base_us, a.tok = p->iter_tok_us;
     a.div = p->iter_ctx_div, a.list_cap = lc, a.spill_cap = sc;
+    a.div_magic = a.div >= 2 ? ~0ull / (uint64_t)a.div + 1 : 0;
     a.ovf_stride = rc + tas::kStage, a.retry = 0;
     *out = c;
     return TAS_OK;

@@ -29,8 +29,8 @@ struct Rec {
     int32_t left;  // tokens still to emit
     int32_t kv;    // tokens with resident KV
     uint32_t gs;   // flags, guard, level and this iteration's chunk (see the kernel)
-    uint32_t tbt;  // max inter-token gap so far (us, saturating)
     uint32_t tl;   // time of the last emitted token, modulo 2^32 (us)
+    uint32_t unused;
 };
 
 struct SimArgs {
@@ -40,7 +40,7 @@ struct SimArgs {
     const DevSetting *inst;  // [n_inst]
     int64_t *tfirst;         // [n_inst][n_req] absolute time of the first token
     int64_t *tlast;          // [n_inst][n_req] absolute time of the last token
-    uint32_t *tbtw;          // [n_inst][n_req] max gap (working copy)
+    uint32_t *tbtw;          // [n_inst][n_req] max gap, raised by atomic max
     uint32_t *ttft;          // [n_inst][n_req] outputs, relative to arrival
     uint32_t *ttlt;
     uint32_t *tbtmax;
@@ -49,6 +49,7 @@ struct SimArgs {
     Rec *spill;              // [n_inst][spill_cap]
     Rec *ovf;                // [n_inst][ovf_stride]
     int64_t max_iters;
+    uint64_t div_magic;      // floor((2^64 - 1) / div) + 1 when div >= 2
     int32_t n_req;
     int32_t n_inst;
     int32_t M, T, c, Kb, bs, base, tok, div;
@@ -60,10 +61,10 @@ struct SimArgs {
 
 // Dynamic LDS bytes per workgroup for a list capacity.
 inline int64_t lds_bytes_for(int32_t list_cap) {
-    const int64_t cap = int64_t(list_cap) + 2 * kStage;  // list, its overflow region, staging
-    // pk (8 B) + w, left, kv, gs, tbt, tl (4 B) per slot; boost table;
-    // 256-bin histogram; a few scalars
-    return cap * (8 + 6 * 4) + kLevels * 8 + 256 * 4 + 64;
+    const int64_t cap = int64_t(list_cap) + kStage;  // the list and its overflow region
+    // pk (8 B) + gs, w, kv, left, tl (4 B) per slot; alignment of the boost
+    // table; the boost table
+    return cap * (8 + 5 * 4) + 8 + kLevels * 8;
 }
 constexpr int kMaxChunk = (1 << 15) - 1;  // the chunk size lives in 15 bits of the flag word
 // At most 64 chunks of 64 entries (list + overflow region): chunk bitmaps are

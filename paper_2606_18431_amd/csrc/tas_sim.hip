@@ -166,42 +166,41 @@ DEV int level_of(int w, int k, int lk) {
 
 // LDS holds the candidate list as three parallel arrays: a 16-byte quad
 // {gs, w, kv, left} (what formation reads, one 128-bit load per lane), the
-// packed key (searches and merges) and {tbt, tl} (emission only). Strides of
-// 16 and 8 bytes keep the 64 lanes of one access on distinct banks.
+// packed key (searches and merges) and the last token time tl (emission
+// only). The maximum inter-token gap lives in HBM, raised by atomic max, so
+// an entry takes 28 bytes of LDS.
 struct Lds {
     uint4 *q;
     uint64_t *k;
-    uint2 *tt;
+    uint32_t *tl;
     int64_t *bt;
-    uint32_t *hist;
 };
 
 struct R {  // one candidate-list record in registers
     uint64_t pk = 0;
     int w = 0, left = 0, kv = 0;
-    uint32_t gs = 0, tbt = 0, tl = 0;
+    uint32_t gs = 0, tl = 0;
 };
 
 DEV void ldr(const Lds &S, int i, R &x) {
     const uint4 q = S.q[i];
-    const uint2 t = S.tt[i];
     x.gs = q.x, x.w = (int)q.y, x.kv = (int)q.z, x.left = (int)q.w;
     x.pk = S.k[i];
-    x.tbt = t.x, x.tl = t.y;
+    x.tl = S.tl[i];
 }
 DEV void str(const Lds &S, int i, const R &x) {
     S.q[i] = make_uint4(x.gs, (uint32_t)x.w, (uint32_t)x.kv, (uint32_t)x.left);
     S.k[i] = x.pk;
-    S.tt[i] = make_uint2(x.tbt, x.tl);
+    S.tl[i] = x.tl;
 }
 DEV R from_rec(const Rec &r) {
     R x;
-    x.pk = r.pk, x.w = r.w, x.left = r.left, x.kv = r.kv, x.gs = r.gs, x.tbt = r.tbt, x.tl = r.tl;
+    x.pk = r.pk, x.w = r.w, x.left = r.left, x.kv = r.kv, x.gs = r.gs, x.tl = r.tl;
     return x;
 }
 DEV Rec to_rec(const R &x) {
     Rec r;
-    r.pk = x.pk, r.w = x.w, r.left = x.left, r.kv = x.kv, r.gs = x.gs, r.tbt = x.tbt, r.tl = x.tl;
+    r.pk = x.pk, r.w = x.w, r.left = x.left, r.kv = x.kv, r.gs = x.gs, r.tl = x.tl, r.unused = 0;
     return r;
 }
 DEV R shfl_rec(const R &x, int src) {
@@ -211,24 +210,51 @@ DEV R shfl_rec(const R &x, int src) {
     y.left = __shfl(x.left, src);
     y.kv = __shfl(x.kv, src);
     y.gs = (uint32_t)__shfl((int)x.gs, src);
-    y.tbt = (uint32_t)__shfl((int)x.tbt, src);
     y.tl = (uint32_t)__shfl((int)x.tl, src);
     return y;
 }
 DEV bool is_waiting(uint32_t g) { return (g & (G_RES | G_DONE)) == 0; }
 
+// Destination lanes of a wavefront permutation: the lanes in m go, in order,
+// to lanes base, base + 1, ...; the other lanes fill the remaining slots in
+// order. Requires base + popc(m) <= 64.
+DEV int place_dest(uint64_t m, int base) {
+    const int before = mbcnt(m);
+    if ((m >> lane()) & 1ull) return base + before;
+    const int k = lane() - before;  // rank among the lanes outside m
+    return k < base ? k : k + popc(m);
+}
+DEV uint32_t perm32(int dest, uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_ds_permute(dest * 4, (int)v);
+}
+// Move a record across lanes (a register transpose: no LDS storage is used).
+// Every lane must be active, and dest must be a permutation.
+DEV R permute_rec(const R &x, int dest) {
+    R y;
+    const uint32_t lo = perm32(dest, (uint32_t)x.pk), hi = perm32(dest, (uint32_t)(x.pk >> 32));
+    y.pk = ((uint64_t)hi << 32) | lo;
+    y.w = (int)perm32(dest, (uint32_t)x.w);
+    y.left = (int)perm32(dest, (uint32_t)x.left);
+    y.kv = (int)perm32(dest, (uint32_t)x.kv);
+    y.gs = perm32(dest, x.gs);
+    y.tl = perm32(dest, x.tl);
+    return y;
+}
+
 // ------------------------------------------------------------ the simulator
 
-// POL: policy. BSH: log2 of the KV block size when it is a power of two
-// (the common 16-token block gets its own instantiation), -1 otherwise.
-template <int POL, int BSH>
+// BSH: log2 of the KV block size when it is a power of two (the common
+// 16-token block gets its own instantiation), -1 otherwise. The policy is a
+// run-time value: one copy of the code serves every policy, so workgroups of
+// different policies on one compute unit share the instruction cache.
+template <int BSH>
 struct Sim {
     const SimArgs &A;
     Lds S;
-    // instance constants
-    int inst, N, M, T, c, Kb, bs, base, tok, div, k, lk, memguard, lcap, scap;
-    int sb;  // first staging slot: the list may use [0, lcap + kStage) during formation
+    // instance constants (memguard and delta are zero unless pol is BOOST)
+    int inst, N, M, T, c, Kb, bs, base, tok, div, pol, k, lk, memguard, lcap, scap;
     int64_t delta, max_iters;
+    uint64_t div_magic;  // ceil(2^64 / div) for div >= 2
     const int64_t *arr;
     const int32_t *Pp, *Dp;
     int64_t *tfirst, *tlast;
@@ -246,6 +272,9 @@ struct Sim {
     int64_t sum_ctx;
     uint64_t emit_chunks;  // 64-entry chunks holding batch members or evictions
     bool emit_all;         // ranks moved during formation: visit every chunk
+    // entries extracted by compact_extract, lanes [0, min(count, kStage));
+    // the rest go to the per-instance HBM overflow
+    R stage;
     // victim masks, lane c = chunk c: residents, and those a voluntary
     // eviction may take (MemGuard). Kept across iterations: bits change in
     // place on admission, eviction and completion; any edit that moves ranks
@@ -259,23 +288,24 @@ struct Sim {
         base = a.base, tok = a.tok, div = a.div, lcap = a.list_cap, scap = a.spill_cap;
         k = st.k > 0 ? st.k : 1;
         lk = 31 - __clz(k);
+        pol = st.policy;
         memguard = st.memguard;
         delta = st.delta;
         max_iters = a.max_iters;
+        div_magic = a.div_magic;
         const size_t toff = (size_t)st.trace * (size_t)N;
         arr = a.arrival + toff, Pp = a.prompt + toff, Dp = a.decode + toff;
         const size_t ioff = (size_t)i * (size_t)N;
         tfirst = a.tfirst + ioff, tlast = a.tlast + ioff, tbtw = a.tbtw + ioff;
         spill = a.spill + (size_t)i * (size_t)scap;
         ovf = a.ovf + (size_t)i * (size_t)a.ovf_stride;
-        sb = lcap + kStage;
-        const int cap = lcap + 2 * kStage;
+        const int cap = lcap + kStage;  // the list may use its overflow region during formation
         size_t o = 0;
         S.q = (uint4 *)(smem + o), o += (size_t)cap * 16;
         S.k = (uint64_t *)(smem + o), o += (size_t)cap * 8;
-        S.tt = (uint2 *)(smem + o), o += (size_t)cap * 8;
-        S.bt = (int64_t *)(smem + o), o += kLevels * 8;
-        S.hist = (uint32_t *)(smem + o);
+        S.tl = (uint32_t *)(smem + o), o += (size_t)cap * 4;
+        o = (o + 7) & ~(size_t)7;
+        S.bt = (int64_t *)(smem + o);
         for (int j = lane(); j < kLevels; j += kWave) S.bt[j] = st.bt[j];
         t = 0;
         U = L = nW = nR = n_holes = spill_n = next = pf = completed = status = 0;
@@ -294,9 +324,20 @@ struct Sim {
     DEV void fail(int code) {
         if (status == 0) status = code;
     }
+    // floor(s / div). Below 2^32 a multiply by the rounded-up reciprocal is
+    // exact: s * ceil(2^64/div) / 2^64 exceeds s/div by less than 2^-32 <= 1/div.
+    DEV uint64_t ctx_quot(uint64_t s) const {
+        if (div == 1) return s;
+        if (s >> 32) return s / (uint64_t)div;
+        const uint32_t x = (uint32_t)s;
+        return ((uint64_t)x * (div_magic >> 32) + __umulhi(x, (uint32_t)div_magic)) >> 32;
+    }
     DEV int blocks(int x) const {
-        if (BSH >= 0) return (x + (1 << BSH) - 1) >> BSH;
-        return (x + bs - 1) / bs;
+        if constexpr (BSH >= 0) {
+            return (x + (1 << BSH) - 1) >> BSH;
+        } else {
+            return (x + bs - 1) / bs;
+        }
     }
 
     // ---------------------------------------------------------- arrivals
@@ -315,9 +356,9 @@ struct Sim {
         x.w = P, x.left = D;
         int64_t key;
         uint32_t lvl = 0;
-        if (POL == P_FCFS) {
+        if (pol == P_FCFS) {
             key = a;
-        } else if (POL == P_SRPT) {
+        } else if (pol == P_SRPT) {
             key = (int64_t)P + D - 1;
         } else {
             lvl = (uint32_t)level_of(P, k, lk);
@@ -487,60 +528,48 @@ struct Sim {
                 spill_n += ns;
                 nW -= ns;
                 const uint64_t km = ballot(lane() < K && !toS);
-                if (lane() < K && !toS) str(S, sb + mbcnt(km), y);
-                wsync();
+                y = permute_rec(y, place_dest(km, 0));
                 K -= ns;
-                if (lane() < K) ldr(S, sb + lane(), y);
-                wsync();
             }
         }
         if (K > 0) merge_new(y, K);
         if (L > lcap) spill_excess();
     }
 
-    // The want-th smallest spilled key (radix select, 8 bits per pass).
+    // The want-th smallest spilled key: radix select over 4-bit digits, the
+    // 16 bin counts held one per lane (no LDS histogram).
     DEV uint64_t select_kth(int want) {
         hbm_fence();
         uint64_t prefix = 0;
         int rank = want;
-        for (int d = 7; d >= 0; d--) {
-            for (int j = lane(); j < 256; j += kWave) S.hist[j] = 0;
-            wsync();
-            const int sh = 8 * d;
+        for (int d = 15; d >= 0; d--) {
+            const int sh = 4 * d;
+            int cnt = 0;  // lane b < 16: matching entries whose digit is b
             for (int rd = 0; rd < spill_n; rd += kWave) {
                 const int i = rd + lane();
+                uint64_t key = 0;
+                bool match = false;
                 if (i < spill_n) {
-                    const uint64_t key = spill[i].pk;
-                    const bool match = (d == 7) || ((key >> (sh + 8)) == (prefix >> (sh + 8)));
-                    if (match) atomicAdd(&S.hist[(key >> sh) & 255u], 1u);
+                    key = spill[i].pk;
+                    match = d == 15 || (key >> (sh + 4)) == (prefix >> (sh + 4));
+                }
+                if (!ballot(match)) continue;
+                const int dig = (int)((key >> sh) & 15u);
+                for (int b = 0; b < 16; b++) {
+                    const int nb = popc(ballot(match && dig == b));
+                    if (lane() == b) cnt += nb;
                 }
             }
-            wsync();
-            const int l4 = 4 * lane();
-            const int h0 = (int)S.hist[l4], h1 = (int)S.hist[l4 + 1], h2 = (int)S.hist[l4 + 2],
-                      h3 = (int)S.hist[l4 + 3];
-            const int s = h0 + h1 + h2 + h3;
-            const int inc = scan_add(s);
-            const int exc = inc - s;
-            const uint64_t hm = ballot(exc < rank && rank <= inc);
+            const int inc = scan_add(lane() < 16 ? cnt : 0);
+            const int exc = inc - cnt;
+            const uint64_t hm = ballot(lane() < 16 && exc < rank && rank <= inc);
             if (hm == 0) {
                 fail(S_ESTATE);
                 return 0;
             }
-            const int ln = ffs0(hm);
-            int rr = rank - rl(exc, ln);
-            const int b0 = rl(h0, ln), b1 = rl(h1, ln), b2 = rl(h2, ln);
-            int bin = 4 * ln;
-            if (rr > b0) {
-                rr -= b0, bin++;
-                if (rr > b1) {
-                    rr -= b1, bin++;
-                    if (rr > b2) rr -= b2, bin++;
-                }
-            }
+            const int bin = ffs0(hm);
+            rank -= rl(exc, bin);
             prefix |= (uint64_t)bin << sh;
-            rank = rr;
-            wsync();
         }
         return prefix;
     }
@@ -563,7 +592,7 @@ struct Sim {
         for (int rd = 0; rd < n0; rd += kWave) {
             const int i = rd + lane();
             const bool v = i < n0;
-            Rec s;
+            Rec s = {};
             if (v) s = spill[i];
             const bool sel = v && s.pk <= theta;
             const bool keep = v && !sel;
@@ -576,11 +605,7 @@ struct Sim {
             wr += popc(km);
             const int ks = popc(sm);
             if (ks) {
-                if (sel) str(S, sb + mbcnt(sm), from_rec(s));
-                wsync();
-                R x;
-                if (lane() < ks) ldr(S, sb + lane(), x);
-                wsync();
+                const R x = permute_rec(from_rec(s), place_dest(sm, 0));
                 merge_new(x, ks);
                 got += ks;
             }
@@ -604,7 +629,7 @@ struct Sim {
             const uint32_t g = r < L ? S.q[r].x : 0u;
             const bool rs = (g & G_RES) != 0;
             bool ev = rs;
-            if (POL == P_BOOST && memguard) ev = rs && ((g >> G_LVL_SHIFT) & 31u) > (g & G_GUARD);
+            if (memguard) ev = rs && ((g >> G_LVL_SHIFT) & 31u) > (g & G_GUARD);
             const uint64_t m1 = ballot(rs), m2 = ballot(ev);
             if (lane() == c) vm_res = m1, vm_ev = m2;
         }
@@ -619,7 +644,7 @@ struct Sim {
         if (lane() == (r >> 6)) {
             if (resident) {
                 vm_res |= bit;
-                if (!(POL == P_BOOST && memguard)) vm_ev |= bit;
+                if (!memguard) vm_ev |= bit;
             } else {
                 vm_res &= ~bit;
                 vm_ev &= ~bit;
@@ -642,12 +667,12 @@ struct Sim {
     // Highest rank > q holding a resident outside the batch that may be
     // evicted for candidate q (voluntary: MemGuard and hysteresis apply).
     // The list is sorted, so the highest such rank is the worst (key, idx).
-    DEV int find_victim(int q, uint64_t pkq, bool voluntary) {
+    DEV int find_victim(int q, bool voluntary) {
         if (!vm_ok) build_victim_masks();
         const int v = top_above(voluntary ? vm_ev : vm_res, q);
-        if (POL == P_BOOST && voluntary && v >= 0 && delta > 0) {
+        if (voluntary && v >= 0 && delta > 0) {
             // the worst eligible key fails the hysteresis test => all fail
-            const uint64_t pv = uniu(S.k[v]);
+            const uint64_t pv = uniu(S.k[v]), pkq = uniu(S.k[q]);
             const int64_t kd = key_of(pv) - delta, kq = key_of(pkq);
             if (!(kd > kq || (kd == kq && idx_of(pv) > idx_of(pkq)))) return -1;
         }
@@ -660,7 +685,7 @@ struct Sim {
         const uint32_t g = (uint32_t)uni((int)qv.x);
         wsync();
         if (lane() == 0) {
-            S.q[v].x = (g & ~G_RES) | G_EVI | (POL == P_SRPT ? G_DIRTY : 0u);
+            S.q[v].x = (g & ~G_RES) | G_EVI | (pol == P_SRPT ? G_DIRTY : 0u);
             S.q[v].z = 0;
         }
         wsync();
@@ -692,21 +717,15 @@ struct Sim {
 
     // Candidate q did not fit: evictions, or closing admissions. r_ahead
     // counts residents at ranks > q.
-    DEV void slow_path(int q, bool &closed, int &r_ahead) {
-        const uint4 qq = S.q[q];
-        const uint32_t g = (uint32_t)uni((int)qq.x);
-        const int w = uni((int)qq.y);
-        const int kvv = uni((int)qq.z);
-        const uint64_t pkq = uniu(S.k[q]);
+    // (g, n, du, kvv: its flag word, chunk size, KV blocks and KV tokens)
+    DEV void slow_path(int q, uint32_t g, int n, int du, int kvv, bool &closed, int &r_ahead) {
         const bool res = (g & G_RES) != 0;
-        const int n = min(min(w - kvv, c), T - used);
-        const int du = blocks(kvv + n) - blocks(kvv);
         for (int it = 0; it <= L + 1; it++) {
             if (U + du <= Kb) {
                 admit_one(q, g, n, du, kvv);
                 return;
             }
-            int v = find_victim(q, pkq, true);
+            int v = find_victim(q, true);
             if (v >= 0) {
                 do_evict(v);
                 r_ahead--;
@@ -714,7 +733,7 @@ struct Sim {
                 continue;
             }
             if (res) {
-                v = find_victim(q, pkq, false);
+                v = find_victim(q, false);
                 if (v >= 0) {
                     do_evict(v);
                     r_ahead--;
@@ -761,35 +780,51 @@ struct Sim {
         int r_ahead = nR;  // residents at ranks >= p
         int p = 0;
         int bstar = spill_n > 0 ? lower_bound(spill_min) : INT32_MAX;
+        // the next chunk's records, loaded while this one is processed; valid
+        // while formation walks whole chunks without touching the list
+        const int lim = lcap + kStage;
+        uint4 nx = make_uint4(0u, 0u, 0u, 0u);
+        bool have_nx = false;
         for (int guard = 0; guard < (1 << 22); guard++) {
             if (cnt >= M || used >= T || (closed && r_ahead <= 0)) break;
             if (!closed && p >= bstar) {  // bstar <= L: spilled entries come next
                 mid_refill(p);
                 if (status) return;
                 bstar = spill_n > 0 ? lower_bound(spill_min) : INT32_MAX;
+                have_nx = false;
                 continue;
             }
             if (p >= L) break;
             const int end = closed ? L : min(L, bstar);
             const int r = p + lane();
             const bool valid = r < end;
-            uint4 qr = make_uint4(0u, 0u, 0u, 0u);
-            if (valid) qr = S.q[r];
-            const uint32_t g = qr.x;
+            uint4 qr = nx;
+            if (!have_nx) {
+                qr = make_uint4(0u, 0u, 0u, 0u);
+                if (r < lim) qr = S.q[r];
+            }
+            if (r + kWave < lim) nx = S.q[r + kWave];
+            const uint32_t g = valid ? qr.x : 0u;
             const int w = (int)qr.y;
             const int kvv = (int)qr.z;
             const bool res = (g & G_RES) != 0;
             const bool cand = valid && !(g & (G_EVI | G_DONE)) && (res || !closed);
+            // one round of scans: the candidates admitted from this chunk
+            // are a prefix of its candidates, and only the last of them can
+            // be clipped by the token budget
             const int m = cand ? min(w - kvv, c) : 0;
-            const int ci = scan_add(cand ? 1 : 0);
+            const int kvc = cand ? kvv : 0;
+            const int dfull = cand ? blocks(kvv + m) - blocks(kvv) : 0;
             const int mi = scan_add(m);
-            const int cb = cnt + ci - (cand ? 1 : 0);
+            const int dfi = scan_add(dfull);
+            const int kvi = scan_add(kvc);
+            const uint64_t cm = ballot(cand);
+            const int cb = cnt + mbcnt(cm);
             const int ub = used + mi - m;
             const bool adm = cand && cb < M && ub < T;
             const int n = adm ? min(m, T - ub) : 0;
             const int du = adm ? blocks(kvv + n) - blocks(kvv) : 0;
-            const int dui = scan_add(du);
-            const int kvi = scan_add(adm ? kvv : 0);
+            const int dui = dfi - dfull + du;
             const bool fit = U + dui <= Kb;
             const uint64_t bad = ballot(adm && !fit);
             const uint64_t am = ballot(adm);
@@ -803,7 +838,8 @@ struct Sim {
             if (okm) {
                 const int last = fls0(okm);
                 const int used_new = rl(ub + n, last);
-                const int nadm_w = popc(ballot(ok && !res));
+                const uint64_t nm = ballot(ok && !res);
+                const int nadm_w = popc(nm);
                 cnt += popc(okm);
                 sum_ctx += rl(kvi, last) + (used_new - used);
                 used = used_new;
@@ -811,11 +847,10 @@ struct Sim {
                 nW -= nadm_w;
                 nR += nadm_w;
                 if (vm_ok && nadm_w) {  // dispatched waiting entries become residents
-                    const uint64_t nm = ballot(ok && !res);
                     // lanes of this chunk land in aligned chunks p>>6 and (p>>6)+1
                     const int c0 = p >> 6, sh = p & 63;
                     const uint64_t lo = nm << sh, hi = sh ? (nm >> (64 - sh)) : 0ull;
-                    const bool ev_too = !(POL == P_BOOST && memguard);
+                    const bool ev_too = !memguard;
                     if (lane() == c0) vm_res |= lo, vm_ev |= ev_too ? lo : 0ull;
                     if (lane() == c0 + 1) vm_res |= hi, vm_ev |= ev_too ? hi : 0ull;
                 }
@@ -828,12 +863,16 @@ struct Sim {
                 // residents among lanes [0, ql] are passed (q included if resident);
                 // waiting entries admitted in this chunk sit below q
                 r_ahead -= popc(resm & (ql == 63 ? ~0ull : ((2ull << ql) - 1ull)));
-                slow_path(p + ql, closed, r_ahead);
+                slow_path(p + ql, (uint32_t)rl((int)g, ql), rl(n, ql), rl(du, ql), rl(kvv, ql),
+                          closed, r_ahead);
                 if (status) return;
                 p = p + ql + 1;
+                have_nx = false;
             } else {
                 r_ahead -= popc(resm);
-                p = min(p + kWave, end);
+                const int p2 = min(p + kWave, end);
+                have_nx = p2 == p + kWave;
+                p = p2;
             }
         }
     }
@@ -842,83 +881,98 @@ struct Sim {
 
     // Returns the lowest rank whose key moved (INT32_MAX if none).
     DEV int emission(int64_t t_end) {
-        int lo = INT32_MAX, ufree = 0, ndone = 0, lohole = INT32_MAX;
+        int lo = INT32_MAX, lohole = INT32_MAX, nd = 0, ufree = 0;
         bool bad_idx = false;
         const uint32_t t32 = (uint32_t)t_end;
         const int nch = (L + kWave - 1) >> 6;
         uint64_t todo = emit_all ? (nch >= 64 ? ~0ull : ((1ull << nch) - 1ull)) : emit_chunks;
-        while (todo) {
-            const int b = ffs0(todo) * kWave;
+        if (!todo) return INT32_MAX;
+        // chunks are visited in ascending order, the next one's records loaded
+        // while this one is processed (a chunk's edits stay inside it)
+        int b = ffs0(todo) * kWave;
+        todo &= todo - 1;
+        uint4 q = make_uint4(0u, 0u, 0u, 0u);
+        uint64_t pk = 0;
+        uint32_t tl = 0;
+        if (b + lane() < L) q = S.q[b + lane()], pk = S.k[b + lane()], tl = S.tl[b + lane()];
+        for (;;) {
+            const int bn = todo ? ffs0(todo) * kWave : -1;
             todo &= todo - 1;
+            uint4 qn = make_uint4(0u, 0u, 0u, 0u);
+            uint64_t pkn = 0;
+            uint32_t tln = 0;
+            if (bn >= 0 && bn + lane() < L)
+                qn = S.q[bn + lane()], pkn = S.k[bn + lane()], tln = S.tl[bn + lane()];
             const int r = b + lane();
-            const uint32_t g = r < L ? S.q[r].x : 0u;
+            const uint32_t g = q.x;
             bool chg = false, fin = false;
             if (g & G_INB) {
-                R x;
-                ldr(S, r, x);
-                x.kv += (int)(x.gs >> G_N_SHIFT);
-                x.gs &= G_LOW & ~G_INB;
-                const int idx = idx_of(x.pk);
+                int w = (int)q.y, kv = (int)q.z + (int)(g >> G_N_SHIFT), left = (int)q.w;
+                uint32_t gs = g & G_LOW & ~G_INB;
+                const int idx = idx_of(pk);
                 if (idx >= N) bad_idx = true;
-                if (x.kv == x.w && idx < N) {
-                    x.w++;
-                    x.left--;
-                    if (!(x.gs & G_FIRST)) {
-                        x.gs |= G_FIRST;
+                bool emit = false;
+                if (kv == w && idx < N) {
+                    emit = true;
+                    w++;
+                    left--;
+                    if (!(gs & G_FIRST)) {
+                        gs |= G_FIRST;
                         tfirst[idx] = t_end;
                     } else {
-                        const uint32_t gp = t32 - x.tl;  // gaps beyond 2^32 overflow TTLT too
-                        if (gp > x.tbt) x.tbt = gp;
+                        // gaps beyond 2^32 overflow TTLT too; tbtw starts at 0
+                        atomicMax(&tbtw[idx], t32 - tl);
                     }
-                    x.tl = t32;
-                    if (x.left == 0) {
-                        x.gs = (x.gs | G_DONE) & ~G_RES;
-                        ufree += blocks(x.kv);
-                        x.kv = 0;
+                    if (left == 0) {
+                        gs = (gs | G_DONE) & ~G_RES;
+                        ufree += blocks(kv);
+                        kv = 0;
                         tlast[idx] = t_end;
-                        tbtw[idx] = x.tbt;
-                        ndone++;
                         fin = true;
-                        if (r < lohole) lohole = r;
-                    } else if (POL == P_BOOST) {
-                        const int lo_ = (int)((x.gs >> G_LVL_SHIFT) & 31u);
-                        const int ln = level_of(x.w, k, lk);
+                    } else if (pol == P_BOOST) {
+                        const int lo_ = (int)((gs >> G_LVL_SHIFT) & 31u);
+                        const int ln = level_of(w, k, lk);
                         if (ln != lo_) {
-                            const int64_t key = key_of(x.pk) + S.bt[lo_] - S.bt[ln];
-                            x.pk = pack(key, idx);
-                            x.gs = (x.gs & ~G_LVL) | ((uint32_t)ln << G_LVL_SHIFT) | G_DIRTY;
+                            pk = pack(key_of(pk) + S.bt[lo_] - S.bt[ln], idx);
+                            gs = (gs & ~G_LVL) | ((uint32_t)ln << G_LVL_SHIFT) | G_DIRTY;
                             chg = true;
                         }
                     }
                 }
-                if (POL == P_SRPT && !(x.gs & G_DONE)) {
-                    x.pk = pack((int64_t)x.w + x.left - 1 - x.kv, idx);
+                if (pol == P_SRPT && !(gs & G_DONE)) {
+                    pk = pack((int64_t)w + left - 1 - kv, idx);
                     chg = true;
                 }
-                str(S, r, x);
+                S.q[r] = make_uint4(gs, (uint32_t)w, (uint32_t)kv, (uint32_t)left);
+                if (chg) S.k[r] = pk;
+                if (emit) S.tl[r] = t32;
             } else if (g & G_EVI) {
-                if (POL == P_SRPT) {
-                    const uint4 qe = S.q[r];
-                    S.k[r] = pack((int64_t)(int)qe.y + (int)qe.w - 1, idx_of(S.k[r]));
+                if (pol == P_SRPT) {
+                    S.k[r] = pack((int64_t)(int)q.y + (int)q.w - 1, idx_of(pk));
                     chg = true;
                 }
                 S.q[r].x = g & ~G_EVI;
             }
-            if (chg && r < lo) lo = r;
-            const uint64_t fm = ballot(fin);
-            if (fm && vm_ok && lane() == (b >> 6)) vm_res &= ~fm, vm_ev &= ~fm;
+            const uint64_t cm = ballot(chg), fm = ballot(fin);
+            if (cm && lo == INT32_MAX) lo = b + ffs0(cm);
+            if (fm) {
+                if (lohole == INT32_MAX) lohole = b + ffs0(fm);
+                nd += popc(fm);
+                if (vm_ok && lane() == (b >> 6)) vm_res &= ~fm, vm_ev &= ~fm;
+            }
+            if (bn < 0) break;
+            b = bn, q = qn, pk = pkn, tl = tln;
         }
         wsync();
         if (ballot(bad_idx)) fail(S_ESTATE);
-        const int nd = wsum(ndone);
         if (nd) {
             U -= wsum(ufree);
             completed += nd;
             nR -= nd;
             n_holes += nd;
-            lo_hole = min(lo_hole, wmin(lohole));
+            lo_hole = min(lo_hole, lohole);
         }
-        return wmin(lo);
+        return lo;
     }
 
     // From rank `from` on: remove holes; extract entries whose key moved
@@ -952,10 +1006,14 @@ struct Sim {
             if (ext) {
                 y.gs &= ~G_DIRTY;
                 const int xi = nx + mbcnt(xm);
-                if (xi < kStage) str(S, sb + xi, y);
-                else ovf[xi - kStage] = to_rec(y);
+                if (xi >= kStage) ovf[xi - kStage] = to_rec(y);
             }
             wsync();
+            if (xm && nx < kStage) {  // the first kStage extracted stay in registers
+                const uint64_t sm = ballot(ext && nx + mbcnt(xm) < kStage);
+                const R z = permute_rec(y, place_dest(sm, nx));
+                if (lane() >= nx && lane() < nx + popc(sm)) stage = z;
+            }
             const uint64_t cm = rlu(inc, 63);
             if (cm > pmax) pmax = cm;
             out += popc(km);
@@ -973,13 +1031,10 @@ struct Sim {
             if (nx > kStage) hbm_fence();
             if (L > lcap) spill_excess();  // a refill during formation used the overflow region
             if (nx > 0 && status == 0) {
-                const int k0 = min(nx, kStage);
-                R x;
-                if (lane() < k0) ldr(S, sb + lane(), x);
-                wsync();
-                add_entries(x, k0);
+                add_entries(stage, min(nx, kStage));
                 for (int b = kStage; b < nx && status == 0; b += kStage) {
                     const int kb = min(nx - b, kStage);
+                    R x;
                     if (lane() < kb) x = from_rec(ovf[b - kStage + lane()]);
                     add_entries(x, kb);
                 }
@@ -991,6 +1046,7 @@ struct Sim {
     // ---------------------------------------------------------- driver
 
     DEV void run() {
+        for (int i = lane(); i < N; i += kWave) tbtw[i] = 0u;
         load_pf();
         take_arrivals();
         for (;;) {
@@ -1025,7 +1081,7 @@ struct Sim {
                 break;
             }
             if (U > maxU) maxU = U;
-            const int64_t dt = (int64_t)base + (int64_t)tok * used + sum_ctx / div;
+            const int64_t dt = (int64_t)base + (int64_t)tok * used + (int64_t)ctx_quot((uint64_t)sum_ctx);
             const int64_t t_end = t + dt;
             const int lo_mod = emission(t_end);
             t = t_end;
@@ -1071,23 +1127,8 @@ struct Sim {
 
 template <int BSH>
 DEV void run_instance(const SimArgs &a, const DevSetting &st, int inst, unsigned char *smem) {
-    switch (st.policy) {
-    case P_FCFS: {
-        Sim<P_FCFS, BSH> s(a, st, inst, smem);
-        s.run();
-        break;
-    }
-    case P_SRPT: {
-        Sim<P_SRPT, BSH> s(a, st, inst, smem);
-        s.run();
-        break;
-    }
-    default: {
-        Sim<P_BOOST, BSH> s(a, st, inst, smem);
-        s.run();
-        break;
-    }
-    }
+    Sim<BSH> s(a, st, inst, smem);
+    s.run();
 }
 
 __global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {

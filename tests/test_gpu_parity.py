@@ -187,6 +187,30 @@ def test_edge_cases(torch, name):
     assert_parity(w, g, o)
 
 
+@pytest.mark.parametrize("div", [1, 2, 3, 7, 64, 100, 997, (1 << 20) + 7, (1 << 31) - 1])
+def test_cost_model_divisors(torch, div):
+    """floor(sum(kv + n) / div) for divisors from 1 to 2^31 - 1."""
+    a, p, d = W.small_random(7, 400, rate_per_s=60.0)
+    e = W.Engine(max_seqs=16, kv_blocks=300, chunk=64, max_tokens=256, iter_ctx_div=div)
+    w = edge_workload(a, p, d, e)
+    o = oracle.run(w)
+    assert o["rc"] == 0
+    assert_parity(w, gpu_run(w), o)
+
+
+def test_context_sum_beyond_32_bits(torch):
+    """300 resident prompts of 2^24 - 3 tokens: the batch's summed context
+    passes 2^32 during prefill."""
+    n, P = 300, (1 << 24) - 3
+    e = W.Engine(max_seqs=n, max_tokens=n * 32767, chunk=32767,
+                 kv_blocks=n * ((P + 1 + 15) // 16), iter_tok_us=0, iter_ctx_div=(1 << 31) - 1)
+    w = edge_workload(np.zeros(n), np.full(n, P), np.full(n, 2), e)
+    o = oracle.run(w)
+    assert o["rc"] == 0
+    assert o["counters"][:, 0].max() > 500
+    assert_parity(w, gpu_run(w), o)
+
+
 def test_more_than_64_arrivals_at_once(torch):
     a = np.concatenate([np.zeros(150), np.full(200, 50_000)])
     w = edge_workload(a, np.full(350, 20), np.full(350, 5),
