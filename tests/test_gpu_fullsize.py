@@ -1,0 +1,77 @@
+"""Parity at the full sizes of the five workloads, in the launch configuration
+the benchmark times (every instance of the sweep in one tas_run, default list
+capacity), checked against the CPU oracle on a sample of instances.
+
+The GPU simulates the whole sweep; the oracle recomputes the sampled
+instances one by one. Every sampled instance must match exactly: per-request
+TTFT, TTLT and maximum gap, the eight counters and the nine percentiles. The
+sample covers every policy variant (FCFS, SRPT, UniBoost and vanilla boost at
+the smallest and largest gamma) on the first and the last trace, plus seeded
+random instances. Every instance's status must be TAS_OK.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_18431_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def sample_instances(w, n_random=4, seed=0):
+    S = w.meta["n_settings"]
+    T = w.n_traces
+    pick = set()
+    for t in (0, T - 1):
+        for s in sorted({0, 1, 2, 3, S - 2, S - 1}):
+            if s < S:
+                pick.add(t * S + s)
+    rng = np.random.default_rng([1234, seed, w.meta["cfg"]])
+    pick.update(int(i) for i in rng.choice(w.n_inst, size=min(n_random, w.n_inst), replace=False))
+    return np.array(sorted(pick), np.int64)
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_full_size_sampled_parity(torch, cfg):
+    from paper_2606_18431_amd import tas
+
+    w = W.make(cfg)
+    print(f"[gpu] full-size {W.NAMES[cfg]}: {w.n_inst} instances x {w.n_req} requests", flush=True)
+    sim = tas.Simulation(w)
+    sim.step()
+    n, m = w.n_inst, w.n_req
+    dev = sim.pct.device
+    lat = [torch.empty((n, m), dtype=torch.int32, device=dev) for _ in range(3)]
+    tas.tas_latencies(sim.ctx, *lat)
+    g = sim.results(latencies=False)
+    assert g["rc"] == 0, tas.tas_strerror(g["rc"])
+    assert (g["status"] == 0).all()
+    sel = sample_instances(w)
+    idx = torch.as_tensor(sel, device=dev)
+    got = {k: t.index_select(0, idx).cpu().numpy().view(np.uint32)
+           for k, t in zip(("ttft", "ttlt", "tbtmax"), lat)}
+    sim.close()
+    del lat
+    o = oracle.run(w.subset(sel), n_threads=min(16, os.cpu_count() or 1))
+    assert o["rc"] == 0
+    for j, i in enumerate(sel):
+        for key in ("ttft", "ttlt", "tbtmax"):
+            if not np.array_equal(got[key][j], o[key][j]):
+                bad = np.nonzero(got[key][j] != o[key][j])[0]
+                raise AssertionError(f"instance {i} {key}: {len(bad)} differ, first request "
+                                     f"{bad[0]}: gpu {got[key][j][bad[0]]} oracle "
+                                     f"{o[key][j][bad[0]]}")
+        assert np.array_equal(g["counters"][i], o["counters"][j]), (i, g["counters"][i],
+                                                                    o["counters"][j])
+        assert np.array_equal(g["pct"][i], o["pct"][j]), (i, g["pct"][i], o["pct"][j])
