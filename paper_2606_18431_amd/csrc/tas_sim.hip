@@ -37,6 +37,8 @@ namespace tas {
 namespace {
 
 #define DEV __device__ __forceinline__
+#define UNLIKELY(x) __builtin_expect(!!(x), 0)
+#define LIKELY(x) __builtin_expect(!!(x), 1)
 
 // record flag word (gs)
 constexpr uint32_t G_GUARD = 0x1fu;      // MemGuard level at the latest dispatch
@@ -381,7 +383,7 @@ struct Sim {
             const int r = pf + lane();
             const bool arrive = lane() >= off && r < N && pa <= t;
             const int n_arr = popc(ballot(arrive));
-            if (n_arr == 0) return;
+            if (LIKELY(n_arr == 0)) return;
             const R x = new_record(r, pa, pP, pD);
             const R y = off ? shfl_rec(x, min(off + lane(), kWave - 1)) : x;
             nW += n_arr;
@@ -668,7 +670,7 @@ struct Sim {
     // evicted for candidate q (voluntary: MemGuard and hysteresis apply).
     // The list is sorted, so the highest such rank is the worst (key, idx).
     DEV int find_victim(int q, bool voluntary) {
-        if (!vm_ok) build_victim_masks();
+        if (UNLIKELY(!vm_ok)) build_victim_masks();
         const int v = top_above(voluntary ? vm_ev : vm_res, q);
         if (voluntary && v >= 0 && delta > 0) {
             // the worst eligible key fails the hysteresis test => all fail
@@ -787,7 +789,7 @@ struct Sim {
         bool have_nx = false;
         for (int guard = 0; guard < (1 << 22); guard++) {
             if (cnt >= M || used >= T || (closed && r_ahead <= 0)) break;
-            if (!closed && p >= bstar) {  // bstar <= L: spilled entries come next
+            if (UNLIKELY(!closed && p >= bstar)) {  // bstar <= L: spilled entries come next
                 mid_refill(p);
                 if (status) return;
                 bstar = spill_n > 0 ? lower_bound(spill_min) : INT32_MAX;
@@ -846,7 +848,7 @@ struct Sim {
                 U += rl(dui, last);
                 nW -= nadm_w;
                 nR += nadm_w;
-                if (vm_ok && nadm_w) {  // dispatched waiting entries become residents
+                if (UNLIKELY(vm_ok && nadm_w)) {  // dispatched waiting entries become residents
                     // lanes of this chunk land in aligned chunks p>>6 and (p>>6)+1
                     const int c0 = p >> 6, sh = p & 63;
                     const uint64_t lo = nm << sh, hi = sh ? (nm >> (64 - sh)) : 0ull;
@@ -921,7 +923,8 @@ struct Sim {
                         tfirst[idx] = t_end;
                     } else {
                         // gaps beyond 2^32 overflow TTLT too; tbtw starts at 0
-                        atomicMax(&tbtw[idx], t32 - tl);
+                        __hip_atomic_fetch_max(&tbtw[idx], t32 - tl, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_WORKGROUP);
                     }
                     if (left == 0) {
                         gs = (gs | G_DONE) & ~G_RES;
@@ -1026,7 +1029,7 @@ struct Sim {
     }
 
     DEV void maintenance(int lo_mod) {
-        if (lo_mod < L || n_holes >= kHoleLimit || L > lcap) {
+        if (UNLIKELY(lo_mod < L || n_holes >= kHoleLimit || L > lcap)) {
             const int nx = compact_extract(min(min(lo_mod, lo_hole), L));
             if (nx > kStage) hbm_fence();
             if (L > lcap) spill_excess();  // a refill during formation used the overflow region
@@ -1051,7 +1054,7 @@ struct Sim {
         take_arrivals();
         for (;;) {
             if (status) break;
-            if (nW + nR == 0) {
+            if (UNLIKELY(nW + nR == 0)) {
                 if (spill_n > 0) {
                     refill();
                     if (status) break;
@@ -1111,7 +1114,8 @@ struct Sim {
                     if (f < 0 || f > 0xFFFFFFFFll || l < 0 || l > 0xFFFFFFFFll) bad = true;
                     A.ttft[ioff + i] = (uint32_t)f;
                     A.ttlt[ioff + i] = (uint32_t)l;
-                    A.tbtmax[ioff + i] = tbtw[i];
+                    A.tbtmax[ioff + i] =
+                        __hip_atomic_load(&tbtw[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
             if (ballot(bad)) fail(S_EOVERFLOW);
