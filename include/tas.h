@@ -13,6 +13,13 @@
  *       TAS_FCFS   key = a_i                                   (Table 1, FCFS)
  *       TAS_SRPT   key = P_i + D_i - 1 - kv_i  (exact remaining tokens;
  *                  Table 1, SRPT with perfect length knowledge)
+ *       TAS_SPF    key = P_i                (Table 1, shortest prefix first)
+ *       TAS_SJF    key = D_i   (Table 1, SJF with perfect output-length rank)
+ *       TAS_LAS    key = P_i + dec_i        (Table 1 and baselines, least
+ *                  attained service)
+ *       TAS_TRAIL  key as TAS_SRPT; a resident that emitted at least 0.6 D_i
+ *                  tokens is never a voluntary victim (baselines, TRAIL+
+ *                  swap-prevention threshold)
  *       TAS_BOOST  key = a_i - boost_us[level(P_i + dec_i)]    (Phase 2 unified
  *                  key Phi = a - b_gamma(w~) with w~ = max(w, s_pre); Phase 3
  *                  MemGuard quantization level = floor(log2(max(w,k)/k)))
@@ -67,7 +74,8 @@ enum {
     TAS_ECAPACITY = -8    /* an instance outgrew its on-chip candidate list    */
 };
 
-enum { TAS_FCFS = 0, TAS_SRPT = 1, TAS_BOOST = 2 };
+enum { TAS_FCFS = 0, TAS_SRPT = 1, TAS_BOOST = 2, TAS_SPF = 3, TAS_SJF = 4, TAS_LAS = 5,
+       TAS_TRAIL = 6 };
 
 #define TAS_LEVELS 24
 
@@ -84,7 +92,7 @@ typedef struct {
 /* One instance: a trace and a policy setting. */
 typedef struct {
     int32_t trace;    /* index into the traces                                 */
-    int32_t policy;   /* TAS_FCFS, TAS_SRPT or TAS_BOOST                       */
+    int32_t policy;   /* one of the TAS_FCFS .. TAS_TRAIL policies above       */
     int32_t k;        /* MemGuard granularity in tokens (BOOST), >= 1          */
     int32_t memguard; /* 1: a dispatched request is non-evictable until its
                          level passes the level it was dispatched at (BOOST)  */
@@ -137,7 +145,7 @@ size_t tas_workspace_bytes(const tas_traces *traces, const tas_params *params);
  * Returns TAS_EINVAL if: n_req < 1 or >= 2^20; an arrival is negative,
  * >= 2^41 or out of order; P or D < 1; P + D >= 2^24; a trace index is out of
  * range; policy unknown; k < 1 (BOOST); delta < 0; memguard or delta nonzero
- * for FCFS/SRPT; gamma <= 0 without table_given (BOOST); an explicit table not
+ * for a policy other than BOOST; gamma <= 0 without table_given (BOOST); an explicit table not
  * non-increasing or outside [0, 2^42]; chunk > max_tokens; any engine limit
  * < 1; chunk > 32767; tau <= 0; list_cap < max_seqs + 64 or > 4032.
  * TAS_EINFEASIBLE if ceil((P + D - 1) / block_tokens) > kv_blocks for some

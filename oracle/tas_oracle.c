@@ -36,6 +36,17 @@
  *   - the iteration that completes the prefill emits the first token; times
  *     are iteration ends; arrivals join at the next iteration start
  *   - SRPT key = remaining computed tokens P + D - 1 - kv; FCFS key = a_i
+ *
+ * Comparison policies (paper: Table 1 and the baselines of the evaluation):
+ *   SPF   shortest prompt first: key = P (static)
+ *   SJF   shortest job first with perfect knowledge of the output length (the
+ *         ranking LTR learns): key = D (static); the starvation quantum of
+ *         LTR+ is not modelled
+ *   LAS   least attained service: key = P + dec, the same signal as the boost
+ *         (grows with every emitted token)
+ *   TRAIL SRPT with perfect knowledge plus the swap-prevention threshold: a
+ *         resident that has emitted at least 0.6 D tokens is never a voluntary
+ *         victim (5 dec >= 3 D)
  */
 #include "tas_oracle.h"
 
@@ -45,7 +56,7 @@
 #include <string.h>
 
 enum { PENDING = 0, WAITING = 1, RESIDENT = 2, DONE = 3 };
-enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2 };
+enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2, P_SPF = 3, P_SJF = 4, P_LAS = 5, P_TRAIL = 6 };
 
 typedef struct {
     int32_t N;
@@ -123,7 +134,14 @@ static int64_t key_of(const inst_t *I, int32_t r, const req_t *q) {
     case P_FCFS:
         return I->a[r];
     case P_SRPT:
+    case P_TRAIL:
         return (int64_t)I->P[r] + I->D[r] - 1 - q->kv;
+    case P_SPF:
+        return I->P[r];
+    case P_SJF:
+        return I->D[r];
+    case P_LAS:
+        return (int64_t)I->P[r] + q->dec;
     default:
         return I->a[r] - I->bt[level_of((int64_t)I->P[r] + q->dec, I->k)];
     }
@@ -229,6 +247,8 @@ static int simulate(const inst_t *I, uint32_t *ttft, uint32_t *ttlt, uint32_t *t
                     if (I->memguard &&
                         !(level_of((int64_t)I->P[x] + p->dec, I->k) > p->guard))
                         continue;
+                    if (I->policy == P_TRAIL && 5 * (int64_t)p->dec >= 3 * (int64_t)I->D[x])
+                        continue; /* past the swap-prevention threshold */
                     if (!lex_gt(p->key - I->delta, x, q->key, r)) continue;
                     if (v < 0 || lex_gt(p->key, x, R[v].key, v)) v = x;
                 }
@@ -443,7 +463,7 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
                    int32_t n_threads) {
     if (n_traces < 1 || n_req < 1 || n_inst < 0) return TOR_EINVAL;
     for (int32_t i = 0; i < n_inst; i++)
-        if (trace[i] < 0 || trace[i] >= n_traces || policy[i] < 0 || policy[i] > 2 || k[i] < 1)
+        if (trace[i] < 0 || trace[i] >= n_traces || policy[i] < 0 || policy[i] > 6 || k[i] < 1)
             return TOR_EINVAL;
     if (eng[0] < 1 || eng[1] < 1 || eng[2] < 1 || eng[2] > eng[1] || eng[3] < 1 || eng[4] < 1 ||
         eng[5] < 1 || eng[6] < 0 || eng[7] < 1)

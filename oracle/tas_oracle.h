@@ -15,7 +15,8 @@
  * All arguments are host pointers. Arrays are flat, C-contiguous:
  *   arrival [n_traces*n_req] int64 us, non-decreasing within a trace
  *   prompt, decode [n_traces*n_req] int32 tokens, >= 1
- *   per instance i: trace[i], policy[i] (0 FCFS, 1 SRPT, 2 BOOST), k[i] >= 1,
+ *   per instance i: trace[i], policy[i] (0 FCFS, 1 SRPT, 2 BOOST, 3 SPF,
+ *   4 SJF, 5 LAS, 6 TRAIL), k[i] >= 1,
  *   memguard[i] in {0,1}, delta[i] >= 0 us, table[i*24 .. i*24+23] int64 us
  *   eng[8] = {max_seqs, max_tokens, chunk, kv_blocks, block_tokens,
  *             iter_base_us, iter_tok_us, iter_ctx_div}

@@ -56,7 +56,12 @@ constexpr uint32_t G_LOW = (1u << G_N_SHIFT) - 1;
 constexpr int kHoleLimit = 16;           // compact once this many holes accumulate
 
 enum { S_OK = 0, S_EOVERFLOW = -5, S_ELIVELOCK = -6, S_ESTATE = -7, S_ECAPACITY = -8 };
-enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2 };
+// Policies: the paper's boosted priority (BOOST), its comparators FCFS and
+// oracle-length SRPT, and the further comparison policies of its Table 1 and
+// evaluation baselines: shortest prompt first (SPF), shortest job first with
+// perfect output-length knowledge (SJF), least attained service (LAS) and
+// SRPT with TRAIL's swap-prevention threshold (TRAIL).
+enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2, P_SPF = 3, P_SJF = 4, P_LAS = 5, P_TRAIL = 6 };
 
 // ------------------------------------------------------------ wave helpers
 
@@ -360,8 +365,12 @@ struct Sim {
         uint32_t lvl = 0;
         if (pol == P_FCFS) {
             key = a;
-        } else if (pol == P_SRPT) {
-            key = (int64_t)P + D - 1;
+        } else if (pol == P_SRPT || pol == P_TRAIL) {
+            key = (int64_t)P + D - 1;  // remaining computed tokens
+        } else if (pol == P_SPF || pol == P_LAS) {
+            key = P;  // prompt length; the attained service P + dec at dec = 0
+        } else if (pol == P_SJF) {
+            key = D;  // output length
         } else {
             lvl = (uint32_t)level_of(P, k, lk);
             key = a - S.bt[lvl];
@@ -632,6 +641,17 @@ struct Sim {
             const bool rs = (g & G_RES) != 0;
             bool ev = rs;
             if (memguard) ev = rs && ((g >> G_LVL_SHIFT) & 31u) > (g & G_GUARD);
+            if (pol == P_TRAIL && ballot(rs)) {
+                // swap prevention: a request that emitted at least 0.6 D of its
+                // D tokens is not a voluntary victim (5 (D - left) >= 3 D)
+                int64_t Dv = 0, lv = 0;
+                if (rs) {
+                    const int idx = idx_of(S.k[r]);
+                    Dv = idx < N ? Dp[idx] : 0;
+                    lv = (int)S.q[r].w;
+                }
+                ev = rs && !(2 * Dv >= 5 * lv);
+            }
             const uint64_t m1 = ballot(rs), m2 = ballot(ev);
             if (lane() == c) vm_res = m1, vm_ev = m2;
         }
@@ -642,6 +662,10 @@ struct Sim {
     // non-evictable until its level moves) or stopped being one.
     DEV void vm_set(int r, bool resident) {
         if (!vm_ok) return;
+        if (resident && pol == P_TRAIL) {  // eligibility depends on progress: rebuild
+            vm_ok = false;
+            return;
+        }
         const uint64_t bit = 1ull << (r & 63);
         if (lane() == (r >> 6)) {
             if (resident) {
@@ -687,7 +711,7 @@ struct Sim {
         const uint32_t g = (uint32_t)uni((int)qv.x);
         wsync();
         if (lane() == 0) {
-            S.q[v].x = (g & ~G_RES) | G_EVI | (pol == P_SRPT ? G_DIRTY : 0u);
+            S.q[v].x = (g & ~G_RES) | G_EVI | (pol == P_SRPT || pol == P_TRAIL ? G_DIRTY : 0u);
             S.q[v].z = 0;
         }
         wsync();
@@ -848,6 +872,7 @@ struct Sim {
                 U += rl(dui, last);
                 nW -= nadm_w;
                 nR += nadm_w;
+                if (pol == P_TRAIL && nadm_w) vm_ok = false;  // eligibility depends on progress
                 if (UNLIKELY(vm_ok && nadm_w)) {  // dispatched waiting entries become residents
                     // lanes of this chunk land in aligned chunks p>>6 and (p>>6)+1
                     const int c0 = p >> 6, sh = p & 63;
@@ -932,6 +957,11 @@ struct Sim {
                         kv = 0;
                         tlast[idx] = t_end;
                         fin = true;
+                    } else if (pol == P_LAS) {
+                        // the attained service grew by one token
+                        pk = pack((int64_t)w, idx);
+                        gs |= G_DIRTY;
+                        chg = true;
                     } else if (pol == P_BOOST) {
                         const int lo_ = (int)((gs >> G_LVL_SHIFT) & 31u);
                         const int ln = level_of(w, k, lk);
@@ -942,7 +972,7 @@ struct Sim {
                         }
                     }
                 }
-                if (pol == P_SRPT && !(gs & G_DONE)) {
+                if ((pol == P_SRPT || pol == P_TRAIL) && !(gs & G_DONE)) {
                     pk = pack((int64_t)w + left - 1 - kv, idx);
                     chg = true;
                 }
@@ -950,7 +980,7 @@ struct Sim {
                 if (chg) S.k[r] = pk;
                 if (emit) S.tl[r] = t32;
             } else if (g & G_EVI) {
-                if (pol == P_SRPT) {
+                if (pol == P_SRPT || pol == P_TRAIL) {
                     S.k[r] = pack((int64_t)(int)q.y + (int)q.w - 1, idx_of(pk));
                     chg = true;
                 }

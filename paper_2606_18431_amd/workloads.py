@@ -20,6 +20,9 @@ Five workloads are defined (``make(cfg)``):
 
 The policy-parameter grid per trace: setting 0 = FCFS, setting 1 = oracle-length
 SRPT, then pairs (UniBoost with MemGuard, vanilla boost) over log-spaced gamma.
+``make(cfg, grid="comparators")`` instead runs every trace under the paper's
+comparison policies (FCFS, SRPT, SPF, SJF, LAS, TRAIL) beside UniBoost and vanilla
+boost.
 """
 from __future__ import annotations
 
@@ -28,8 +31,9 @@ import math
 
 import numpy as np
 
-FCFS, SRPT, BOOST = 0, 1, 2
-POLICY_NAMES = {FCFS: "fcfs", SRPT: "srpt", BOOST: "boost"}
+FCFS, SRPT, BOOST, SPF, SJF, LAS, TRAIL = 0, 1, 2, 3, 4, 5, 6
+POLICY_NAMES = {FCFS: "fcfs", SRPT: "srpt", BOOST: "boost", SPF: "spf", SJF: "sjf", LAS: "las",
+                TRAIL: "trail"}
 LEVELS = 24
 
 # One numpy record per instance; field order mirrors the C struct tas_setting.
@@ -131,6 +135,19 @@ def settings_grid(n_traces: int, n_settings: int) -> np.ndarray:
                 var = VANILLA if (s - 2) % 2 else UNIBOOST
                 rec = setting(t, BOOST, gamma=float(gammas[(s - 2) // 2]), **var)
             out[t * n_settings + s] = rec
+    return out
+
+
+def comparator_settings(n_traces: int, gamma: float = 1e-3) -> np.ndarray:
+    """Per trace, 8 settings: FCFS, SRPT, SPF, SJF, LAS, TRAIL, then UniBoost and
+    vanilla boost at one gamma. Instance id = trace * 8 + s."""
+    per = [dict(policy=FCFS), dict(policy=SRPT), dict(policy=SPF), dict(policy=SJF),
+           dict(policy=LAS), dict(policy=TRAIL), dict(policy=BOOST, gamma=gamma, **UNIBOOST),
+           dict(policy=BOOST, gamma=gamma, **VANILLA)]
+    out = np.zeros(n_traces * len(per), dtype=SETTING_DTYPE)
+    for t in range(n_traces):
+        for s, kw in enumerate(per):
+            out[t * len(per) + s] = setting(t, **kw)
     return out
 
 
@@ -276,10 +293,11 @@ def _trace(cfg: int, trace: int, n: int, eng: Engine):
 
 
 def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
-         n_req: int | None = None) -> Workload:
+         n_req: int | None = None, grid: str = "sweep") -> Workload:
     """Build workload ``cfg``. The optional overrides shrink it (fewer traces,
     settings or requests) for tests; traces keep their seeds, so trace t of a
-    shrunk workload equals trace t of the full one when n_req is unchanged."""
+    shrunk workload equals trace t of the full one when n_req is unchanged.
+    ``grid="comparators"`` replaces the settings grid by comparator_settings."""
     T0, S0, N0 = SHAPES[cfg]
     T = T0 if n_traces is None else n_traces
     S = S0 if n_settings is None else n_settings
@@ -290,7 +308,10 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
     de = np.empty((T, N), np.int32)
     for t in range(T):
         arr[t], pr[t], de[t] = _trace(cfg, t, N, eng)
-    if cfg == 0 and S == 8:
+    if grid == "comparators":
+        sets = comparator_settings(T)
+        S = 8
+    elif cfg == 0 and S == 8:
         st = [setting(0, FCFS), setting(0, SRPT)]
         st += [setting(0, BOOST, gamma=g, **UNIBOOST)
                for g in (1e-4, 3e-4, 1e-3, 3e-3, 1e-2, 3e-2)]
@@ -299,7 +320,7 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
     else:
         sets = settings_grid(T, S)
     return Workload(NAMES[cfg], arr, pr, de, eng, sets,
-                    meta=dict(cfg=cfg, n_traces=T, n_settings=S, n_req=N))
+                    meta=dict(cfg=cfg, n_traces=T, n_settings=S, n_req=N, grid=grid))
 
 
 def small_random(seed: int, n_req: int, *, rate_per_s: float = 20.0, p_med=64, d_med=20,

@@ -105,7 +105,10 @@ def test_rejects_invalid_settings():
     w = small()
     cases = []
     s = w.settings.copy(); s[0]["trace"] = 5; cases.append(s)
-    s = w.settings.copy(); s[0]["policy"] = 3; cases.append(s)
+    s = w.settings.copy(); s[0]["policy"] = 7; cases.append(s)           # unknown policy
+    s = w.settings.copy(); s[0]["policy"] = -1; cases.append(s)
+    s = w.settings.copy(); s[0]["policy"] = 5; s[0]["memguard"] = 1; cases.append(s)  # LAS + MemGuard
+    s = w.settings.copy(); s[1]["policy"] = 6; s[1]["delta_us"] = 5; cases.append(s)  # TRAIL + delta
     s = w.settings.copy(); s[0]["memguard"] = 1; cases.append(s)          # FCFS with MemGuard
     s = w.settings.copy(); s[1]["delta_us"] = 10; cases.append(s)         # SRPT with delta
     s = w.settings.copy(); s[2]["k"] = 0; cases.append(s)

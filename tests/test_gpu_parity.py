@@ -95,6 +95,34 @@ def test_parity_reduced_configs(torch, cfg, n_traces, n_settings, n_req):
     assert_parity(w, g, o)
 
 
+@pytest.mark.parametrize("cfg,n_traces,n_req", [
+    (1, 2, 3000),
+    (2, 2, 3000),         # KV pressure: TRAIL's threshold and the victims matter
+    (3, 1, 5000),
+    (4, 1, 6000),
+])
+def test_parity_comparators(torch, cfg, n_traces, n_req):
+    """FCFS, SRPT, SPF, SJF, LAS, TRAIL, UniBoost and vanilla boost on every trace.
+    LAS starves long requests under load: where a latency exceeds 2^32-1 us both
+    sides must report TAS_EOVERFLOW for that instance; every other instance is
+    compared element by element."""
+    w = W.make(cfg, n_traces=n_traces, n_req=n_req, grid="comparators")
+    o = oracle.run(w)
+    g = gpu_run(w)
+    assert np.array_equal(g["status"], o["status"]), (g["status"], o["status"])
+    assert set(np.unique(o["status"]).tolist()) <= {0, -5}
+    assert_parity(w, g, o, inst=np.nonzero(o["status"] == 0)[0])
+
+
+@pytest.mark.parametrize("cfg,list_cap", [(2, 192), (3, 128)])
+def test_parity_comparators_with_spill(torch, cfg, list_cap):
+    w = W.make(cfg, n_traces=1, n_req=4000, grid="comparators")
+    o = oracle.run(w)
+    g = gpu_run(w, list_cap=list_cap)
+    assert np.array_equal(g["status"], o["status"]), (g["status"], o["status"])
+    assert_parity(w, g, o, inst=np.nonzero(o["status"] == 0)[0])
+
+
 @pytest.mark.parametrize("cfg,list_cap", [(2, 192), (4, 320), (3, 128)])
 def test_parity_with_spill(torch, cfg, list_cap):
     """A small on-chip list forces the HBM spill, refill and radix-select paths."""

@@ -1,0 +1,152 @@
+"""Pins of the oracle's comparison policies (paper: Table 1 and the
+evaluation's baselines): shortest prefix first (SPF), shortest job first with
+perfect output-length knowledge (SJF, the ranking LTR learns), least attained
+service (LAS) and SRPT with TRAIL's swap-prevention threshold (TRAIL).
+
+Each pin checks the oracle against something other than itself: optimal orders
+over all permutations on a single machine, the defining selection rule
+replayed from the oracle's own iteration log, and identities with policies
+pinned elsewhere.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_18431_amd import workloads as W
+from test_oracle_pins import alone_schedule, engine
+
+FCFS, SRPT, BOOST, SPF, SJF, LAS, TRAIL = 0, 1, 2, 3, 4, 5, 6
+
+
+def job_time(P, D, e):
+    return alone_schedule(P, D, e)[1]
+
+
+def spt_best(p):
+    return min(sum(itertools.accumulate(p[i] for i in perm))
+               for perm in itertools.permutations(range(len(p))))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_sjf_minimizes_total_latency_brute_force(seed):
+    """Common release 0, equal prompts, M=1, ample KV: each request's processing
+    time grows with D, so ordering by D is SPT, the minimum total TTLT over all
+    n! orders; SJF and SRPT then run the same schedule."""
+    rng = np.random.default_rng([17, seed])
+    n = int(rng.integers(3, 7))
+    P = int(rng.integers(16, 200))
+    D = rng.integers(1, 40, n).astype(np.int32)
+    e = engine(max_seqs=1)
+    best = spt_best([job_time(P, int(d), e) for d in D])
+    o = oracle.log(np.zeros(n), np.full(n, P), D, e, SJF)
+    assert int(o["ttlt"].astype(np.int64).sum()) == best
+    s = oracle.log(np.zeros(n), np.full(n, P), D, e, SRPT)
+    for key in ("ttft", "ttlt", "tbtmax", "counters"):
+        assert np.array_equal(o[key], s[key])
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_spf_minimizes_total_latency_brute_force(seed):
+    """Common release 0, one output token each, M=1, one-chunk prefills: each
+    request's time grows with its prompt, so prompt order is SPT."""
+    rng = np.random.default_rng([18, seed])
+    n = int(rng.integers(3, 7))
+    P = rng.integers(1, 1000, n).astype(np.int32)
+    e = engine(max_seqs=1)
+    best = spt_best([job_time(int(x), 1, e) for x in P])
+    o = oracle.log(np.zeros(n), P, np.ones(n, np.int32), e, SPF)
+    assert int(o["ttlt"].astype(np.int64).sum()) == best
+    # dispatch order is the (prompt, index) order
+    order = o["batch"][:, 0].tolist()
+    assert order == sorted(range(n), key=lambda i: (int(P[i]), i))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_las_serves_least_attained_service(seed):
+    """M=1, ample KV, one-chunk prefills: every iteration serves the active
+    request with the least attained service P + dec (ties by index)."""
+    a, p, d = W.small_random(seed, 60, rate_per_s=30.0)
+    e = engine(max_seqs=1, chunk=1024)
+    o = oracle.log(a, p, d, e, LAS)
+    assert o["rc"] == 0
+    dec = np.zeros(len(a), np.int64)
+    done = np.zeros(len(a), bool)
+    for row, it in enumerate(o["iters"]):
+        assert it[2] == 1
+        r = int(o["batch"][row][0])
+        active = [i for i in range(len(a)) if a[i] <= it[0] and not done[i]]
+        assert r == min(active, key=lambda i: (int(p[i]) + int(dec[i]), i))
+        dec[r] += 1
+        done[r] = dec[r] == d[r]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_trail_equals_srpt_without_kv_pressure(seed):
+    """The threshold only restricts victims: with KV for everyone (no eviction
+    can happen) TRAIL and SRPT run the same schedule."""
+    a, p, d = W.small_random(seed, 150, rate_per_s=60.0)
+    e = engine(max_seqs=6, chunk=128, max_tokens=384)
+    t = oracle.log(a, p, d, e, TRAIL)
+    s = oracle.log(a, p, d, e, SRPT)
+    assert t["counters"][3] == 0 and t["counters"][4] == 0
+    for key in ("ttft", "ttlt", "tbtmax", "counters"):
+        assert np.array_equal(t[key], s[key])
+
+
+def test_trail_never_preempts_past_threshold():
+    """Replayed from the log under KV pressure: no voluntary victim had emitted
+    0.6 of its output (5 dec >= 3 D); some evictions do happen."""
+    a, p, d = W.small_random(5, 200, rate_per_s=80.0, p_max=300, d_max=150)
+    e = engine(max_seqs=8, kv_blocks=40, chunk=64, max_tokens=256)
+    o = oracle.log(a, p, d, e, TRAIL)
+    assert o["rc"] == 0
+    kv = np.zeros(len(a), np.int64)
+    dec = np.zeros(len(a), np.int64)
+    ev = o["evict"]
+    ep, row, vol = 0, 0, 0
+    for i, it in enumerate(o["iters"]):
+        while ep < len(ev) and ev[ep][0] == i:
+            _, v, forced = ev[ep]
+            ep += 1
+            if not forced:
+                assert 5 * dec[v] < 3 * d[v]
+                vol += 1
+            kv[v] = 0
+        for r, n in o["batch"][row:row + it[2]]:
+            kv[r] += n
+            if kv[r] == p[r] + dec[r]:
+                dec[r] += 1
+                if dec[r] == d[r]:
+                    kv[r] = 0
+        row += it[2]
+    assert vol > 0
+    s = oracle.log(a, p, d, e, SRPT)
+    assert not np.array_equal(s["counters"], o["counters"])  # the threshold changed something
+
+
+@pytest.mark.parametrize("policy,blind", [(SPF, True), (LAS, True), (SJF, False)])
+def test_blindness(policy, blind):
+    """SPF and LAS use no knowledge of the output length (prediction-free):
+    lengthening one request's decode leaves every event before its original
+    completion unchanged. SJF reads the length."""
+    changed = 0
+    for seed in range(4):
+        a, p, d = W.small_random(seed, 120, rate_per_s=60.0)
+        e = engine(max_seqs=4, kv_blocks=80, chunk=128, max_tokens=384)
+        j = 17
+        d2 = d.copy()
+        d2[j] += 500
+        o1 = oracle.log(a, p, d, e, policy)
+        o2 = oracle.log(a, p, d2, e, policy)
+        ends = np.cumsum(o1["iters"][:, 2])
+        last = max(i for i in range(len(ends))
+                   if j in o1["batch"][(ends[i] - o1["iters"][i, 2]):ends[i], 0])
+        same = (np.array_equal(o1["iters"][: last + 1], o2["iters"][: last + 1])
+                and np.array_equal(o1["batch"][: ends[last]], o2["batch"][: ends[last]]))
+        if blind:
+            assert same
+        changed += not same
+    if not blind:
+        assert changed > 0

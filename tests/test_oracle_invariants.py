@@ -57,6 +57,8 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0):
                 vol_per_req[v] += 1
                 if memguard:  # I9: MemGuard eligibility
                     assert oracle.level(int(p[v] + dec[v]), k) > guard[v]
+                if policy == 6:  # TRAIL swap prevention
+                    assert 5 * dec[v] < 3 * d[v]
             evicted_kv_total += kv[v]
             kv[v] = 0
             evicted.add(v)
@@ -137,6 +139,10 @@ ENGINES = [
 POLICIES = [
     dict(policy=0),
     dict(policy=1),
+    dict(policy=3),  # SPF
+    dict(policy=4),  # SJF
+    dict(policy=5),  # LAS
+    dict(policy=6),  # TRAIL
     dict(policy=2, k=16, memguard=1, delta_us=20000, gamma=1e-3),
     dict(policy=2, k=1, memguard=0, delta_us=0, gamma=1e-3),
     dict(policy=2, k=32, memguard=1, delta_us=0, gamma=3e-2),
