@@ -31,7 +31,20 @@
  *     (the engine's forward step, Algorithm 1 ExecuteOneStep, replaced by an
  *     integer cost model);
  *   - each request's TTFT, TTLT and maximum inter-token gap are recorded, and
- *     reduced per instance to nearest-rank P50/P90/P99 (Phase 4, t_p).
+ *     reduced per instance to nearest-rank P50/P90/P99 (Phase 4, t_p);
+ *   - optionally (TAS_BOOST, tas_setting.ada = 1) gamma adapts online (Phase 4,
+ *     gamma-Ada; Algorithm 2 UpdateGamma, run before the keys of every
+ *     iteration): once the window of the last `ada_window` end-to-end
+ *     latencies (TTLT of completed requests, in completion order; requests
+ *     finishing in one iteration in batch order) holds `ada_min_samples`
+ *     values, gamma_hat = (tau_us ln 5) / max(t99 - t95, ada_eps_us) with
+ *     nearest-rank t95, t99 of the window (the tail-band slope of
+ *     Eq. gamma_estimator, ln 5 = ln(0.05/0.01), per token of boost), and
+ *     gamma = clip((1 - beta) gamma + beta gamma_hat, gamma_min, gamma_max),
+ *     each step one rounded IEEE double operation. The boost table in use is
+ *     that of the grid point nearest gamma in log scale on the grid
+ *     g_j = gamma_min (gamma_max/gamma_min)^(j/(G-1)), j < G (midpoints
+ *     sqrt(g_j g_{j+1}) round up), so priorities stay integers.
  *
  * Everything is integer arithmetic; results are deterministic and independent
  * of the launch configuration.
@@ -101,10 +114,24 @@ typedef struct {
     double gamma;     /* BOOST: > 0 builds boost_us from the gamma-Boost curve
                          (tas_boost_table); 0 uses boost_us as given           */
     int32_t table_given; /* 1: boost_us is an explicit table (gamma ignored)  */
-    int32_t reserved;
+    int32_t ada;         /* 1: adaptive gamma from `gamma` (BOOST, no explicit
+                            table); 0: the ada_* fields are ignored           */
     int64_t boost_us[TAS_LEVELS]; /* explicit table: non-increasing, in
                                      [0, 2^42]                                 */
+    /* adaptive gamma (ada = 1), see the top of this file */
+    double ada_beta;       /* EMA weight per iteration, in [0, 1]              */
+    double ada_gamma_min;  /* clip bounds and grid ends: 0 < gamma_min <       */
+    double ada_gamma_max;  /*   gamma_max, gamma_min <= gamma <= gamma_max     */
+    double ada_eps_us;     /* floor of t99 - t95, > 0                          */
+    int32_t ada_window;    /* latencies kept, in [1, TAS_ADA_WINDOW_MAX]       */
+    int32_t ada_min_samples; /* window size before the first update, in
+                                [1, ada_window]                                */
+    int32_t ada_grid;      /* grid points G, in [2, TAS_ADA_GRID_MAX]          */
+    int32_t ada_reserved;  /* 0                                                */
 } tas_setting;
+
+#define TAS_ADA_WINDOW_MAX 2048
+#define TAS_ADA_GRID_MAX 64
 
 /* Engine limits, cost model and the instance list (HOST). */
 typedef struct {
@@ -146,7 +173,9 @@ size_t tas_workspace_bytes(const tas_traces *traces, const tas_params *params);
  * >= 2^41 or out of order; P or D < 1; P + D >= 2^24; a trace index is out of
  * range; policy unknown; k < 1 (BOOST); delta < 0; memguard or delta nonzero
  * for a policy other than BOOST; gamma <= 0 without table_given (BOOST); an explicit table not
- * non-increasing or outside [0, 2^42]; chunk > max_tokens; any engine limit
+ * non-increasing or outside [0, 2^42]; ada not 0 or 1; ada = 1 with a policy
+ * other than BOOST, with table_given, or with an ada_* field outside its
+ * range; chunk > max_tokens; any engine limit
  * < 1; chunk > 32767; tau <= 0; list_cap < max_seqs + 64 or > 4032.
  * TAS_EINFEASIBLE if ceil((P + D - 1) / block_tokens) > kv_blocks for some
  * request. TAS_ENOMEM if ws_bytes is too small. TAS_EHIP if a copy fails. */

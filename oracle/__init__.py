@@ -27,8 +27,11 @@ def build(force: bool = False) -> str:
     """Compile the oracle with gcc (-O2, plain C11, pthreads)."""
     if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
         tmp = LIB + ".tmp"
+        # -ffp-contract=off: every floating-point step of the adaptive gamma is one
+        # rounded IEEE operation (no fused multiply-add)
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-D_GNU_SOURCE", "-fPIC", "-shared",
-                               "-Wall", "-Wextra", "-o", tmp, SRC, "-lm", "-lpthread"])
+                               "-ffp-contract=off", "-Wall", "-Wextra", "-o", tmp, SRC, "-lm",
+                               "-lpthread"])
         os.replace(tmp, LIB)
     return LIB
 
@@ -47,10 +50,12 @@ def lib():
         L.tas_oracle_boost_table.argtypes = [f64, i32, f64, P]
         L.tas_oracle_boost_table.restype = ctypes.c_int
         L.tas_oracle_run.argtypes = [i32, i32, P, P, P, i32, P, P, P, P, P, P, P, i64,
-                                     P, P, P, P, P, P, i32]
+                                     P, P, P, P, P, P, P, P, P, i32]
         L.tas_oracle_run.restype = ctypes.c_int
-        L.tas_oracle_log.argtypes = [i32, P, P, P, i32, i32, i32, i64, P, P, i64, P, P, P, P,
-                                     P, i64, P, i64, P, i64, P, P, P]
+        L.tas_oracle_log.argtypes = [i32, P, P, P, i32, i32, i32, i64, P, P, P, i64, P, P, P,
+                                     P, P, i64, P, i64, P, i64, P, P, P]
+        L.tas_oracle_ada_grid.argtypes = [P, i32, P, P, P]
+        L.tas_oracle_ada_grid.restype = ctypes.c_int
         L.tas_oracle_log.restype = ctypes.c_int
         L.tas_oracle_level.argtypes = [i64, i32]
         L.tas_oracle_level.restype = ctypes.c_int32
@@ -87,6 +92,32 @@ def tables(settings: np.ndarray, tau_us: float) -> np.ndarray:
     return out
 
 
+ADA_FIELDS = ("ada_beta", "ada_gamma_min", "ada_gamma_max", "ada_eps_us", "ada_window",
+              "ada_min_samples", "ada_grid")
+
+
+def ada_params(s, tau_us: float) -> np.ndarray:
+    """The oracle's 10 adaptive-gamma parameters of one setting record
+    {on, gamma0, beta, gamma_min, gamma_max, eps_us, window, min_samples,
+    grid, tau_us} (on = 0 when the setting does not adapt gamma)."""
+    if not int(s["ada"]):
+        return np.zeros(10, np.float64)
+    return np.array([1.0, float(s["gamma"])] + [float(s[f]) for f in ADA_FIELDS] +
+                    [float(tau_us)], np.float64)
+
+
+def ada_grid(s, tau_us: float = 5000.0):
+    """(grid [G], midpoints [G-1], tables [G, 24]) of an adaptive setting."""
+    prm = ada_params(s, tau_us)
+    G = int(s["ada_grid"])
+    grid, bound = np.zeros(64, np.float64), np.zeros(64, np.float64)
+    tab = np.zeros((64, LEVELS), np.int64)
+    rc = lib().tas_oracle_ada_grid(_p(prm), int(s["k"]), _p(grid), _p(bound), _p(tab))
+    if rc:
+        raise ValueError("adaptive-gamma parameters rejected")
+    return grid[:G].copy(), bound[:G - 1].copy(), tab[:G].copy()
+
+
 def _eng(engine) -> np.ndarray:
     return np.array([engine.max_seqs, engine.max_tokens, engine.chunk, engine.kv_blocks,
                      engine.block_tokens, engine.iter_base_us, engine.iter_tok_us,
@@ -96,7 +127,8 @@ def _eng(engine) -> np.ndarray:
 def run(w, n_threads: int | None = None, max_iters: int | None = None):
     """Simulate every instance of workload ``w``. Returns a dict of host arrays:
     ttft/ttlt/tbtmax [n_inst, n_req] uint32, counters [n_inst, 8] int64,
-    pct [n_inst, 3, 3] uint32, status [n_inst] int32, rc."""
+    pct [n_inst, 3, 3] uint32, status [n_inst] int32, gamma [n_inst] float64
+    (final adaptive gamma, 0 when fixed), switches [n_inst] int64, rc."""
     s = w.settings
     n_inst, n_req = len(s), w.n_req
     arr = np.ascontiguousarray(w.arrival_us, np.int64)
@@ -108,6 +140,8 @@ def run(w, n_threads: int | None = None, max_iters: int | None = None):
     mg = np.ascontiguousarray(s["memguard"], np.int32)
     dl = np.ascontiguousarray(s["delta_us"], np.int64)
     tb = np.ascontiguousarray(tables(s, w.engine.tau_us))
+    ada = np.ascontiguousarray(np.stack([ada_params(x, w.engine.tau_us) for x in s])
+                               if n_inst else np.zeros((0, 10)), np.float64)
     out = dict(
         ttft=np.zeros((n_inst, n_req), np.uint32),
         ttlt=np.zeros((n_inst, n_req), np.uint32),
@@ -115,20 +149,25 @@ def run(w, n_threads: int | None = None, max_iters: int | None = None):
         counters=np.zeros((n_inst, 8), np.int64),
         pct=np.zeros((n_inst, 3, 3), np.uint32),
         status=np.zeros(n_inst, np.int32),
+        gamma=np.zeros(n_inst, np.float64),
+        switches=np.zeros(n_inst, np.int64),
     )
     mi = w.engine.max_iters if max_iters is None else max_iters
     nt = n_threads or os.cpu_count() or 1
     rc = lib().tas_oracle_run(w.n_traces, n_req, _p(arr), _p(pr), _p(de), n_inst, _p(tr),
                               _p(po), _p(kk), _p(mg), _p(dl), _p(tb), _p(_eng(w.engine)),
                               int(mi), _p(out["ttft"]), _p(out["ttlt"]), _p(out["tbtmax"]),
-                              _p(out["counters"]), _p(out["pct"]), _p(out["status"]), int(nt))
+                              _p(out["counters"]), _p(out["pct"]), _p(out["status"]), _p(ada),
+                              _p(out["gamma"]), _p(out["switches"]), int(nt))
     out["rc"] = rc
     return out
 
 
 def log(arrival, prompt, decode, engine, policy, k=1, memguard=0, delta_us=0, table=None,
-        gamma=None, max_iters=None, cap_iter=1 << 20, cap_batch=1 << 22, cap_evict=1 << 20):
-    """Run one instance and return its schedule log (see tas_oracle.h)."""
+        gamma=None, ada=None, max_iters=None, cap_iter=1 << 20, cap_batch=1 << 22,
+        cap_evict=1 << 20):
+    """Run one instance and return its schedule log (see tas_oracle.h). ``ada``:
+    adaptive-gamma parameters as in workloads.ADA (gamma is the start)."""
     arrival = np.ascontiguousarray(arrival, np.int64)
     prompt = np.ascontiguousarray(prompt, np.int32)
     decode = np.ascontiguousarray(decode, np.int32)
@@ -137,20 +176,27 @@ def log(arrival, prompt, decode, engine, policy, k=1, memguard=0, delta_us=0, ta
         table = (boost_table(gamma, k, engine.tau_us) if gamma is not None
                  else np.zeros(LEVELS, np.int64))
     table = np.ascontiguousarray(table, np.int64)
+    prm = np.zeros(10, np.float64)
+    if ada is not None:
+        prm = np.array([1.0, float(gamma), ada["beta"], ada["gamma_min"], ada["gamma_max"],
+                        ada["eps_us"], ada["window"], ada["min_samples"], ada["grid"],
+                        float(engine.tau_us)], np.float64)
     o = dict(ttft=np.zeros(n, np.uint32), ttlt=np.zeros(n, np.uint32),
              tbtmax=np.zeros(n, np.uint32), counters=np.zeros(8, np.int64))
-    it = np.zeros((cap_iter, 6), np.int64)
+    it = np.zeros((cap_iter, 8), np.int64)
     bt = np.zeros((cap_batch, 2), np.int32)
     ev = np.zeros((cap_evict, 3), np.int64)
     ni, nb, ne = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     mi = engine.max_iters if max_iters is None else max_iters
     rc = lib().tas_oracle_log(n, _p(arrival), _p(prompt), _p(decode), policy, k, memguard,
-                              int(delta_us), _p(table), _p(_eng(engine)), int(mi),
+                              int(delta_us), _p(table), _p(prm), _p(_eng(engine)), int(mi),
                               _p(o["ttft"]), _p(o["ttlt"]), _p(o["tbtmax"]), _p(o["counters"]),
                               _p(it), cap_iter, _p(bt), cap_batch, _p(ev), cap_evict,
                               ctypes.byref(ni), ctypes.byref(nb), ctypes.byref(ne))
     o["rc"] = rc
-    o["iters"] = it[: ni.value].copy()
+    o["iters"] = it[: ni.value, :6].copy()
+    o["cell"] = it[: ni.value, 6].copy()
+    o["gamma"] = it[: ni.value, 7].copy().view(np.float64)
     o["batch"] = bt[: nb.value].copy()
     o["evict"] = ev[: ne.value].copy()
     return o

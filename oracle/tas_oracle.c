@@ -20,6 +20,10 @@
  *                                   KV capacity, victim selection + swap-out,
  *                                   ExecuteOneStep, UpdateStats
  *   Phase 4                         t_p = inf{t : Fbar(t) <= (100-p)/100}
+ *   Phase 4 (gamma-Ada), Eq. gamma_estimator, Algorithm 2 UpdateGamma
+ *                                   gamma_hat = (ln Fbar(t95) - ln Fbar(t99)) /
+ *                                   (t99 - t95) over a window of recent
+ *                                   end-to-end latencies, EMA, clip
  *
  * Where the paper is silent, the readings are (each is listed, with its
  * reason, in the design notes of the repository):
@@ -47,6 +51,22 @@
  *   TRAIL SRPT with perfect knowledge plus the swap-prevention threshold: a
  *         resident that has emitted at least 0.6 D tokens is never a voluntary
  *         victim (5 dec >= 3 D)
+ *
+ * Adaptive gamma (Phase 4, gamma-Ada), for BOOST instances that ask for it:
+ *   - the window holds the end-to-end latencies (TTLT, us, capped at 2^32-1)
+ *     of the last W completed requests; requests that complete in the same
+ *     iteration enter it in batch order
+ *   - at the start of every iteration (Algorithm 1 calls UpdateGamma before
+ *     the keys), once the window holds at least min_samples latencies:
+ *       t95, t99 = nearest-rank percentiles of the window
+ *       gamma_hat = (tau ln 5) / max(t99 - t95, eps)   (per token: the
+ *           estimator is per microsecond and one token of boost is tau us;
+ *           ln 5 = ln(0.05 / 0.01) from the tail-band definition)
+ *       gamma = clip((1 - beta) gamma + beta gamma_hat, gamma_min, gamma_max)
+ *   - the boost table in use is that of the nearest point of a log-spaced
+ *     grid of G values from gamma_min to gamma_max (nearest in log scale,
+ *     midpoints sqrt(g_j g_{j+1}) going up), so priorities stay integers
+ *   - every floating-point step is one IEEE double operation, in this order
  */
 #include "tas_oracle.h"
 
@@ -58,6 +78,17 @@
 enum { PENDING = 0, WAITING = 1, RESIDENT = 2, DONE = 3 };
 enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2, P_SPF = 3, P_SJF = 4, P_LAS = 5, P_TRAIL = 6 };
 
+#define ADA_GRID_MAX 64
+#define ADA_WINDOW_MAX 2048
+
+typedef struct {
+    int32_t on;
+    double gamma0, beta, gmin, gmax, eps, num; /* num = tau ln 5 */
+    int32_t W, nmin, G;
+    double grid[ADA_GRID_MAX], bound[ADA_GRID_MAX];
+    int64_t table[ADA_GRID_MAX][TOR_LEVELS];
+} ada_t;
+
 typedef struct {
     int32_t N;
     const int64_t *a;
@@ -67,6 +98,7 @@ typedef struct {
     const int64_t *bt;
     int32_t M, T, c, Kb, bs, base, tok, div;
     int64_t max_iters;
+    const ada_t *ada; /* NULL: gamma fixed */
 } inst_t;
 
 typedef struct {
@@ -159,10 +191,65 @@ static void evict(req_t *q, int64_t *U, int32_t bs, int64_t iter) {
     q->evicted_at = iter;
 }
 
+/* ------------------------------------------------------------ gamma-Ada */
+
+/* One instance's adaptive-gamma parameters from prm[10] = {on, gamma0, beta,
+ * gamma_min, gamma_max, eps_us, window, min_samples, grid points, tau_us}:
+ * the log-spaced grid g_j = gamma_min (gamma_max/gamma_min)^(j/(G-1)), the
+ * midpoints sqrt(g_j g_{j+1}) between neighbours and the boost table of every
+ * grid point. Returns 0 or TOR_EINVAL. */
+static int ada_setup(ada_t *A, const double *prm, int32_t policy, int32_t k) {
+    memset(A, 0, sizeof *A);
+    if (prm[0] == 0.0) return 0;
+    if (prm[0] != 1.0 || policy != P_BOOST) return TOR_EINVAL;
+    A->on = 1;
+    A->gamma0 = prm[1], A->beta = prm[2], A->gmin = prm[3], A->gmax = prm[4], A->eps = prm[5];
+    const double tau = prm[9];
+    if (!(prm[6] >= 1 && prm[6] <= ADA_WINDOW_MAX && prm[7] >= 1 && prm[7] <= prm[6] &&
+          prm[8] >= 2 && prm[8] <= ADA_GRID_MAX))
+        return TOR_EINVAL;
+    A->W = (int32_t)prm[6], A->nmin = (int32_t)prm[7], A->G = (int32_t)prm[8];
+    if (!(A->beta >= 0.0 && A->beta <= 1.0 && A->gmin > 0.0 && A->gmax > A->gmin &&
+          isfinite(A->gmax) && A->gamma0 >= A->gmin && A->gamma0 <= A->gmax && A->eps > 0.0 &&
+          isfinite(A->eps) && tau > 0.0 && isfinite(tau)))
+        return TOR_EINVAL;
+    A->num = tau * log(5.0);
+    for (int32_t j = 0; j < A->G; j++)
+        A->grid[j] = A->gmin * pow(A->gmax / A->gmin, (double)j / (double)(A->G - 1));
+    for (int32_t j = 0; j + 1 < A->G; j++) A->bound[j] = sqrt(A->grid[j] * A->grid[j + 1]);
+    for (int32_t j = 0; j < A->G; j++)
+        if (tas_oracle_boost_table(A->grid[j], k, tau, A->table[j])) return TOR_EINVAL;
+    return 0;
+}
+
+/* The grid point nearest to gamma in log scale (a midpoint goes up). */
+static int32_t ada_cell(const ada_t *A, double gamma) {
+    int32_t j = 0;
+    while (j + 1 < A->G && gamma >= A->bound[j]) j++;
+    return j;
+}
+
+int tas_oracle_ada_grid(const double *prm, int32_t k, double *grid, double *bound,
+                        int64_t *tables) {
+    ada_t *A = (ada_t *)malloc(sizeof *A);
+    if (!A) return TOR_EINVAL;
+    int rc = ada_setup(A, prm, P_BOOST, k);
+    if (rc == 0 && A->on) {
+        memcpy(grid, A->grid, sizeof(double) * (size_t)A->G);
+        memcpy(bound, A->bound, sizeof(double) * (size_t)(A->G - 1));
+        memcpy(tables, A->table, sizeof(int64_t) * TOR_LEVELS * (size_t)A->G);
+    }
+    free(A);
+    return rc;
+}
+
 /* ------------------------------------------------------------ one instance */
 
-static int simulate(const inst_t *I, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
-                    int64_t *cnt, log_t *lg) {
+static int simulate(const inst_t *I0, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
+                    int64_t *cnt, double *gamma_out, int64_t *switch_out, log_t *lg) {
+    inst_t J = *I0; /* J.bt follows the adaptive gamma */
+    const inst_t *I = &J;
+    const ada_t *A = I->ada && I->ada->on ? I->ada : NULL;
     const int32_t N = I->N;
     for (int32_t i = 0; i < N; i++) {
         if (I->P[i] < 1 || I->D[i] < 1 || I->a[i] < 0 || (i && I->a[i] < I->a[i - 1]))
@@ -173,8 +260,9 @@ static int simulate(const inst_t *I, uint32_t *ttft, uint32_t *ttlt, uint32_t *t
     int32_t *act = (int32_t *)malloc(sizeof(int32_t) * (size_t)N);
     int32_t *bidx = (int32_t *)malloc(sizeof(int32_t) * (size_t)I->M);
     int32_t *bn = (int32_t *)malloc(sizeof(int32_t) * (size_t)I->M);
+    uint32_t *win = A ? (uint32_t *)malloc(sizeof(uint32_t) * (size_t)A->W) : NULL;
     int status = 0;
-    if (!R || !act || !bidx || !bn) {
+    if (!R || !act || !bidx || !bn || (A && !win)) {
         status = TOR_EINVAL;
         goto out;
     }
@@ -183,6 +271,11 @@ static int simulate(const inst_t *I, uint32_t *ttft, uint32_t *ttlt, uint32_t *t
     int64_t t = 0, U = 0, iters = 0, reqiters = 0, tokens = 0, ev_vol = 0, ev_forced = 0;
     int64_t maxU = 0, idle = 0;
     int32_t next = 0, nact = 0;
+    /* gamma-Ada state: gamma, its grid cell, the latency window */
+    double gamma = A ? A->gamma0 : 0.0, ghat = 0.0;
+    int32_t cell = A ? ada_cell(A, gamma) : -1, wn = 0, whead = 0, wnew = 0;
+    int64_t switches = 0;
+    if (A) J.bt = A->table[cell];
 
     for (;;) {
         /* O2 arrivals: a_i <= t joins the waiting set (idx order). */
@@ -196,6 +289,27 @@ static int simulate(const inst_t *I, uint32_t *ttft, uint32_t *ttlt, uint32_t *t
             idle += I->a[next] - t;
             t = I->a[next];
             continue;
+        }
+        /* Phase 4 UpdateGamma, before the keys of this iteration. */
+        if (A && wn >= A->nmin) {
+            if (wnew) { /* the window changed since the last estimate */
+                uint32_t t95 = tas_oracle_percentile(win, wn, 95);
+                uint32_t t99 = tas_oracle_percentile(win, wn, 99);
+                double d = (double)(t99 - t95);
+                if (d < A->eps) d = A->eps;
+                ghat = A->num / d;
+                wnew = 0;
+            }
+            double g = (1.0 - A->beta) * gamma + A->beta * ghat;
+            if (g < A->gmin) g = A->gmin;
+            if (g > A->gmax) g = A->gmax;
+            gamma = g;
+            int32_t c2 = ada_cell(A, gamma);
+            if (c2 != cell) {
+                cell = c2;
+                switches++;
+                J.bt = A->table[cell];
+            }
         }
         /* O4/O5 keys of every active request, then rank by (key, idx). */
         for (int32_t j = 0; j < nact; j++) R[act[j]].key = key_of(I, act[j], &R[act[j]]);
@@ -308,8 +422,10 @@ static int simulate(const inst_t *I, uint32_t *ttft, uint32_t *ttlt, uint32_t *t
                     nw += R[act[m]].st == WAITING;
                     nr += R[act[m]].st == RESIDENT;
                 }
-                int64_t *e = lg->it + 6 * lg->n_it++;
+                int64_t *e = lg->it + 8 * lg->n_it++;
                 e[0] = t, e[1] = dt, e[2] = nb, e[3] = U, e[4] = nw, e[5] = nr;
+                e[6] = cell;
+                memcpy(&e[7], &gamma, sizeof gamma);
             } else
                 lg->full = 1;
             for (int32_t b = 0; b < nb; b++) {
@@ -339,6 +455,13 @@ static int simulate(const inst_t *I, uint32_t *ttft, uint32_t *ttlt, uint32_t *t
                     q->st = DONE;
                     U -= blocks(q->kv, I->bs);
                     q->kv = 0;
+                    if (A) { /* UpdateStats: the window keeps the last W latencies */
+                        int64_t e2e = t_end - I->a[r];
+                        win[whead] = e2e > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)e2e;
+                        whead = (whead + 1) % A->W;
+                        if (wn < A->W) wn++;
+                        wnew = 1;
+                    }
                 }
             }
         }
@@ -371,7 +494,10 @@ static int simulate(const inst_t *I, uint32_t *ttft, uint32_t *ttlt, uint32_t *t
     }
     cnt[0] = iters, cnt[1] = reqiters, cnt[2] = tokens, cnt[3] = ev_vol;
     cnt[4] = ev_forced, cnt[5] = t, cnt[6] = maxU, cnt[7] = idle;
+    if (gamma_out) *gamma_out = gamma;
+    if (switch_out) *switch_out = switches;
 out:
+    free(win);
     free(R);
     free(act);
     free(bidx);
@@ -411,6 +537,9 @@ typedef struct {
     uint32_t *ttft, *ttlt, *tbtmax, *pct;
     int64_t *counters;
     int32_t *status;
+    const double *ada; /* [n_inst*10] or NULL */
+    double *gamma_out;
+    int64_t *switch_out;
     int32_t next; /* work counter */
 } job_t;
 
@@ -422,6 +551,7 @@ static void fill_inst(inst_t *I, const int32_t *eng, int32_t n_req, const int64_
     I->M = eng[0], I->T = eng[1], I->c = eng[2], I->Kb = eng[3], I->bs = eng[4];
     I->base = eng[5], I->tok = eng[6], I->div = eng[7];
     I->max_iters = max_iters;
+    I->ada = NULL;
 }
 
 static void run_one(job_t *J, int32_t i) {
@@ -432,8 +562,18 @@ static void run_one(job_t *J, int32_t i) {
               J->policy[i], J->k[i], J->memguard[i], J->delta[i], J->table + (size_t)i * 24,
               J->max_iters);
     size_t o = (size_t)i * (size_t)J->n_req;
-    int st = simulate(&I, J->ttft + o, J->ttlt + o, J->tbtmax + o, J->counters + (size_t)i * 8,
-                      NULL);
+    ada_t *A = NULL;
+    int st = 0;
+    if (J->ada && J->ada[(size_t)i * 10] != 0.0) {
+        A = (ada_t *)malloc(sizeof *A);
+        st = A ? ada_setup(A, J->ada + (size_t)i * 10, J->policy[i], J->k[i]) : TOR_EINVAL;
+        I.ada = A;
+    }
+    if (st == 0)
+        st = simulate(&I, J->ttft + o, J->ttlt + o, J->tbtmax + o, J->counters + (size_t)i * 8,
+                      J->gamma_out ? J->gamma_out + i : NULL,
+                      J->switch_out ? J->switch_out + i : NULL, NULL);
+    free(A);
     J->status[i] = st;
     if (st == 0) {
         const uint32_t *m[3] = {J->ttft + o, J->ttlt + o, J->tbtmax + o};
@@ -460,6 +600,7 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
                    const int32_t *memguard, const int64_t *delta, const int64_t *table,
                    const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
                    uint32_t *tbtmax, int64_t *counters, uint32_t *pct, int32_t *status,
+                   const double *ada, double *gamma_out, int64_t *switch_out,
                    int32_t n_threads) {
     if (n_traces < 1 || n_req < 1 || n_inst < 0) return TOR_EINVAL;
     for (int32_t i = 0; i < n_inst; i++)
@@ -468,8 +609,9 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
     if (eng[0] < 1 || eng[1] < 1 || eng[2] < 1 || eng[2] > eng[1] || eng[3] < 1 || eng[4] < 1 ||
         eng[5] < 1 || eng[6] < 0 || eng[7] < 1)
         return TOR_EINVAL;
-    job_t J = {n_req, n_inst, arrival, prompt, decode, trace, policy, k, memguard, delta, table,
-               eng, max_iters, ttft, ttlt, tbtmax, pct, counters, status, 0};
+    job_t J = {n_req,    n_inst, arrival, prompt, decode,    trace,      policy,
+               k,        memguard, delta, table,  eng,    max_iters, ttft,       ttlt,
+               tbtmax,   pct,    counters, status, ada,    gamma_out, switch_out, 0};
     if (n_threads < 1) n_threads = 1;
     if (n_threads > n_inst) n_threads = n_inst > 0 ? n_inst : 1;
     pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)n_threads);
@@ -487,7 +629,7 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
 
 int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
                    const int32_t *decode, int32_t policy, int32_t k, int32_t memguard,
-                   int64_t delta, const int64_t *table, const int32_t *eng,
+                   int64_t delta, const int64_t *table, const double *ada, const int32_t *eng,
                    int64_t max_iters, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
                    int64_t *counters, int64_t *log_iter, int64_t iter_cap,
                    int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
@@ -495,8 +637,19 @@ int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
     inst_t I;
     fill_inst(&I, eng, n_req, arrival, prompt, decode, policy, k, memguard, delta, table,
               max_iters);
+    ada_t *A = NULL;
+    if (ada && ada[0] != 0.0) {
+        A = (ada_t *)malloc(sizeof *A);
+        int rc = A ? ada_setup(A, ada, policy, k) : TOR_EINVAL;
+        if (rc) {
+            free(A);
+            return rc;
+        }
+        I.ada = A;
+    }
     log_t lg = {log_iter, iter_cap, 0, log_batch, batch_cap, 0, log_evict, evict_cap, 0, 0};
-    int st = simulate(&I, ttft, ttlt, tbtmax, counters, &lg);
+    int st = simulate(&I, ttft, ttlt, tbtmax, counters, NULL, NULL, &lg);
+    free(A);
     *n_iter = lg.n_it, *n_batch = lg.n_b, *n_evict = lg.n_ev;
     if (lg.full) return TOR_EINVAL;
     return st;

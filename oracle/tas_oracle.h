@@ -7,7 +7,7 @@
  *
  * What it computes: for every instance (one request trace, one scheduling
  * policy setting), an iteration-level simulation of a continuous-batching
- * LLM server (paper: Algorithm 1, UniBoost, with gamma fixed) whose per-step
+ * LLM server (paper: Algorithm 1, UniBoost, gamma fixed or adaptive) whose per-step
  * execution is replaced by an integer cost model, followed by the per-request
  * latencies TTFT / TTLT / max inter-token gap and their nearest-rank
  * percentiles (paper: section "Phase 4", the definition of t_p).
@@ -27,6 +27,15 @@
  *     idle us
  *   pct [n_inst*9] uint32: {TTFT, TTLT, TBTmax} x {P50, P90, P99}
  *   status [n_inst] int32: 0 or one of the TOR_E* codes
+ *
+ * Adaptive gamma (paper: Phase 4, gamma-Ada; Algorithm 2 UpdateGamma), per
+ * instance, optional (ada == NULL: none): ada[i*10 .. i*10+9] = {on (0/1),
+ * gamma0, beta in [0,1], gamma_min, gamma_max, eps_us, window (1..2048),
+ * min_samples (1..window), grid points (2..64), tau_us}. An adaptive instance
+ * (BOOST only) ignores its table: it uses the table of the grid point nearest
+ * to the current gamma (see tas_oracle.c). Outputs gamma_out [n_inst] (final
+ * gamma, 0 when not adaptive) and switch_out [n_inst] (grid-cell changes) may
+ * be NULL.
  */
 #ifndef TAS_ORACLE_H
 #define TAS_ORACLE_H
@@ -56,22 +65,30 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
                    const int32_t *memguard, const int64_t *delta, const int64_t *table,
                    const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
                    uint32_t *tbtmax, int64_t *counters, uint32_t *pct, int32_t *status,
+                   const double *ada, double *gamma_out, int64_t *switch_out,
                    int32_t n_threads);
 
 /* Run ONE instance and record its schedule, for invariant checks.
- * log_iter[it*6 + {0..5}] = {t_start, dt, batch size, KV blocks in use
- *   after formation, waiting count, resident count after formation};
+ * log_iter[it*8 + {0..7}] = {t_start, dt, batch size, KV blocks in use
+ *   after formation, waiting count, resident count after formation, grid
+ *   cell of the boost table used (-1 when gamma is fixed), the bits of gamma
+ *   (IEEE double)}; ada: 10 parameters as above, or NULL;
  * log_batch[...] = (request index, tokens) pairs, iteration after iteration;
  * log_evict[...] = (iteration, request index, forced flag) triples.
  * Capacities are in records. *n_iter, *n_batch, *n_evict receive the counts.
  * Returns the instance status, or TOR_EINVAL if a log buffer is too small. */
 int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
                    const int32_t *decode, int32_t policy, int32_t k, int32_t memguard,
-                   int64_t delta, const int64_t *table, const int32_t *eng,
+                   int64_t delta, const int64_t *table, const double *ada, const int32_t *eng,
                    int64_t max_iters, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
                    int64_t *counters, int64_t *log_iter, int64_t iter_cap,
                    int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
                    int64_t evict_cap, int64_t *n_iter, int64_t *n_batch, int64_t *n_evict);
+
+/* The adaptive-gamma grid of prm[10] (layout as above, on = 1): grid[G],
+ * midpoints bound[G-1], boost tables tables[G*24]. Returns 0 or TOR_EINVAL. */
+int tas_oracle_ada_grid(const double *prm, int32_t k, double *grid, double *bound,
+                        int64_t *tables);
 
 /* MemGuard level of signal w at granularity k: floor(log2(max(w,k)/k)),
  * capped at 23 (paper, Eq. memguard_level). */

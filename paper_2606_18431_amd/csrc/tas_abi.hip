@@ -103,6 +103,7 @@ double log1mexp(double x) { return x <= 0.6931471805599453 ? std::log(-std::expm
 
 int check_setting(const tas_setting &s, int32_t n_traces) {
     if (s.trace < 0 || s.trace >= n_traces) return TAS_EINVAL;
+    if (s.ada != 0) return TAS_EINVAL;  // adaptive gamma: not built yet
     if (s.policy < TAS_FCFS || s.policy > TAS_TRAIL) return TAS_EINVAL;
     if (s.delta_us < 0) return TAS_EINVAL;
     if (s.policy != TAS_BOOST) {

@@ -41,7 +41,11 @@ class tas_setting(ctypes.Structure):
     _fields_ = [("trace", ctypes.c_int32), ("policy", ctypes.c_int32), ("k", ctypes.c_int32),
                 ("memguard", ctypes.c_int32), ("delta_us", ctypes.c_int64),
                 ("gamma", ctypes.c_double), ("table_given", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("boost_us", ctypes.c_int64 * LEVELS)]
+                ("ada", ctypes.c_int32), ("boost_us", ctypes.c_int64 * LEVELS),
+                ("ada_beta", ctypes.c_double), ("ada_gamma_min", ctypes.c_double),
+                ("ada_gamma_max", ctypes.c_double), ("ada_eps_us", ctypes.c_double),
+                ("ada_window", ctypes.c_int32), ("ada_min_samples", ctypes.c_int32),
+                ("ada_grid", ctypes.c_int32), ("ada_reserved", ctypes.c_int32)]
 
 
 class tas_params(ctypes.Structure):
@@ -55,7 +59,7 @@ class tas_params(ctypes.Structure):
                 ("inst", ctypes.c_void_p)]
 
 
-assert ctypes.sizeof(tas_setting) == W.SETTING_DTYPE.itemsize == 232
+assert ctypes.sizeof(tas_setting) == W.SETTING_DTYPE.itemsize == 280
 
 EXPORTS = ["tas_workspace_bytes", "tas_create", "tas_run", "tas_percentiles", "tas_latencies",
            "tas_counters", "tas_status", "tas_instance_status", "tas_destroy", "tas_strerror",

@@ -22,7 +22,7 @@ The policy-parameter grid per trace: setting 0 = FCFS, setting 1 = oracle-length
 SRPT, then pairs (UniBoost with MemGuard, vanilla boost) over log-spaced gamma.
 ``make(cfg, grid="comparators")`` instead runs every trace under the paper's
 comparison policies (FCFS, SRPT, SPF, SJF, LAS, TRAIL) beside UniBoost and vanilla
-boost.
+boost; ``make(cfg, grid="ada")`` runs fixed against adaptive gamma (Phase 4).
 """
 from __future__ import annotations
 
@@ -46,8 +46,16 @@ SETTING_DTYPE = np.dtype(
         ("delta_us", np.int64),
         ("gamma", np.float64),
         ("table_given", np.int32),
-        ("pad", np.int32),
+        ("ada", np.int32),
         ("boost_us", np.int64, (LEVELS,)),
+        ("ada_beta", np.float64),
+        ("ada_gamma_min", np.float64),
+        ("ada_gamma_max", np.float64),
+        ("ada_eps_us", np.float64),
+        ("ada_window", np.int32),
+        ("ada_min_samples", np.int32),
+        ("ada_grid", np.int32),
+        ("ada_reserved", np.int32),
     ]
 )
 
@@ -102,10 +110,16 @@ class Workload:
 # ---------------------------------------------------------------- settings
 
 
-def setting(trace, policy, k=1, memguard=0, delta_us=0, gamma=0.0, table=None):
+def setting(trace, policy, k=1, memguard=0, delta_us=0, gamma=0.0, table=None, ada=None):
+    """One instance record. ``ada``: adaptive-gamma parameters (keys of ADA
+    without the ``ada_`` prefix, e.g. ``dict(ADA)``), gamma being the start."""
     s = np.zeros((), dtype=SETTING_DTYPE)
     s["trace"], s["policy"], s["k"], s["memguard"] = trace, policy, k, memguard
     s["delta_us"], s["gamma"] = delta_us, gamma
+    if ada is not None:
+        s["ada"] = 1
+        for key, v in ada.items():
+            s["ada_" + key] = v
     if table is not None:
         t = np.asarray(table, dtype=np.int64)
         s["boost_us"][: len(t)] = t
@@ -116,6 +130,11 @@ def setting(trace, policy, k=1, memguard=0, delta_us=0, gamma=0.0, table=None):
 
 UNIBOOST = dict(k=256, memguard=1, delta_us=100_000)  # defaults k=256, delta=0.1 s
 VANILLA = dict(k=1, memguard=0, delta_us=0)
+# Adaptive gamma: EMA weight per iteration, clip bounds = grid ends (10 grid
+# points per decade), floor of the tail band in us, window of completed
+# requests and the samples needed before the first update.
+ADA = dict(beta=0.01, gamma_min=1e-5, gamma_max=1e-1, eps_us=1000.0, window=256,
+           min_samples=64, grid=41)
 
 
 def settings_grid(n_traces: int, n_settings: int) -> np.ndarray:
@@ -292,12 +311,31 @@ def _trace(cfg: int, trace: int, n: int, eng: Engine):
     return arr, p, d
 
 
+def ada_settings(n_traces: int, ada: dict | None = None) -> np.ndarray:
+    """Per trace, 8 settings: for gamma0 in (1e-4, 1e-3, 1e-2) UniBoost with that
+    fixed gamma and UniBoost with adaptive gamma started there, then vanilla
+    boost with adaptive gamma from 1e-3, then FCFS. Instance id = trace * 8 + s."""
+    ada = dict(ADA if ada is None else ada)
+    per = []
+    for g0 in (1e-4, 1e-3, 1e-2):
+        per.append(dict(policy=BOOST, gamma=g0, **UNIBOOST))
+        per.append(dict(policy=BOOST, gamma=g0, ada=ada, **UNIBOOST))
+    per.append(dict(policy=BOOST, gamma=1e-3, ada=ada, **VANILLA))
+    per.append(dict(policy=FCFS))
+    out = np.zeros(n_traces * len(per), dtype=SETTING_DTYPE)
+    for t in range(n_traces):
+        for s, kw in enumerate(per):
+            out[t * len(per) + s] = setting(t, **kw)
+    return out
+
+
 def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
          n_req: int | None = None, grid: str = "sweep") -> Workload:
     """Build workload ``cfg``. The optional overrides shrink it (fewer traces,
     settings or requests) for tests; traces keep their seeds, so trace t of a
     shrunk workload equals trace t of the full one when n_req is unchanged.
-    ``grid="comparators"`` replaces the settings grid by comparator_settings."""
+    ``grid="comparators"`` replaces the settings grid by comparator_settings,
+    ``grid="ada"`` by ada_settings."""
     T0, S0, N0 = SHAPES[cfg]
     T = T0 if n_traces is None else n_traces
     S = S0 if n_settings is None else n_settings
@@ -310,6 +348,9 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
         arr[t], pr[t], de[t] = _trace(cfg, t, N, eng)
     if grid == "comparators":
         sets = comparator_settings(T)
+        S = 8
+    elif grid == "ada":
+        sets = ada_settings(T)
         S = 8
     elif cfg == 0 and S == 8:
         st = [setting(0, FCFS), setting(0, SRPT)]

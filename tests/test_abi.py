@@ -4,6 +4,7 @@ invalid inputs before touching the GPU (no compute calls here)."""
 import ctypes
 import os
 import re
+import subprocess
 
 import numpy as np
 import pytest
@@ -31,10 +32,30 @@ def test_library_exports_every_declared_symbol():
     assert set(tas.EXPORTS) <= set(names)
 
 
-def test_struct_layouts_match_header():
-    assert ctypes.sizeof(tas.tas_setting) == 232
-    assert ctypes.sizeof(tas.tas_params) == 72
-    assert ctypes.sizeof(tas.tas_traces) == 32
+def test_struct_layouts_match_header(tmp_path):
+    """The ctypes mirrors have the C compiler's size and field offsets."""
+    structs = [tas.tas_setting, tas.tas_params, tas.tas_traces]
+    lines = ['#include <stddef.h>', '#include <stdio.h>', '#include "tas.h"', 'int main(void) {']
+    for st in structs:
+        n = st.__name__
+        lines.append(f'printf("{n} %zu\\n", sizeof({n}));')
+        for f, _ in st._fields_:
+            lines.append(f'printf("{n}.{f} %zu\\n", offsetof({n}, {f}));')
+    lines.append('return 0; }')
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.check_call(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), "-o", str(exe),
+                           str(src)])
+    got = dict(l.split() for l in subprocess.check_output([str(exe)], text=True).splitlines())
+    for st in structs:
+        n = st.__name__
+        assert int(got[n]) == ctypes.sizeof(st), n
+        for f, _ in st._fields_:
+            assert int(got[f"{n}.{f}"]) == getattr(st, f).offset, (n, f)
+    assert ctypes.sizeof(tas.tas_setting) == W.SETTING_DTYPE.itemsize
+    for f, _ in tas.tas_setting._fields_:
+        assert W.SETTING_DTYPE.fields[f][1] == getattr(tas.tas_setting, f).offset, f
 
 
 @pytest.mark.parametrize("k", [1, 7, 16, 256])

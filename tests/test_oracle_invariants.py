@@ -4,8 +4,9 @@ The replay below rebuilds every request's KV, emitted tokens and timestamps
 from the logged batches and evictions alone, re-derives each iteration's
 duration from the cost model, and checks the result against the oracle's
 outputs and the rules: KV capacity, batch limits, work conservation, token
-conservation, completion exactly once, FCFS dispatch order, the MemGuard
-eligibility of every voluntary eviction and the Phase 3 revision bound.
+conservation, completion exactly once, FCFS dispatch order, every batch in
+ascending (key, idx) order of the policy's keys, the MemGuard eligibility of
+every voluntary eviction and the Phase 3 revision bound.
 """
 import math
 
@@ -20,7 +21,23 @@ def blocks(x, bs):
     return -(-x // bs)
 
 
-def replay(a, p, d, e, o, policy, k=1, memguard=0):
+def key_of(policy, r, a, p, d, kv, dec, k, table):
+    """Iteration-start priority key of request r (lower is served first)."""
+    if policy == 0:
+        return int(a[r])  # FCFS: arrival
+    if policy in (1, 6):
+        return int(p[r] + d[r] - 1 - kv[r])  # SRPT / TRAIL: remaining computed tokens
+    if policy == 3:
+        return int(p[r])  # SPF
+    if policy == 4:
+        return int(d[r])  # SJF
+    if policy == 5:
+        return int(p[r] + dec[r])  # LAS: attained service
+    lvl = min(23, (max(int(p[r] + dec[r]), k) // k).bit_length() - 1)
+    return int(a[r]) - int(table[lvl])  # boost: a - b(quantized signal)
+
+
+def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None):
     N = len(a)
     bs = e.block_tokens
     kv = np.zeros(N, np.int64)
@@ -70,6 +87,11 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0):
         assert np.all(ns >= 1) and np.all(ns <= e.chunk) and ns.sum() <= e.max_tokens
         members = batch[:, 0].tolist()
         assert len(set(members)) == nb
+        # formation takes candidates in ascending (key, idx) order of the
+        # iteration-start keys (batch members were not evicted, so their kv is
+        # still the iteration-start value)
+        keys = [(key_of(policy, r, a, p, d, kv, dec, k, table), r) for r in members]
+        assert keys == sorted(keys)
         assert not (set(members) & evicted)
         for r in members:
             assert a[r] <= t0 and not done[r]
@@ -159,7 +181,10 @@ def test_replay_invariants(seed, ei, pi):
     o = oracle.log(a, p, d, e, pol["policy"], k=pol.get("k", 1), memguard=pol.get("memguard", 0),
                    delta_us=pol.get("delta_us", 0), gamma=pol.get("gamma"))
     assert o["rc"] == 0
-    replay(a, p, d, e, o, pol["policy"], k=pol.get("k", 1), memguard=pol.get("memguard", 0))
+    table = (oracle.boost_table(pol["gamma"], pol.get("k", 1), e.tau_us)
+             if pol["policy"] == 2 else None)
+    replay(a, p, d, e, o, pol["policy"], k=pol.get("k", 1), memguard=pol.get("memguard", 0),
+           table=table)
 
 
 def test_replay_sees_evictions():
