@@ -6,6 +6,7 @@ percentile kernel. Inputs (traces, settings) are resident in HBM before the
 timed region. Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 4]
+                 [--grid sweep|ada|comparators] [--no-ada]
 
 Roofline: the simulation kernel is counted against HBM bandwidth with
 algorithmic bytes of 32 B per request-iteration (read + write of the request's
@@ -79,6 +80,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", type=int, default=4, choices=[0, 1, 2, 3, 4])
     ap.add_argument("--traces", type=int, default=None, help="shrink the sweep (testing)")
+    ap.add_argument("--grid", default="sweep", choices=["sweep", "ada", "comparators"],
+                    help="settings grid per trace (default: the gamma sweep)")
+    ap.add_argument("--no-ada", action="store_true",
+                    help="run the adaptive settings of the grid with gamma fixed at its start")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
     ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--list-cap", type=int, default=0,
@@ -109,9 +114,14 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": n, "ok": bool(dst[-1].item() == 1)}))
         return
-    w = W.make(args.workload, n_traces=args.traces)
+    w = W.make(args.workload, n_traces=args.traces, grid=args.grid)
     name = f"{W.NAMES[args.workload]}: {w.n_traces} traces x {w.meta['n_settings']} settings x " \
            f"{w.n_req} requests"
+    if args.grid != "sweep":
+        name += f", {args.grid} settings grid"
+    if args.no_ada:
+        w.settings["ada"] = 0
+        name += " with gamma fixed"
     print(f"[bench] building {name}", file=sys.stderr, flush=True)
     sim = tas.Simulation(w, device=dev, list_cap=args.list_cap)
     stream = torch.cuda.current_stream()

@@ -146,8 +146,9 @@ typedef struct {
     int64_t max_iters;     /* per-instance iteration limit (TAS_ELIVELOCK)     */
     double tau_us;         /* microseconds per token of boost, > 0             */
     int32_t list_cap;      /* on-chip candidate entries per instance, in
-                              [max_seqs + 64, 4032]; 0 picks max_seqs + 128
-                              rounded up to 64                                 */
+                              [max_seqs + 64, 4032]; 0 picks max_seqs + 128,
+                              or max_seqs + 512 when some instance adapts
+                              gamma, rounded up to 64                          */
     int32_t spill_cap;     /* waiting entries per instance kept in HBM beyond
                               the on-chip list; 0 = n_req                      */
     int32_t n_inst;
@@ -205,6 +206,12 @@ int tas_latencies(tas_ctx *ctx, uint32_t *d_ttft, uint32_t *d_ttlt, uint32_t *d_
  * idle us. */
 int tas_counters(tas_ctx *ctx, int64_t *d_out, void *stream);
 
+/* Enqueue copies of the adaptive-gamma state at the end of each instance:
+ * d_gamma DEVICE double [n_inst] (the final gamma; 0 for an instance without
+ * adaptive gamma) and d_switches DEVICE int64 [n_inst] (how often the boost
+ * table changed grid point). Either pointer may be NULL. */
+int tas_gamma(tas_ctx *ctx, double *d_gamma, int64_t *d_switches, void *stream);
+
 /* Synchronise the stream of the last enqueued call and return TAS_OK or the
  * first per-instance error (lowest instance index), e.g. TAS_ELIVELOCK,
  * TAS_EOVERFLOW, TAS_ECAPACITY; TAS_EHIP if the stream reports a failure. */
@@ -224,6 +231,16 @@ const char *tas_strerror(int code);
  * exp(-gamma w))), evaluated in double precision on the host. out: HOST
  * int64[TAS_LEVELS]. Returns TAS_EINVAL unless gamma > 0, k >= 1, tau > 0. */
 int tas_boost_table(double gamma, int32_t k, double tau_us, int64_t *out);
+
+/* The adaptive-gamma grid of a setting (ada = 1 and valid ada_* fields, as
+ * tas_create requires): grid[j] = gamma_min (gamma_max/gamma_min)^(j/(G-1)),
+ * bound[j] = sqrt(grid[j] grid[j+1]) for j < G-1, and tables[j*TAS_LEVELS ..]
+ * = the tas_boost_table of grid[j] (k and tau_us as given), all evaluated in
+ * double precision on the host (Phase 4 with the boost curve of
+ * Eq. boost_function). grid, bound, tables: HOST arrays of G, G-1 and
+ * G*TAS_LEVELS elements. Returns TAS_EINVAL for an invalid setting. */
+int tas_ada_grid(const tas_setting *s, double tau_us, double *grid, double *bound,
+                 int64_t *tables);
 
 /* The boost table an instance uses (as built by tas_create). out: HOST
  * int64[TAS_LEVELS]. */

@@ -19,6 +19,9 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           # every floating-point step of the adaptive gamma is one rounded
+           # IEEE operation, as in its definition: no fused multiply-add
+           "-ffp-contract=off",
            "-Wall", "-Wno-unused-function",
            "-I", os.path.join(ROOT, "include"), "-I", CSRC, "-o", tmp] + srcs
     if verbose:

@@ -19,6 +19,7 @@ struct tas_ctx {
     int64_t lds_bytes = 0, lds_retry = 0;
     tas::SimArgs args{};
     std::vector<tas::DevSetting> settings;
+    std::vector<tas::DevAda> ada;
     hipStream_t last_stream = nullptr;
 };
 
@@ -31,15 +32,32 @@ constexpr int64_t kTwo42 = int64_t(1) << 42;
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-    size_t arrival, prompt, decode, settings, tfirst, tlast, tbtw, ttft, ttlt, tbtmax, counters,
-        status, spill, ovf, total;
+    size_t arrival, prompt, decode, settings, ada, tfirst, tlast, tbtw, ttft, ttlt, tbtmax,
+        counters, status, gamma, switches, spill, ovf, total;
 };
+
+// Adaptive-gamma instances and their largest window (clamped: an invalid
+// window is rejected by check_setting).
+int32_t ada_count(const tas_params *p, int32_t *wmax) {
+    int32_t n = 0, w = 0;
+    for (int32_t i = 0; i < p->n_inst; i++) {
+        if (p->inst[i].ada == 0) continue;
+        n++;
+        w = std::max(w, std::min(std::max(p->inst[i].ada_window, 0), tas::kAdaWindowMax));
+    }
+    *wmax = w;
+    return n;
+}
 
 // First pass: room for about max_seqs residents plus a window of waiting
 // entries, small enough for several instances per compute unit. Instances
 // that hold more residents than that rerun in a second pass with a large list.
-int32_t default_list_cap(int32_t max_seqs) {
-    int64_t lc = (int64_t)max_seqs + 128;
+// With adaptive gamma every grid change reorders the queue; requests admitted
+// under the old order keep their KV until the budget binds, so residents
+// outside the batch accumulate (to about 2.8 max_seqs on the large sweep):
+// launches with adaptive instances start with 384 more entries.
+int32_t default_list_cap(int32_t max_seqs, bool adaptive) {
+    int64_t lc = (int64_t)max_seqs + (adaptive ? 512 : 128);
     lc = (lc + 63) / 64 * 64;
     return (int32_t)std::min<int64_t>(lc, tas::kMaxListCap);
 }
@@ -64,12 +82,15 @@ bool shape_ok(const tas_traces *t) {
 
 // Effective capacities; false if invalid. *rc == *lc means no second pass.
 bool caps(const tas_traces *t, const tas_params *p, int32_t *lc, int32_t *rc, int32_t *sc) {
-    const int32_t l = p->list_cap ? p->list_cap : default_list_cap(p->max_seqs);
+    int32_t wmax;
+    const bool adaptive = ada_count(p, &wmax) > 0;
+    const int32_t l = p->list_cap ? p->list_cap : default_list_cap(p->max_seqs, adaptive);
     if ((int64_t)l < (int64_t)p->max_seqs + 64 || l > tas::kMaxListCap) return false;
-    if (tas::lds_bytes_for(l) > kMaxLds) return false;
+    if (tas::lds_bytes_for(l, wmax) > kMaxLds) return false;
     int32_t r = p->retry_cap ? p->retry_cap : default_retry_cap(l);
     if (r < l) r = l;
-    if (r > tas::kMaxListCap || tas::lds_bytes_for(r) > kMaxLds) return false;
+    while (r > l && tas::lds_bytes_for(r, wmax) > kMaxLds) r -= 64;  // room for the window
+    if (r > tas::kMaxListCap || tas::lds_bytes_for(r, wmax) > kMaxLds) return false;
     *lc = l;
     *rc = r;
     *sc = p->spill_cap ? p->spill_cap : t->n_req;
@@ -84,6 +105,8 @@ bool layout(const tas_traces *t, const tas_params *p, int32_t rc, int32_t sc, La
     L->prompt = o, o = align256(o + tn * 4);
     L->decode = o, o = align256(o + tn * 4);
     L->settings = o, o = align256(o + (size_t)p->n_inst * sizeof(tas::DevSetting));
+    int32_t wmax;
+    L->ada = o, o = align256(o + (size_t)ada_count(p, &wmax) * sizeof(tas::DevAda));
     L->tfirst = o, o = align256(o + in * 8);
     L->tlast = o, o = align256(o + in * 8);
     L->tbtw = o, o = align256(o + in * 4);
@@ -92,6 +115,8 @@ bool layout(const tas_traces *t, const tas_params *p, int32_t rc, int32_t sc, La
     L->tbtmax = o, o = align256(o + in * 4);
     L->counters = o, o = align256(o + (size_t)p->n_inst * 8 * 8);
     L->status = o, o = align256(o + (size_t)p->n_inst * 4);
+    L->gamma = o, o = align256(o + (size_t)p->n_inst * 8);
+    L->switches = o, o = align256(o + (size_t)p->n_inst * 8);
     L->spill = o, o = align256(o + (size_t)p->n_inst * (size_t)sc * sizeof(tas::Rec));
     L->ovf = o, o = align256(o + (size_t)p->n_inst * (size_t)(rc + tas::kStage) * sizeof(tas::Rec));
     L->total = o;
@@ -101,9 +126,18 @@ bool layout(const tas_traces *t, const tas_params *p, int32_t rc, int32_t sc, La
 // ln(1 - exp(-x)) for x > 0, accurate on both sides of ln 2 (Maechler 2012).
 double log1mexp(double x) { return x <= 0.6931471805599453 ? std::log(-std::expm1(-x)) : std::log1p(-std::exp(-x)); }
 
+bool ada_ok(const tas_setting &s) {
+    return s.policy == TAS_BOOST && !s.table_given && s.ada_beta >= 0.0 && s.ada_beta <= 1.0 &&
+           s.ada_gamma_min > 0.0 && s.ada_gamma_max > s.ada_gamma_min &&
+           std::isfinite(s.ada_gamma_max) && s.gamma >= s.ada_gamma_min &&
+           s.gamma <= s.ada_gamma_max && s.ada_eps_us > 0.0 && std::isfinite(s.ada_eps_us) &&
+           s.ada_window >= 1 && s.ada_window <= TAS_ADA_WINDOW_MAX && s.ada_min_samples >= 1 &&
+           s.ada_min_samples <= s.ada_window && s.ada_grid >= 2 && s.ada_grid <= TAS_ADA_GRID_MAX;
+}
+
 int check_setting(const tas_setting &s, int32_t n_traces) {
     if (s.trace < 0 || s.trace >= n_traces) return TAS_EINVAL;
-    if (s.ada != 0) return TAS_EINVAL;  // adaptive gamma: not built yet
+    if (s.ada != 0 && (s.ada != 1 || !ada_ok(s))) return TAS_EINVAL;
     if (s.policy < TAS_FCFS || s.policy > TAS_TRAIL) return TAS_EINVAL;
     if (s.delta_us < 0) return TAS_EINVAL;
     if (s.policy != TAS_BOOST) {
@@ -136,6 +170,21 @@ int tas_boost_table(double gamma, int32_t k, double tau_us, int64_t *out) {
         const double us = tau_us * b;
         out[j] = us >= cap ? kTwo42 : (int64_t)std::llround(us);
     }
+    return TAS_OK;
+}
+
+int tas_ada_grid(const tas_setting *s, double tau_us, double *grid, double *bound,
+                 int64_t *tables) {
+    if (!s || !grid || !bound || !tables || s->ada != 1 || !ada_ok(*s) || s->k < 1 ||
+        !(tau_us > 0.0) || !std::isfinite(tau_us))
+        return TAS_EINVAL;
+    const int G = s->ada_grid;
+    const double lo = s->ada_gamma_min, hi = s->ada_gamma_max;
+    for (int j = 0; j < G; j++) grid[j] = lo * std::pow(hi / lo, (double)j / (double)(G - 1));
+    for (int j = 0; j + 1 < G; j++) bound[j] = std::sqrt(grid[j] * grid[j + 1]);
+    for (int j = 0; j < G; j++)
+        if (tas_boost_table(grid[j], s->k, tau_us, tables + (size_t)j * TAS_LEVELS))
+            return TAS_EINVAL;
     return TAS_OK;
 }
 
@@ -182,9 +231,13 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     if (!c) return TAS_ENOMEM;
     c->n_traces = t->n_traces, c->n_req = N, c->n_inst = p->n_inst;
     c->list_cap = lc, c->spill_cap = sc, c->retry_cap = rc;
-    c->lds_bytes = tas::lds_bytes_for(lc);
-    c->lds_retry = tas::lds_bytes_for(rc);
+    int32_t wmax;
+    const int32_t n_ada = ada_count(p, &wmax);
+    c->lds_bytes = tas::lds_bytes_for(lc, wmax);
+    c->lds_retry = tas::lds_bytes_for(rc, wmax);
     c->settings.resize((size_t)p->n_inst);
+    c->ada.resize((size_t)n_ada);
+    int32_t ai = 0;
     for (int32_t i = 0; i < p->n_inst; i++) {
         const tas_setting &s = p->inst[i];
         tas::DevSetting &d = c->settings[(size_t)i];
@@ -192,9 +245,25 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
         d.trace = s.trace, d.policy = s.policy, d.k = s.policy == TAS_BOOST ? s.k : 1;
         d.memguard = s.policy == TAS_BOOST ? s.memguard : 0;
         d.delta = s.policy == TAS_BOOST ? s.delta_us : 0;
+        d.ada = -1;
         if (s.policy == TAS_BOOST) {
             if (s.table_given) std::memcpy(d.bt, s.boost_us, sizeof d.bt);
             else tas_boost_table(s.gamma, s.k, p->tau_us, d.bt);
+        }
+        if (s.ada) {
+            tas::DevAda &A = c->ada[(size_t)ai];
+            std::memset(&A, 0, sizeof A);
+            double grid[tas::kAdaGridMax];
+            tas_ada_grid(&s, p->tau_us, grid, A.bound, &A.table[0][0]);
+            for (int j = s.ada_grid - 1; j < tas::kAdaGridMax; j++) A.bound[j] = INFINITY;
+            A.beta = s.ada_beta, A.gmin = s.ada_gamma_min, A.gmax = s.ada_gamma_max;
+            A.eps = s.ada_eps_us, A.num = p->tau_us * std::log(5.0), A.gamma0 = s.gamma;
+            A.window = s.ada_window, A.min_samples = s.ada_min_samples, A.grid = s.ada_grid;
+            int cell = 0;  // the grid point nearest gamma0 in log scale
+            while (cell + 1 < s.ada_grid && s.gamma >= A.bound[cell]) cell++;
+            A.cell0 = cell;
+            std::memcpy(d.bt, A.table[cell], sizeof d.bt);
+            d.ada = ai++;
         }
     }
     char *ws = (char *)d_ws;
@@ -205,6 +274,12 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
         ok = hipMemcpy(ws + L.settings, c->settings.data(),
                        c->settings.size() * sizeof(tas::DevSetting),
                        hipMemcpyHostToDevice) == hipSuccess;
+    if (ok && n_ada > 0)
+        ok = hipMemcpy(ws + L.ada, c->ada.data(), c->ada.size() * sizeof(tas::DevAda),
+                       hipMemcpyHostToDevice) == hipSuccess;
+    // the fixed-gamma kernel build leaves the adaptive outputs alone: zero them
+    if (ok && p->n_inst > 0)
+        ok = hipMemset(ws + L.gamma, 0, L.spill - L.gamma) == hipSuccess;
     if (!ok) {
         delete c;
         return TAS_EHIP;
@@ -231,6 +306,10 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     a.div = p->iter_ctx_div, a.list_cap = lc, a.spill_cap = sc;
     a.div_magic = a.div >= 2 ? ~0ull / (uint64_t)a.div + 1 : 0;
     a.ovf_stride = rc + tas::kStage, a.retry = 0;
+    a.ada = (const tas::DevAda *)(ws + L.ada);
+    a.gamma_out = (double *)(ws + L.gamma);
+    a.switch_out = (int64_t *)(ws + L.switches);
+    a.ada_window = wmax;
     *out = c;
     return TAS_OK;
 }
@@ -280,6 +359,20 @@ int tas_counters(tas_ctx *c, int64_t *d_out, void *stream) {
                           hipMemcpyDeviceToDevice, (hipStream_t)stream) == hipSuccess
                ? TAS_OK
                : TAS_EHIP;
+}
+
+int tas_gamma(tas_ctx *c, double *d_gamma, int64_t *d_switches, void *stream) {
+    if (!c) return TAS_EINVAL;
+    c->last_stream = (hipStream_t)stream;
+    if (c->n_inst == 0) return TAS_OK;
+    const size_t bytes = (size_t)c->n_inst * 8;
+    if (d_gamma && hipMemcpyAsync(d_gamma, c->args.gamma_out, bytes, hipMemcpyDeviceToDevice,
+                                  (hipStream_t)stream) != hipSuccess)
+        return TAS_EHIP;
+    if (d_switches && hipMemcpyAsync(d_switches, c->args.switch_out, bytes,
+                                     hipMemcpyDeviceToDevice, (hipStream_t)stream) != hipSuccess)
+        return TAS_EHIP;
+    return TAS_OK;
 }
 
 int tas_instance_status(tas_ctx *c, int32_t *d_out, void *stream) {

@@ -11,6 +11,9 @@ constexpr int64_t kKeyOff = int64_t(1) << 42;
 constexpr int kIdxBits = 21;            // packed key = (key + 2^42) << 21 | idx
 constexpr uint64_t kIdxMask = (uint64_t(1) << kIdxBits) - 1;
 
+constexpr int kAdaGridMax = 64;       // grid points of the adaptive gamma
+constexpr int kAdaWindowMax = 2048;   // latencies in its window
+
 // Policy parameters of one instance, as the kernel reads them.
 struct DevSetting {
     int32_t trace;
@@ -18,7 +21,21 @@ struct DevSetting {
     int32_t k;
     int32_t memguard;
     int64_t delta;
-    int64_t bt[kLevels];  // boost in us per MemGuard level (non-increasing)
+    int64_t bt[kLevels];  // boost in us per MemGuard level (non-increasing);
+                          // with adaptive gamma, the table of the first grid cell
+    int32_t ada;          // index into SimArgs::ada, or -1
+    int32_t pad;
+};
+
+// Adaptive gamma of one instance (host-built): the update constants, the
+// grid midpoints (a cell is the number of midpoints <= gamma) and the boost
+// table of every grid point.
+struct DevAda {
+    double beta, gmin, gmax, eps, num;  // num = tau ln 5
+    double gamma0;
+    int32_t window, min_samples, grid, cell0;
+    double bound[kAdaGridMax];          // [grid - 1] midpoints, then +infinity
+    int64_t table[kAdaGridMax][kLevels];
 };
 
 // A candidate-list record as it is parked in HBM (spilled waiting entries and
@@ -57,14 +74,27 @@ struct SimArgs {
     int32_t spill_cap;
     int32_t ovf_stride;  // records per instance in `ovf` (largest list + 64)
     int32_t retry;       // second pass: only instances whose first pass ran out of list
+    const DevAda *ada;   // [number of adaptive instances]
+    double *gamma_out;   // [n_inst] final adaptive gamma (0 without)
+    int64_t *switch_out; // [n_inst] grid-cell changes
+    int32_t ada_window;  // largest window over the adaptive instances (LDS), 0 if none
+    int32_t pad;
 };
 
-// Dynamic LDS bytes per workgroup for a list capacity.
-inline int64_t lds_bytes_for(int32_t list_cap) {
+// Bytes of the adaptive-gamma block: its state (gamma, gamma_hat, counters),
+// then the window in completion order and sorted, 4 bytes per latency each.
+constexpr int64_t kAdaStateBytes = 48;
+inline int64_t ada_lds_bytes(int32_t window) {
+    return window > 0 ? kAdaStateBytes + int64_t(window) * 8 : 0;
+}
+
+// Dynamic LDS bytes per workgroup for a list capacity and the largest
+// adaptive-gamma window (0: none).
+inline int64_t lds_bytes_for(int32_t list_cap, int32_t ada_window = 0) {
     const int64_t cap = int64_t(list_cap) + kStage;  // the list and its overflow region
     // pk (8 B) + gs, w, kv, left, tl (4 B) per slot; alignment of the boost
-    // table; the boost table
-    return cap * (8 + 5 * 4) + 8 + kLevels * 8;
+    // table; the boost table; the adaptive-gamma block
+    return cap * (8 + 5 * 4) + 8 + kLevels * 8 + ada_lds_bytes(ada_window);
 }
 constexpr int kMaxChunk = (1 << 15) - 1;  // the chunk size lives in 15 bits of the flag word
 // At most 64 chunks of 64 entries (list + overflow region): chunk bitmaps are

@@ -1,8 +1,10 @@
 // tas_sim.hip - the iteration-level serving simulation, one wavefront per
 // instance (one trace x one policy setting), for gfx950.
 //
-// What each iteration computes (arXiv 2606.18431, Algorithm 1 with gamma
-// fixed; Phase 2 unified key and hysteresis; Phase 3 MemGuard):
+// What each iteration computes (arXiv 2606.18431, Algorithm 1; Phase 2
+// unified key and hysteresis; Phase 3 MemGuard; Phase 4 adaptive gamma):
+//   0. with adaptive gamma, gamma follows the tail of the recent end-to-end
+//      latencies, and the boost table that of its nearest grid point;
 //   1. arrivals with a_i <= t join the waiting set;
 //   2. every waiting or resident request has a key; candidates are taken in
 //      ascending (key, idx) order;
@@ -181,7 +183,19 @@ struct Lds {
     uint64_t *k;
     uint32_t *tl;
     int64_t *bt;
+    struct AdaLds *as;  // adaptive gamma: state, then the window in completion
+    uint32_t *wr, *ws;  // order (a ring) and sorted
 };
+
+// Adaptive-gamma state of one instance (LDS, written by lane 0).
+struct AdaLds {
+    double gamma, ghat;      // current gamma, latest estimate
+    int32_t wn, whead;       // latencies in the window, ring slot of the oldest
+    int32_t cell, wnew;      // grid cell in use; 1: the window changed since ghat
+    int64_t switches;        // grid-cell changes
+    int32_t window, min_samples;
+};
+static_assert(sizeof(AdaLds) == kAdaStateBytes, "adaptive-gamma LDS block");
 
 struct R {  // one candidate-list record in registers
     uint64_t pk = 0;
@@ -254,7 +268,7 @@ DEV R permute_rec(const R &x, int dest) {
 // 16-token block gets its own instantiation), -1 otherwise. The policy is a
 // run-time value: one copy of the code serves every policy, so workgroups of
 // different policies on one compute unit share the instruction cache.
-template <int BSH>
+template <int BSH, bool ADA>
 struct Sim {
     const SimArgs &A;
     Lds S;
@@ -288,6 +302,10 @@ struct Sim {
     // clears vm_ok and the next victim search rebuilds them.
     uint64_t vm_res, vm_ev;
     bool vm_ok;
+    // adaptive gamma (null without): constants, and lane j < grid - 1 holds
+    // the midpoint above grid point j (+infinity beyond)
+    const DevAda *ad;
+    double bnd;
 
     DEV Sim(const SimArgs &a, const DevSetting &st, int i, unsigned char *smem) : A(a) {
         inst = i;
@@ -312,8 +330,27 @@ struct Sim {
         S.k = (uint64_t *)(smem + o), o += (size_t)cap * 8;
         S.tl = (uint32_t *)(smem + o), o += (size_t)cap * 4;
         o = (o + 7) & ~(size_t)7;
-        S.bt = (int64_t *)(smem + o);
+        S.bt = (int64_t *)(smem + o), o += (size_t)kLevels * 8;
         for (int j = lane(); j < kLevels; j += kWave) S.bt[j] = st.bt[j];
+        ad = nullptr;
+        bnd = 0.0;
+        if constexpr (ADA) {
+            S.as = (AdaLds *)(smem + o), o += kAdaStateBytes;
+            S.wr = (uint32_t *)(smem + o), o += (size_t)a.ada_window * 4;
+            S.ws = (uint32_t *)(smem + o);
+            ad = st.ada >= 0 ? a.ada + st.ada : nullptr;
+        }
+        if (ADA && ad) {  // the table of the first cell is st.bt
+            bnd = ad->bound[lane()];
+            if (lane() == 0) {
+                AdaLds &G = *S.as;
+                G.gamma = ad->gamma0, G.ghat = 0.0;
+                G.wn = G.whead = G.wnew = 0;
+                G.cell = ad->cell0;
+                G.switches = 0;
+                G.window = ad->window, G.min_samples = ad->min_samples;
+            }
+        }
         t = 0;
         U = L = nW = nR = n_holes = spill_n = next = pf = completed = status = 0;
         lo_hole = INT32_MAX;
@@ -330,6 +367,17 @@ struct Sim {
 
     DEV void fail(int code) {
         if (status == 0) status = code;
+    }
+    // Entries the list keeps before spilling waiting ones. The adaptive build
+    // sizes the waiting window from the residents (max(M, residents) + 128,
+    // within lcap): its grid changes let residents outside the batch pile up,
+    // and a list padded with waiting entries costs every pass over it.
+    DEV int cap_now() const {
+        if constexpr (ADA) {
+            return min(lcap, max(M, nR) + 128);
+        } else {
+            return lcap;
+        }
     }
     // floor(s / div). Below 2^32 a multiply by the rounded-up reciprocal is
     // exact: s * ceil(2^64/div) / 2^64 exceeds s/div by less than 2^-32 <= 1/div.
@@ -483,12 +531,13 @@ struct Sim {
         lo_hole = INT32_MAX;
     }
 
-    // Keep at most lcap entries: drop holes, then spill the largest waiting
-    // entries to HBM.
+    // Keep at most cap_now() entries: drop holes, then spill the largest
+    // waiting entries to HBM.
     DEV void spill_excess() {
-        if (L <= lcap) return;
+        const int cap = cap_now();
+        if (L <= cap) return;
         drop_holes();
-        const int E = L - lcap;
+        const int E = L - cap;
         if (E <= 0) return;
         if (spill_n + E > scap) {
             fail(S_ECAPACITY);
@@ -524,7 +573,7 @@ struct Sim {
     }
 
     // Add K records (lanes [0, K)) to the list; waiting ones whose key exceeds
-    // the spill's minimum go straight to the spill. L <= lcap on entry.
+    // the spill's minimum go straight to the spill. L <= cap_now() on entry.
     DEV void add_entries(R y, int K) {
         if (spill_n > 0) {
             const bool toS = lane() < K && is_waiting(y.gs) && y.pk > spill_min;
@@ -544,7 +593,7 @@ struct Sim {
             }
         }
         if (K > 0) merge_new(y, K);
-        if (L > lcap) spill_excess();
+        if (L > cap_now()) spill_excess();
     }
 
     // The want-th smallest spilled key: radix select over 4-bit digits, the
@@ -588,7 +637,7 @@ struct Sim {
     // Bring the smallest spilled entries back on chip (as many as fit).
     DEV void refill() {
         drop_holes();
-        refill_into(lcap - L);
+        refill_into(cap_now() - L);
     }
 
     DEV void refill_into(int room) {
@@ -788,7 +837,8 @@ struct Sim {
             n_holes -= L0 - L;
             if (n_holes == 0) lo_hole = INT32_MAX;
         }
-        const int room = lcap + kStage - L;  // may use the overflow region
+        int room = cap_now() + kStage - L;  // may use the overflow region
+        if (room <= 0) room = lcap + kStage - L;
         if (room <= 0) {
             fail(S_ECAPACITY);
             return;
@@ -992,6 +1042,17 @@ struct Sim {
                 if (lohole == INT32_MAX) lohole = b + ffs0(fm);
                 nd += popc(fm);
                 if (vm_ok && lane() == (b >> 6)) vm_res &= ~fm, vm_ev &= ~fm;
+                if constexpr (ADA) {
+                    if (ad) {  // end-to-end latencies enter the window in batch order
+                        uint32_t lat = 0;
+                        if (fin) {
+                            const int64_t e2e = t_end - arr[idx_of(pk)];
+                            lat = e2e > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)e2e;
+                        }
+                        for (uint64_t m = fm; m; m &= m - 1)
+                            ada_push((uint32_t)rl((int)lat, ffs0(m)));
+                    }
+                }
             }
             if (bn < 0) break;
             b = bn, q = qn, pk = pkn, tl = tln;
@@ -1059,10 +1120,10 @@ struct Sim {
     }
 
     DEV void maintenance(int lo_mod) {
-        if (UNLIKELY(lo_mod < L || n_holes >= kHoleLimit || L > lcap)) {
+        if (UNLIKELY(lo_mod < L || n_holes >= kHoleLimit || L > cap_now())) {
             const int nx = compact_extract(min(min(lo_mod, lo_hole), L));
             if (nx > kStage) hbm_fence();
-            if (L > lcap) spill_excess();  // a refill during formation used the overflow region
+            if (L > cap_now()) spill_excess();  // a refill during formation used the overflow region
             if (nx > 0 && status == 0) {
                 add_entries(stage, min(nx, kStage));
                 for (int b = kStage; b < nx && status == 0; b += kStage) {
@@ -1074,6 +1135,142 @@ struct Sim {
             }
         }
         if (status == 0) take_arrivals();
+    }
+
+    // ---------------------------------------------------------- adaptive gamma
+
+    // Entries of the sorted window (n of them) below x.
+    DEV int window_below(uint32_t x, int n) const {
+        int c = 0;
+        for (int b = 0; b < n; b += kWave) {
+            const int r = b + lane();
+            c += popc(ballot(r < n && S.ws[r] < x));
+        }
+        return c;
+    }
+
+    // UpdateStats (Algorithm 1): the end-to-end latency x (wave-uniform) of a
+    // completed request enters the window; when it is full the oldest leaves.
+    // The ring keeps completion order, the sorted copy serves the percentiles.
+    DEV void ada_push(uint32_t x) {
+        AdaLds &G = *S.as;
+        int n = uni(G.wn);
+        const int W = uni(G.window), head = uni(G.whead);
+        if (n == W) {  // drop the oldest: close the gap at its first copy
+            const uint32_t old = (uint32_t)uni((int)S.wr[head]);
+            const int po = window_below(old, n);
+            for (int b = ((po + 1) >> 6) << 6; b < n; b += kWave) {
+                const int r = b + lane();
+                const bool mv = r > po && r < n;
+                uint32_t v = 0;
+                if (mv) v = S.ws[r];
+                wsync();
+                if (mv) S.ws[r - 1] = v;
+                wsync();
+            }
+            n--;
+        }
+        const int pn = window_below(x, n);  // open a slot at the insertion rank
+        for (int b = ((n - 1) >> 6) << 6; b >= 0 && b + kWave > pn; b -= kWave) {
+            const int r = b + lane();
+            const bool mv = r >= pn && r < n;
+            uint32_t v = 0;
+            if (mv) v = S.ws[r];
+            wsync();
+            if (mv) S.ws[r + 1] = v;
+            wsync();
+        }
+        if (lane() == 0) {
+            S.ws[pn] = x;
+            S.wr[head] = x;
+            G.whead = head + 1 == W ? 0 : head + 1;
+            G.wn = n + 1;
+            G.wnew = 1;
+        }
+        wsync();
+    }
+
+    // UpdateGamma (Phase 4, Algorithm 2), before the keys of every iteration:
+    // with at least min_samples latencies in the window, gamma_hat =
+    // tau ln 5 / max(t99 - t95, eps) from the nearest-rank t95, t99 (only
+    // recomputed when the window changed), then gamma = clip((1 - beta) gamma
+    // + beta gamma_hat); each is one rounded double operation (no contraction).
+    // A new grid cell re-keys every waiting and resident request.
+    DEV void ada_update() {
+#pragma clang fp contract(off)
+        AdaLds &G = *S.as;
+        const int wn = uni(G.wn);
+        if (wn < uni(G.min_samples)) return;
+        double gh = G.ghat;
+        if (uni(G.wnew)) {
+            const int r95 = (95 * wn + 99) / 100, r99 = (99 * wn + 99) / 100;
+            const uint32_t t95 = S.ws[r95 - 1], t99 = S.ws[r99 - 1];
+            double d = (double)(t99 - t95);
+            if (d < ad->eps) d = ad->eps;
+            gh = ad->num / d;
+        }
+        double g = (1.0 - ad->beta) * G.gamma + ad->beta * gh;
+        if (g < ad->gmin) g = ad->gmin;
+        if (g > ad->gmax) g = ad->gmax;
+        const int cell = popc(ballot(g >= bnd));
+        const int old = uni(G.cell);
+        wsync();
+        if (lane() == 0) {
+            G.ghat = gh, G.wnew = 0;
+            G.gamma = g;
+            if (cell != old) G.cell = cell, G.switches++;
+        }
+        wsync();
+        if (cell != old) ada_rekey(cell);
+    }
+
+    // The boost table changes to that of `cell`: keys a - bt[level] of the
+    // spilled, waiting and resident entries shift by bt_old - bt_new of their
+    // level; every on-chip entry is then re-inserted, so waiting entries above
+    // the new spill minimum move to the spill and the list is sorted again.
+    DEV void ada_rekey(int cell) {
+        const int64_t *nt = ad->table[cell];
+        hbm_fence();
+        uint64_t mn = ~0ull;
+        for (int b = 0; b < spill_n; b += kWave) {
+            const int i = b + lane();
+            if (i < spill_n) {
+                const uint64_t pk = spill[i].pk;
+                const int lv = min((int)((spill[i].gs >> G_LVL_SHIFT) & 31u), kLevels - 1);
+                const uint64_t pk2 = pack(key_of(pk) + S.bt[lv] - nt[lv], idx_of(pk));
+                spill[i].pk = pk2;
+                mn = pk2 < mn ? pk2 : mn;
+            }
+        }
+        spill_min = wminu(mn);
+        for (int b = 0; b < L; b += kWave) {
+            const int r = b + lane();
+            if (r < L) {
+                const uint32_t g = S.q[r].x;
+                if (!(g & G_DONE)) {
+                    const int lv = min((int)((g >> G_LVL_SHIFT) & 31u), kLevels - 1);
+                    const uint64_t pk = S.k[r];
+                    S.k[r] = pack(key_of(pk) + S.bt[lv] - nt[lv], idx_of(pk));
+                    S.q[r].x = g | G_DIRTY;
+                }
+            }
+        }
+        int64_t v = 0;
+        if (lane() < kLevels) v = nt[lane()];
+        wsync();
+        if (lane() < kLevels) S.bt[lane()] = v;
+        wsync();
+        const int nx = compact_extract(0);  // every live entry is flagged
+        if (nx > kStage) hbm_fence();
+        if (nx > 0 && status == 0) {
+            add_entries(stage, min(nx, kStage));
+            for (int b = kStage; b < nx && status == 0; b += kStage) {
+                const int kb = min(nx - b, kStage);
+                R x;
+                if (lane() < kb) x = from_rec(ovf[b - kStage + lane()]);
+                add_entries(x, kb);
+            }
+        }
     }
 
     // ---------------------------------------------------------- driver
@@ -1106,6 +1303,12 @@ struct Sim {
                 t = an;
                 take_arrivals();
                 continue;
+            }
+            if constexpr (ADA) {
+                if (ad) {
+                    ada_update();
+                    if (status) break;
+                }
             }
             formation();
             if (status) break;
@@ -1154,25 +1357,32 @@ struct Sim {
             int64_t *cn = A.counters + (size_t)inst * 8;
             cn[0] = iters, cn[1] = reqiters, cn[2] = tokens, cn[3] = ev_vol;
             cn[4] = ev_forced, cn[5] = t, cn[6] = maxU, cn[7] = idle;
+            if constexpr (ADA) {  // (zero from tas_create for the other build)
+                A.gamma_out[inst] = ad ? S.as->gamma : 0.0;
+                A.switch_out[inst] = ad ? S.as->switches : 0;
+            }
             A.status[inst] = status;
         }
     }
 };
 
-template <int BSH>
+template <int BSH, bool ADA>
 DEV void run_instance(const SimArgs &a, const DevSetting &st, int inst, unsigned char *smem) {
-    Sim<BSH> s(a, st, inst, smem);
+    Sim<BSH, ADA> s(a, st, inst, smem);
     s.run();
 }
 
+// ADA: the build with adaptive gamma, launched when some instance uses it
+// (its extra state costs the fixed-gamma path registers).
+template <bool ADA>
 __global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int inst = blockIdx.x;
     if (inst >= a.n_inst) return;
     if (a.retry && a.status[inst] != S_ECAPACITY) return;
     const DevSetting &st = a.inst[inst];
-    if (a.bs == 16) run_instance<4>(a, st, inst, smem);
-    else run_instance<-1>(a, st, inst, smem);
+    if (a.bs == 16) run_instance<4, ADA>(a, st, inst, smem);
+    else run_instance<-1, ADA>(a, st, inst, smem);
 }
 
 }  // namespace
@@ -1181,13 +1391,18 @@ __global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
 int tas_launch_sim(const tas::SimArgs &a, int64_t lds_bytes, void *stream) {
     if (a.n_inst <= 0) return 0;
     hipStream_t s = (hipStream_t)stream;
+    const void *fn = a.ada_window > 0 ? (const void *)tas::sim_kernel<true>
+                                      : (const void *)tas::sim_kernel<false>;
     if (lds_bytes > 65536) {
-        if (hipFuncSetAttribute((const void *)tas::sim_kernel,
-                                hipFuncAttributeMaxDynamicSharedMemorySize,
+        if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)lds_bytes) != hipSuccess)
             return -4;
     }
-    hipLaunchKernelGGL(tas::sim_kernel, dim3((unsigned)a.n_inst), dim3(64), (size_t)lds_bytes, s,
-                       a);
+    if (a.ada_window > 0)
+        hipLaunchKernelGGL(tas::sim_kernel<true>, dim3((unsigned)a.n_inst), dim3(64),
+                           (size_t)lds_bytes, s, a);
+    else
+        hipLaunchKernelGGL(tas::sim_kernel<false>, dim3((unsigned)a.n_inst), dim3(64),
+                           (size_t)lds_bytes, s, a);
     return hipGetLastError() == hipSuccess ? 0 : -4;
 }

@@ -62,8 +62,9 @@ class tas_params(ctypes.Structure):
 assert ctypes.sizeof(tas_setting) == W.SETTING_DTYPE.itemsize == 280
 
 EXPORTS = ["tas_workspace_bytes", "tas_create", "tas_run", "tas_percentiles", "tas_latencies",
-           "tas_counters", "tas_status", "tas_instance_status", "tas_destroy", "tas_strerror",
-           "tas_boost_table", "tas_instance_table", "tas_list_cap"]
+           "tas_counters", "tas_gamma", "tas_status", "tas_instance_status", "tas_destroy",
+           "tas_strerror", "tas_boost_table", "tas_ada_grid", "tas_instance_table",
+           "tas_list_cap"]
 
 _lib = None
 
@@ -81,13 +82,15 @@ def lib():
         L.tas_workspace_bytes.restype = ctypes.c_size_t
         L.tas_create.argtypes = [P, P, P, ctypes.c_size_t, ctypes.POINTER(P)]
         for name in ("tas_create", "tas_run", "tas_percentiles", "tas_latencies", "tas_counters",
-                     "tas_status", "tas_instance_status", "tas_boost_table",
-                     "tas_instance_table"):
+                     "tas_gamma", "tas_status", "tas_instance_status", "tas_boost_table",
+                     "tas_ada_grid", "tas_instance_table"):
             getattr(L, name).restype = ctypes.c_int
         L.tas_run.argtypes = [P, P]
         L.tas_percentiles.argtypes = [P, P, P]
         L.tas_latencies.argtypes = [P, P, P, P, P]
         L.tas_counters.argtypes = [P, P, P]
+        L.tas_gamma.argtypes = [P, P, P, P]
+        L.tas_ada_grid.argtypes = [P, f64, P, P, P]
         L.tas_status.argtypes = [P]
         L.tas_instance_status.argtypes = [P, P, P]
         L.tas_destroy.argtypes = [P]
@@ -183,6 +186,23 @@ def tas_counters(ctx, out, stream=None):
     _check(lib().tas_counters(ctx, _ptr(out), _stream(stream)), "tas_counters")
 
 
+def tas_gamma(ctx, gamma=None, switches=None, stream=None):
+    _check(lib().tas_gamma(ctx, _ptr(gamma), _ptr(switches), _stream(stream)), "tas_gamma")
+
+
+def tas_ada_grid(setting, tau_us: float = 5000.0):
+    """(grid [G], midpoints [G-1], tables [G, 24]) of an adaptive setting record."""
+    rec = np.ascontiguousarray(np.asarray(setting, W.SETTING_DTYPE).reshape(1))
+    G = int(rec[0]["ada_grid"])
+    if not 2 <= G <= 64:
+        raise TasError(TAS_EINVAL, "tas_ada_grid")
+    grid, bound = np.zeros(G, np.float64), np.zeros(max(G - 1, 1), np.float64)
+    tabs = np.zeros((G, LEVELS), np.int64)
+    _check(lib().tas_ada_grid(rec.ctypes.data, float(tau_us), grid.ctypes.data,
+                              bound.ctypes.data, tabs.ctypes.data), "tas_ada_grid")
+    return grid, bound[:G - 1], tabs
+
+
 def tas_instance_status(ctx, out, stream=None):
     _check(lib().tas_instance_status(ctx, _ptr(out), _stream(stream)), "tas_instance_status")
 
@@ -234,6 +254,8 @@ class Simulation:
         n, m = w.n_inst, w.n_req
         self.pct = torch.zeros((n, 3, 3), dtype=torch.int32, device=device)
         self.counters = torch.zeros((n, 8), dtype=torch.int64, device=device)
+        self.gamma_buf = torch.zeros(n, dtype=torch.float64, device=device)
+        self.switch_buf = torch.zeros(n, dtype=torch.int64, device=device)
         self.status_buf = torch.zeros(n, dtype=torch.int32, device=device)
         self.m = m
 
@@ -260,9 +282,12 @@ class Simulation:
             for key, t in zip(("ttft", "ttlt", "tbtmax"), lat):
                 out[key] = t.cpu().numpy().view(np.uint32)
         tas_counters(self.ctx, self.counters)
+        tas_gamma(self.ctx, self.gamma_buf, self.switch_buf)
         tas_instance_status(self.ctx, self.status_buf)
         out["rc"] = tas_status(self.ctx)
         out["counters"] = self.counters.cpu().numpy()
+        out["gamma"] = self.gamma_buf.cpu().numpy()
+        out["switches"] = self.switch_buf.cpu().numpy()
         out["status"] = self.status_buf.cpu().numpy()
         out["pct"] = self.pct.cpu().numpy().view(np.uint32)
         return out

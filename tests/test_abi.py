@@ -26,7 +26,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = tas.lib()
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 15
     for n in names:
         assert hasattr(lib, n), n
     assert set(tas.EXPORTS) <= set(names)
@@ -65,6 +65,62 @@ def test_boost_table_matches_oracle(k):
     for g in np.concatenate([np.geomspace(1e-6, 2.0, 60), 10.0 ** np.linspace(-5, -1, 31)]):
         for tau in (5000.0, 1234.5):
             assert np.array_equal(tas.tas_boost_table(g, k, tau), oracle.boost_table(g, k, tau))
+
+
+@pytest.mark.parametrize("k", [1, 16, 256])
+def test_ada_grid_matches_oracle(k):
+    """The adaptive-gamma grid, midpoints and tables agree bit for bit with the
+    oracle's own construction."""
+    for ada in (dict(W.ADA), dict(W.ADA, grid=2, gamma_min=2e-3, gamma_max=10.0),
+                dict(W.ADA, grid=64, gamma_min=1e-6, gamma_max=3.0)):
+        for tau in (5000.0, 777.25):
+            s = W.setting(0, W.BOOST, k=k, gamma=ada["gamma_min"], ada=ada)
+            g1, b1, t1 = tas.tas_ada_grid(s, tau)
+            g2, b2, t2 = oracle.ada_grid(s, tau)
+            assert np.array_equal(g1, g2) and np.array_equal(b1, b2) and np.array_equal(t1, t2)
+
+
+def test_ada_settings_rejected():
+    w = small()
+    good = dict(W.ADA)
+    bad = [dict(good, beta=1.5), dict(good, beta=-0.1), dict(good, window=0),
+           dict(good, window=4096), dict(good, min_samples=300), dict(good, grid=1),
+           dict(good, grid=65), dict(good, gamma_min=0.0), dict(good, gamma_max=1e-6),
+           dict(good, eps_us=0.0), dict(good, eps_us=float("inf"))]
+    for b in bad:
+        s = w.settings.copy()
+        s[2] = W.setting(int(s[2]["trace"]), W.BOOST, k=256, memguard=1, gamma=1e-3, ada=b)
+        assert create_rc(w, settings=s)[0] == tas.TAS_EINVAL, b
+        with pytest.raises(tas.TasError):
+            tas.tas_ada_grid(s[2])
+    s = w.settings.copy()
+    s[2] = W.setting(int(s[2]["trace"]), W.BOOST, gamma=0.5, ada=good)  # gamma0 > gamma_max
+    assert create_rc(w, settings=s)[0] == tas.TAS_EINVAL
+    s = w.settings.copy()
+    s[0]["ada"] = 1  # FCFS
+    for f, v in good.items():
+        s[0]["ada_" + f] = v
+    assert create_rc(w, settings=s)[0] == tas.TAS_EINVAL
+    s = w.settings.copy()
+    s[2] = W.setting(int(s[2]["trace"]), W.BOOST, gamma=1e-3, ada=good,
+                     table=np.arange(24)[::-1])  # explicit table and adaptive gamma
+    assert create_rc(w, settings=s)[0] == tas.TAS_EINVAL
+    s = w.settings.copy()
+    s[2] = W.setting(int(s[2]["trace"]), W.BOOST, gamma=1e-3, ada=good)
+    s[2]["ada"] = 2
+    assert create_rc(w, settings=s)[0] == tas.TAS_EINVAL
+
+
+def test_ada_window_fits_lds():
+    """The largest window still leaves room for the default list."""
+    w = small()
+    s = w.settings.copy()
+    s[2] = W.setting(int(s[2]["trace"]), W.BOOST, gamma=1e-3, ada=dict(W.ADA, window=2048))
+    t, _ = tas.make_traces(w.arrival_us, w.prompt, w.decode)
+    p, _ = tas.make_params(w.engine, s)
+    p0, _ = tas.make_params(w.engine, w.settings)
+    extra = tas.tas_workspace_bytes(t, p) - tas.tas_workspace_bytes(t, p0)
+    assert extra > 0  # the adaptive block, the gamma and switch outputs
 
 
 def test_boost_table_rejects():
