@@ -147,7 +147,7 @@ typedef struct {
     double tau_us;         /* microseconds per token of boost, > 0             */
     int32_t list_cap;      /* on-chip candidate entries per instance, in
                               [max_seqs + 64, 4032]; 0 picks max_seqs + 128,
-                              or max_seqs + 512 when some instance adapts
+                              or max_seqs + 768 when some instance adapts
                               gamma, rounded up to 64                          */
     int32_t spill_cap;     /* waiting entries per instance kept in HBM beyond
                               the on-chip list; 0 = n_req                      */

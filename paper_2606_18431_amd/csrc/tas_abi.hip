@@ -54,10 +54,12 @@ int32_t ada_count(const tas_params *p, int32_t *wmax) {
 // that hold more residents than that rerun in a second pass with a large list.
 // With adaptive gamma every grid change reorders the queue; requests admitted
 // under the old order keep their KV until the budget binds, so residents
-// outside the batch accumulate (to about 2.8 max_seqs on the large sweep):
-// launches with adaptive instances start with 384 more entries.
+// outside the batch accumulate (beyond 3 max_seqs on the large sweep):
+// launches with adaptive instances start with 640 more entries, so that a
+// rerun is rare (the adaptive build keeps only residents + 128 on chip, so
+// the larger list costs occupancy, not longer passes).
 int32_t default_list_cap(int32_t max_seqs, bool adaptive) {
-    int64_t lc = (int64_t)max_seqs + (adaptive ? 512 : 128);
+    int64_t lc = (int64_t)max_seqs + (adaptive ? 768 : 128);
     lc = (lc + 63) / 64 * 64;
     return (int32_t)std::min<int64_t>(lc, tas::kMaxListCap);
 }
