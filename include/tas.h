@@ -127,7 +127,9 @@ typedef struct {
     int32_t ada_min_samples; /* window size before the first update, in
                                 [1, ada_window]                                */
     int32_t ada_grid;      /* grid points G, in [2, TAS_ADA_GRID_MAX]          */
-    int32_t ada_reserved;  /* 0                                                */
+    int32_t signal;        /* BOOST: 0 = P + dec; 1 = the phase-aware signal of
+                              Algorithm 2 (P in prefill, dec in decode); 0
+                              for every other policy                          */
 } tas_setting;
 
 #define TAS_ADA_WINDOW_MAX 2048

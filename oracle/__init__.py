@@ -50,10 +50,10 @@ def lib():
         L.tas_oracle_boost_table.argtypes = [f64, i32, f64, P]
         L.tas_oracle_boost_table.restype = ctypes.c_int
         L.tas_oracle_run.argtypes = [i32, i32, P, P, P, i32, P, P, P, P, P, P, P, i64,
-                                     P, P, P, P, P, P, P, P, P, i32]
+                                     P, P, P, P, P, P, P, P, P, P, i32]
         L.tas_oracle_run.restype = ctypes.c_int
-        L.tas_oracle_log.argtypes = [i32, P, P, P, i32, i32, i32, i64, P, P, P, i64, P, P, P,
-                                     P, P, i64, P, i64, P, i64, P, P, P]
+        L.tas_oracle_log.argtypes = [i32, P, P, P, i32, i32, i32, i64, P, P, i32, P, i64, P,
+                                     P, P, P, P, i64, P, i64, P, i64, P, P, P]
         L.tas_oracle_ada_grid.argtypes = [P, i32, P, P, P]
         L.tas_oracle_ada_grid.restype = ctypes.c_int
         L.tas_oracle_log.restype = ctypes.c_int
@@ -83,7 +83,7 @@ def tables(settings: np.ndarray, tau_us: float) -> np.ndarray:
     where one is given, else the table of gamma; zeros for FCFS/SRPT."""
     out = np.zeros((len(settings), LEVELS), np.int64)
     for i, s in enumerate(settings):
-        if int(s["policy"]) != 2:
+        if int(s["policy"]) not in (2, 7):  # the boost policies
             continue
         if int(s["table_given"]):
             out[i] = s["boost_us"]
@@ -142,6 +142,7 @@ def run(w, n_threads: int | None = None, max_iters: int | None = None):
     tb = np.ascontiguousarray(tables(s, w.engine.tau_us))
     ada = np.ascontiguousarray(np.stack([ada_params(x, w.engine.tau_us) for x in s])
                                if n_inst else np.zeros((0, 10)), np.float64)
+    sg = np.ascontiguousarray(s["signal"], np.int32)
     out = dict(
         ttft=np.zeros((n_inst, n_req), np.uint32),
         ttlt=np.zeros((n_inst, n_req), np.uint32),
@@ -158,13 +159,13 @@ def run(w, n_threads: int | None = None, max_iters: int | None = None):
                               _p(po), _p(kk), _p(mg), _p(dl), _p(tb), _p(_eng(w.engine)),
                               int(mi), _p(out["ttft"]), _p(out["ttlt"]), _p(out["tbtmax"]),
                               _p(out["counters"]), _p(out["pct"]), _p(out["status"]), _p(ada),
-                              _p(out["gamma"]), _p(out["switches"]), int(nt))
+                              _p(sg), _p(out["gamma"]), _p(out["switches"]), int(nt))
     out["rc"] = rc
     return out
 
 
 def log(arrival, prompt, decode, engine, policy, k=1, memguard=0, delta_us=0, table=None,
-        gamma=None, ada=None, max_iters=None, cap_iter=1 << 20, cap_batch=1 << 22,
+        gamma=None, ada=None, signal=0, max_iters=None, cap_iter=1 << 20, cap_batch=1 << 22,
         cap_evict=1 << 20):
     """Run one instance and return its schedule log (see tas_oracle.h). ``ada``:
     adaptive-gamma parameters as in workloads.ADA (gamma is the start)."""
@@ -185,11 +186,12 @@ def log(arrival, prompt, decode, engine, policy, k=1, memguard=0, delta_us=0, ta
              tbtmax=np.zeros(n, np.uint32), counters=np.zeros(8, np.int64))
     it = np.zeros((cap_iter, 8), np.int64)
     bt = np.zeros((cap_batch, 2), np.int32)
-    ev = np.zeros((cap_evict, 3), np.int64)
+    ev = np.zeros((cap_evict, 4), np.int64)
     ni, nb, ne = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     mi = engine.max_iters if max_iters is None else max_iters
     rc = lib().tas_oracle_log(n, _p(arrival), _p(prompt), _p(decode), policy, k, memguard,
-                              int(delta_us), _p(table), _p(prm), _p(_eng(engine)), int(mi),
+                              int(delta_us), _p(table), _p(prm), int(signal),
+                              _p(_eng(engine)), int(mi),
                               _p(o["ttft"]), _p(o["ttlt"]), _p(o["tbtmax"]), _p(o["counters"]),
                               _p(it), cap_iter, _p(bt), cap_batch, _p(ev), cap_evict,
                               ctypes.byref(ni), ctypes.byref(nb), ctypes.byref(ne))

@@ -52,6 +52,18 @@
  *         resident that has emitted at least 0.6 D tokens is never a voluntary
  *         victim (5 dec >= 3 D)
  *
+ * Phase ladder (paper: Phase 1 DistBoost; Algorithm 2 Signal):
+ *   DIST  DistBoost: two queues. A request in its prefill (no token emitted
+ *         yet) has the prefill priority a - b(P) (the boost table at the level
+ *         of its prompt); once it has emitted its first token it is in the
+ *         decode queue, ordered by the time it entered it (its first-token
+ *         time), and every decode-queue request ranks before every prefill-
+ *         queue request: the decode batch first, prefill chunks fill the rest.
+ *         Key = t_first - 2^42 in decode, below every prefill key.
+ *   signal 1 (BOOST): the phase-aware signal of Algorithm 2: the prompt length
+ *         while in prefill, the decode tokens emitted after it (the level,
+ *         the key and MemGuard's guard all use it)
+ *
  * Adaptive gamma (Phase 4, gamma-Ada), for BOOST instances that ask for it:
  *   - the window holds the end-to-end latencies (TTLT, us, capped at 2^32-1)
  *     of the last W completed requests; requests that complete in the same
@@ -76,7 +88,9 @@
 #include <string.h>
 
 enum { PENDING = 0, WAITING = 1, RESIDENT = 2, DONE = 3 };
-enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2, P_SPF = 3, P_SJF = 4, P_LAS = 5, P_TRAIL = 6 };
+enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2, P_SPF = 3, P_SJF = 4, P_LAS = 5, P_TRAIL = 6,
+       P_DIST = 7 };
+#define DECODE_QUEUE_OFFSET ((int64_t)1 << 42) /* decode-queue keys lie below every prefill key */
 
 #define ADA_GRID_MAX 64
 #define ADA_WINDOW_MAX 2048
@@ -99,6 +113,7 @@ typedef struct {
     int32_t M, T, c, Kb, bs, base, tok, div;
     int64_t max_iters;
     const ada_t *ada; /* NULL: gamma fixed */
+    int32_t signal;   /* BOOST: 0 = P + dec, 1 = Algorithm 2's phase-aware signal */
 } inst_t;
 
 typedef struct {
@@ -161,6 +176,13 @@ static int32_t level_of(int64_t w, int32_t k) {
 
 int32_t tas_oracle_level(int64_t w, int32_t k) { return level_of(w, k); }
 
+/* The boost signal of request r: P + dec, or (signal 1) P during the prefill
+ * and the decode tokens emitted after it. */
+static int64_t signal_of(const inst_t *I, int32_t r, const req_t *q) {
+    if (I->signal == 1) return q->dec == 0 ? I->P[r] : q->dec;
+    return (int64_t)I->P[r] + q->dec;
+}
+
 static int64_t key_of(const inst_t *I, int32_t r, const req_t *q) {
     switch (I->policy) {
     case P_FCFS:
@@ -174,8 +196,11 @@ static int64_t key_of(const inst_t *I, int32_t r, const req_t *q) {
         return I->D[r];
     case P_LAS:
         return (int64_t)I->P[r] + q->dec;
+    case P_DIST:
+        if (q->dec > 0) return q->t_first - DECODE_QUEUE_OFFSET; /* decode queue */
+        return I->a[r] - I->bt[level_of(I->P[r], I->k)];         /* prefill queue */
     default:
-        return I->a[r] - I->bt[level_of((int64_t)I->P[r] + q->dec, I->k)];
+        return I->a[r] - I->bt[level_of(signal_of(I, r, q), I->k)];
     }
 }
 
@@ -342,7 +367,7 @@ static int simulate(const inst_t *I0, uint32_t *ttft, uint32_t *ttlt, uint32_t *
                 if (U + dU <= I->Kb) {
                     if (q->st == WAITING) { /* dispatch */
                         q->st = RESIDENT;
-                        q->guard = level_of((int64_t)I->P[r] + q->dec, I->k);
+                        q->guard = level_of(signal_of(I, r, q), I->k);
                     }
                     q->in_batch = 1;
                     bidx[nb] = r;
@@ -358,8 +383,7 @@ static int simulate(const inst_t *I0, uint32_t *ttft, uint32_t *ttlt, uint32_t *
                     int32_t x = act[m];
                     const req_t *p = &R[x];
                     if (x == r || p->st != RESIDENT || p->in_batch) continue;
-                    if (I->memguard &&
-                        !(level_of((int64_t)I->P[x] + p->dec, I->k) > p->guard))
+                    if (I->memguard && !(level_of(signal_of(I, x, p), I->k) > p->guard))
                         continue;
                     if (I->policy == P_TRAIL && 5 * (int64_t)p->dec >= 3 * (int64_t)I->D[x])
                         continue; /* past the swap-prevention threshold */
@@ -370,8 +394,8 @@ static int simulate(const inst_t *I0, uint32_t *ttft, uint32_t *ttlt, uint32_t *
                     evict(&R[v], &U, I->bs, iters);
                     ev_vol++;
                     if (lg && lg->n_ev < lg->ev_cap) {
-                        int64_t *e = lg->ev + 3 * lg->n_ev++;
-                        e[0] = iters, e[1] = v, e[2] = 0;
+                        int64_t *e = lg->ev + 4 * lg->n_ev++;
+                        e[0] = iters, e[1] = v, e[2] = 0, e[3] = r;
                     } else if (lg)
                         lg->full = 1;
                     continue;
@@ -389,8 +413,8 @@ static int simulate(const inst_t *I0, uint32_t *ttft, uint32_t *ttlt, uint32_t *
                     evict(&R[v], &U, I->bs, iters);
                     ev_forced++;
                     if (lg && lg->n_ev < lg->ev_cap) {
-                        int64_t *e = lg->ev + 3 * lg->n_ev++;
-                        e[0] = iters, e[1] = v, e[2] = 1;
+                        int64_t *e = lg->ev + 4 * lg->n_ev++;
+                        e[0] = iters, e[1] = v, e[2] = 1, e[3] = r;
                     } else if (lg)
                         lg->full = 1;
                     if (self) break;
@@ -538,6 +562,7 @@ typedef struct {
     int64_t *counters;
     int32_t *status;
     const double *ada; /* [n_inst*10] or NULL */
+    const int32_t *signal; /* [n_inst] or NULL */
     double *gamma_out;
     int64_t *switch_out;
     int32_t next; /* work counter */
@@ -552,6 +577,7 @@ static void fill_inst(inst_t *I, const int32_t *eng, int32_t n_req, const int64_
     I->base = eng[5], I->tok = eng[6], I->div = eng[7];
     I->max_iters = max_iters;
     I->ada = NULL;
+    I->signal = 0;
 }
 
 static void run_one(job_t *J, int32_t i) {
@@ -564,6 +590,7 @@ static void run_one(job_t *J, int32_t i) {
     size_t o = (size_t)i * (size_t)J->n_req;
     ada_t *A = NULL;
     int st = 0;
+    if (J->signal) I.signal = J->signal[i];
     if (J->ada && J->ada[(size_t)i * 10] != 0.0) {
         A = (ada_t *)malloc(sizeof *A);
         st = A ? ada_setup(A, J->ada + (size_t)i * 10, J->policy[i], J->k[i]) : TOR_EINVAL;
@@ -600,18 +627,24 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
                    const int32_t *memguard, const int64_t *delta, const int64_t *table,
                    const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
                    uint32_t *tbtmax, int64_t *counters, uint32_t *pct, int32_t *status,
-                   const double *ada, double *gamma_out, int64_t *switch_out,
-                   int32_t n_threads) {
+                   const double *ada, const int32_t *signal, double *gamma_out,
+                   int64_t *switch_out, int32_t n_threads) {
     if (n_traces < 1 || n_req < 1 || n_inst < 0) return TOR_EINVAL;
-    for (int32_t i = 0; i < n_inst; i++)
-        if (trace[i] < 0 || trace[i] >= n_traces || policy[i] < 0 || policy[i] > 6 || k[i] < 1)
+    for (int32_t i = 0; i < n_inst; i++) {
+        if (trace[i] < 0 || trace[i] >= n_traces || policy[i] < 0 || policy[i] > 7 || k[i] < 1)
             return TOR_EINVAL;
+        if (signal && signal[i] != 0 && (signal[i] != 1 || policy[i] != P_BOOST))
+            return TOR_EINVAL;
+    }
     if (eng[0] < 1 || eng[1] < 1 || eng[2] < 1 || eng[2] > eng[1] || eng[3] < 1 || eng[4] < 1 ||
         eng[5] < 1 || eng[6] < 0 || eng[7] < 1)
         return TOR_EINVAL;
-    job_t J = {n_req,    n_inst, arrival, prompt, decode,    trace,      policy,
-               k,        memguard, delta, table,  eng,    max_iters, ttft,       ttlt,
-               tbtmax,   pct,    counters, status, ada,    gamma_out, switch_out, 0};
+    job_t J = {.n_req = n_req, .n_inst = n_inst, .arrival = arrival, .prompt = prompt,
+               .decode = decode, .trace = trace, .policy = policy, .k = k,
+               .memguard = memguard, .delta = delta, .table = table, .eng = eng,
+               .max_iters = max_iters, .ttft = ttft, .ttlt = ttlt, .tbtmax = tbtmax,
+               .pct = pct, .counters = counters, .status = status, .ada = ada,
+               .signal = signal, .gamma_out = gamma_out, .switch_out = switch_out, .next = 0};
     if (n_threads < 1) n_threads = 1;
     if (n_threads > n_inst) n_threads = n_inst > 0 ? n_inst : 1;
     pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)n_threads);
@@ -629,14 +662,17 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
 
 int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
                    const int32_t *decode, int32_t policy, int32_t k, int32_t memguard,
-                   int64_t delta, const int64_t *table, const double *ada, const int32_t *eng,
-                   int64_t max_iters, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
-                   int64_t *counters, int64_t *log_iter, int64_t iter_cap,
+                   int64_t delta, const int64_t *table, const double *ada, int32_t signal,
+                   const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
+                   uint32_t *tbtmax, int64_t *counters, int64_t *log_iter, int64_t iter_cap,
                    int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
                    int64_t evict_cap, int64_t *n_iter, int64_t *n_batch, int64_t *n_evict) {
+    if (policy < 0 || policy > 7 || (signal != 0 && (signal != 1 || policy != P_BOOST)))
+        return TOR_EINVAL;
     inst_t I;
     fill_inst(&I, eng, n_req, arrival, prompt, decode, policy, k, memguard, delta, table,
               max_iters);
+    I.signal = signal;
     ada_t *A = NULL;
     if (ada && ada[0] != 0.0) {
         A = (ada_t *)malloc(sizeof *A);

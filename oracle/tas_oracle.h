@@ -16,7 +16,7 @@
  *   arrival [n_traces*n_req] int64 us, non-decreasing within a trace
  *   prompt, decode [n_traces*n_req] int32 tokens, >= 1
  *   per instance i: trace[i], policy[i] (0 FCFS, 1 SRPT, 2 BOOST, 3 SPF,
- *   4 SJF, 5 LAS, 6 TRAIL), k[i] >= 1,
+ *   4 SJF, 5 LAS, 6 TRAIL, 7 DIST), k[i] >= 1,
  *   memguard[i] in {0,1}, delta[i] >= 0 us, table[i*24 .. i*24+23] int64 us
  *   eng[8] = {max_seqs, max_tokens, chunk, kv_blocks, block_tokens,
  *             iter_base_us, iter_tok_us, iter_ctx_div}
@@ -36,6 +36,10 @@
  * to the current gamma (see tas_oracle.c). Outputs gamma_out [n_inst] (final
  * gamma, 0 when not adaptive) and switch_out [n_inst] (grid-cell changes) may
  * be NULL.
+ *
+ * signal [n_inst] (NULL: all 0): the boost signal of a BOOST instance, 0 =
+ * prompt plus emitted tokens, 1 = Algorithm 2's phase-aware signal (prompt
+ * length in prefill, emitted tokens in decode).
  */
 #ifndef TAS_ORACLE_H
 #define TAS_ORACLE_H
@@ -65,8 +69,8 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
                    const int32_t *memguard, const int64_t *delta, const int64_t *table,
                    const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
                    uint32_t *tbtmax, int64_t *counters, uint32_t *pct, int32_t *status,
-                   const double *ada, double *gamma_out, int64_t *switch_out,
-                   int32_t n_threads);
+                   const double *ada, const int32_t *signal, double *gamma_out,
+                   int64_t *switch_out, int32_t n_threads);
 
 /* Run ONE instance and record its schedule, for invariant checks.
  * log_iter[it*8 + {0..7}] = {t_start, dt, batch size, KV blocks in use
@@ -74,14 +78,15 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
  *   cell of the boost table used (-1 when gamma is fixed), the bits of gamma
  *   (IEEE double)}; ada: 10 parameters as above, or NULL;
  * log_batch[...] = (request index, tokens) pairs, iteration after iteration;
- * log_evict[...] = (iteration, request index, forced flag) triples.
+ * log_evict[...] = (iteration, evicted request, forced flag, the candidate
+ *   whose admission caused it) records of 4.
  * Capacities are in records. *n_iter, *n_batch, *n_evict receive the counts.
  * Returns the instance status, or TOR_EINVAL if a log buffer is too small. */
 int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
                    const int32_t *decode, int32_t policy, int32_t k, int32_t memguard,
-                   int64_t delta, const int64_t *table, const double *ada, const int32_t *eng,
-                   int64_t max_iters, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
-                   int64_t *counters, int64_t *log_iter, int64_t iter_cap,
+                   int64_t delta, const int64_t *table, const double *ada, int32_t signal,
+                   const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
+                   uint32_t *tbtmax, int64_t *counters, int64_t *log_iter, int64_t iter_cap,
                    int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
                    int64_t evict_cap, int64_t *n_iter, int64_t *n_batch, int64_t *n_evict);
 

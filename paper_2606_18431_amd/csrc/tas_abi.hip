@@ -140,6 +140,7 @@ bool ada_ok(const tas_setting &s) {
 int check_setting(const tas_setting &s, int32_t n_traces) {
     if (s.trace < 0 || s.trace >= n_traces) return TAS_EINVAL;
     if (s.ada != 0 && (s.ada != 1 || !ada_ok(s))) return TAS_EINVAL;
+    if (s.signal != 0) return TAS_EINVAL;  // the phase-aware signal: not built yet
     if (s.policy < TAS_FCFS || s.policy > TAS_TRAIL) return TAS_EINVAL;
     if (s.delta_us < 0) return TAS_EINVAL;
     if (s.policy != TAS_BOOST) {

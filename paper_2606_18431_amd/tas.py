@@ -45,7 +45,7 @@ class tas_setting(ctypes.Structure):
                 ("ada_beta", ctypes.c_double), ("ada_gamma_min", ctypes.c_double),
                 ("ada_gamma_max", ctypes.c_double), ("ada_eps_us", ctypes.c_double),
                 ("ada_window", ctypes.c_int32), ("ada_min_samples", ctypes.c_int32),
-                ("ada_grid", ctypes.c_int32), ("ada_reserved", ctypes.c_int32)]
+                ("ada_grid", ctypes.c_int32), ("signal", ctypes.c_int32)]
 
 
 class tas_params(ctypes.Structure):

@@ -31,9 +31,9 @@ import math
 
 import numpy as np
 
-FCFS, SRPT, BOOST, SPF, SJF, LAS, TRAIL = 0, 1, 2, 3, 4, 5, 6
+FCFS, SRPT, BOOST, SPF, SJF, LAS, TRAIL, DIST = 0, 1, 2, 3, 4, 5, 6, 7
 POLICY_NAMES = {FCFS: "fcfs", SRPT: "srpt", BOOST: "boost", SPF: "spf", SJF: "sjf", LAS: "las",
-                TRAIL: "trail"}
+                TRAIL: "trail", DIST: "distboost"}
 LEVELS = 24
 
 # One numpy record per instance; field order mirrors the C struct tas_setting.
@@ -55,7 +55,7 @@ SETTING_DTYPE = np.dtype(
         ("ada_window", np.int32),
         ("ada_min_samples", np.int32),
         ("ada_grid", np.int32),
-        ("ada_reserved", np.int32),
+        ("signal", np.int32),
     ]
 )
 
@@ -110,12 +110,14 @@ class Workload:
 # ---------------------------------------------------------------- settings
 
 
-def setting(trace, policy, k=1, memguard=0, delta_us=0, gamma=0.0, table=None, ada=None):
+def setting(trace, policy, k=1, memguard=0, delta_us=0, gamma=0.0, table=None, ada=None,
+            signal=0):
     """One instance record. ``ada``: adaptive-gamma parameters (keys of ADA
-    without the ``ada_`` prefix, e.g. ``dict(ADA)``), gamma being the start."""
+    without the ``ada_`` prefix, e.g. ``dict(ADA)``), gamma being the start.
+    ``signal`` 1: Algorithm 2's phase-aware boost signal (BOOST)."""
     s = np.zeros((), dtype=SETTING_DTYPE)
     s["trace"], s["policy"], s["k"], s["memguard"] = trace, policy, k, memguard
-    s["delta_us"], s["gamma"] = delta_us, gamma
+    s["delta_us"], s["gamma"], s["signal"] = delta_us, gamma, signal
     if ada is not None:
         s["ada"] = 1
         for key, v in ada.items():

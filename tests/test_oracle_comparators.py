@@ -108,7 +108,7 @@ def test_trail_never_preempts_past_threshold():
     ep, row, vol = 0, 0, 0
     for i, it in enumerate(o["iters"]):
         while ep < len(ev) and ev[ep][0] == i:
-            _, v, forced = ev[ep]
+            _, v, forced, _ = ev[ep]
             ep += 1
             if not forced:
                 assert 5 * dec[v] < 3 * d[v]
@@ -126,11 +126,15 @@ def test_trail_never_preempts_past_threshold():
     assert not np.array_equal(s["counters"], o["counters"])  # the threshold changed something
 
 
-@pytest.mark.parametrize("policy,blind", [(SPF, True), (LAS, True), (SJF, False)])
-def test_blindness(policy, blind):
-    """SPF and LAS use no knowledge of the output length (prediction-free):
-    lengthening one request's decode leaves every event before its original
-    completion unchanged. SJF reads the length."""
+@pytest.mark.parametrize("policy,blind,kw", [
+    (SPF, True, {}), (LAS, True, {}), (SJF, False, {}),
+    (W.DIST, True, dict(k=1, gamma=1e-3)), (W.DIST, True, dict(k=16, gamma=3e-2)),
+    (W.BOOST, True, dict(k=16, memguard=1, delta_us=20000, gamma=1e-3, signal=1))])
+def test_blindness(policy, blind, kw):
+    """SPF, LAS, DistBoost and the boost with the phase-aware signal use no
+    knowledge of the output length (prediction-free): lengthening one
+    request's decode leaves every event before its original completion
+    unchanged. SJF reads the length."""
     changed = 0
     for seed in range(4):
         a, p, d = W.small_random(seed, 120, rate_per_s=60.0)
@@ -138,8 +142,8 @@ def test_blindness(policy, blind):
         j = 17
         d2 = d.copy()
         d2[j] += 500
-        o1 = oracle.log(a, p, d, e, policy)
-        o2 = oracle.log(a, p, d2, e, policy)
+        o1 = oracle.log(a, p, d, e, policy, **kw)
+        o2 = oracle.log(a, p, d2, e, policy, **kw)
         ends = np.cumsum(o1["iters"][:, 2])
         last = max(i for i in range(len(ends))
                    if j in o1["batch"][(ends[i] - o1["iters"][i, 2]):ends[i], 0])
@@ -150,3 +154,4 @@ def test_blindness(policy, blind):
         changed += not same
     if not blind:
         assert changed > 0
+

@@ -21,7 +21,14 @@ def blocks(x, bs):
     return -(-x // bs)
 
 
-def key_of(policy, r, a, p, d, kv, dec, k, table):
+def sig_of(r, p, dec, signal):
+    """The boost signal: P + dec, or (signal 1) P in prefill and dec in decode."""
+    if signal == 1:
+        return int(p[r]) if dec[r] == 0 else int(dec[r])
+    return int(p[r] + dec[r])
+
+
+def key_of(policy, r, a, p, d, kv, dec, k, table, signal=0, t_first=None):
     """Iteration-start priority key of request r (lower is served first)."""
     if policy == 0:
         return int(a[r])  # FCFS: arrival
@@ -33,11 +40,16 @@ def key_of(policy, r, a, p, d, kv, dec, k, table):
         return int(d[r])  # SJF
     if policy == 5:
         return int(p[r] + dec[r])  # LAS: attained service
-    lvl = min(23, (max(int(p[r] + dec[r]), k) // k).bit_length() - 1)
+    if policy == 7:  # DistBoost: the decode queue (by entry time) before the prefill queue
+        if dec[r] > 0:
+            return (0, int(t_first[r]))
+        lvl = min(23, (max(int(p[r]), k) // k).bit_length() - 1)
+        return (1, int(a[r]) - int(table[lvl]))
+    lvl = min(23, (max(sig_of(r, p, dec, signal), k) // k).bit_length() - 1)
     return int(a[r]) - int(table[lvl])  # boost: a - b(quantized signal)
 
 
-def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None):
+def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_us=0):
     N = len(a)
     bs = e.block_tokens
     kv = np.zeros(N, np.int64)
@@ -64,23 +76,50 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None):
             assert t0 == min(a[r] for r in range(N) if not done[r] and a[r] > t_expect)
             idle += t0 - t_expect
         resident_before = {r for r in range(N) if kv[r] > 0}
-        # evictions of this iteration
+        batch = o["batch"][row:row + nb]
+        row += nb
+        # iteration-start keys of every active request
+        active = [r for r in range(N) if a[r] <= t0 and not done[r]]
+        key0 = {r: key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first) for r in active}
+
+        def eligible(x):  # may be a voluntary victim (MemGuard, TRAIL threshold)
+            if memguard and not oracle.level(sig_of(x, p, dec, signal), k) > guard[x]:
+                return False
+            return not (policy == 6 and 5 * dec[x] >= 3 * d[x])
+
+        def worse(x, r):  # x ranks after r by more than delta
+            if isinstance(key0[x], tuple):
+                return (key0[x], x) > (key0[r], r)
+            return (key0[x] - delta_us, x) > (key0[r], r)
+
+        # evictions of this iteration, each checked against the victim rules:
+        # a voluntary victim is the worst eligible resident outside the batch
+        # that ranks after the candidate by more than delta; a forced one only
+        # happens when there is none, and takes the worst other resident
+        # outside the batch, or the candidate itself when none is left
         evicted = set()
+        mem_set = [int(x) for x in batch[:, 0]]
         while ev_ptr < len(ev) and ev[ev_ptr][0] == i:
-            _, v, forced = ev[ev_ptr]
+            _, v, forced, cand = (int(x) for x in ev[ev_ptr])
             ev_ptr += 1
             assert kv[v] > 0 and not done[v]
+            assert kv[cand] > 0 or not forced  # only a resident candidate forces
+            before = {m for m in mem_set if (key0[m], m) < (key0[cand], cand)}
+            outside = [x for x in resident_before
+                       if x not in evicted and x not in before and x != cand]
+            vol = [x for x in outside if eligible(x) and worse(x, cand)]
             if not forced:
                 vol_per_req[v] += 1
-                if memguard:  # I9: MemGuard eligibility
-                    assert oracle.level(int(p[v] + dec[v]), k) > guard[v]
-                if policy == 6:  # TRAIL swap prevention
-                    assert 5 * dec[v] < 3 * d[v]
+                assert vol and v == max(vol, key=lambda x: (key0[x], x)), (i, v, cand)
+            else:
+                assert not vol, (i, v, cand, vol)
+                if v != cand:
+                    assert v == max(outside, key=lambda x: (key0[x], x)), (i, v, cand)
+                else:
+                    assert not outside, (i, v, outside)
             evicted_kv_total += kv[v]
             kv[v] = 0
             evicted.add(v)
-        batch = o["batch"][row:row + nb]
-        row += nb
         # I2 batch limits
         assert 1 <= nb <= e.max_seqs
         ns = batch[:, 1].astype(np.int64)
@@ -90,14 +129,15 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None):
         # formation takes candidates in ascending (key, idx) order of the
         # iteration-start keys (batch members were not evicted, so their kv is
         # still the iteration-start value)
-        keys = [(key_of(policy, r, a, p, d, kv, dec, k, table), r) for r in members]
+        keys = [(key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first), r)
+                for r in members]
         assert keys == sorted(keys)
         assert not (set(members) & evicted)
         for r in members:
             assert a[r] <= t0 and not done[r]
             assert kv[r] < p[r] + dec[r]
             if kv[r] == 0:
-                guard[r] = oracle.level(int(p[r] + dec[r]), k)
+                guard[r] = oracle.level(sig_of(r, p, dec, signal), k)
                 if r not in first_dispatch:
                     first_dispatch.append(r)
         # no request may wait while the batch still has room (stop rule), except
@@ -106,6 +146,25 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None):
         if nb < e.max_seqs and ns.sum() < e.max_tokens:
             for r in resident_before:
                 assert r in members or r in evicted
+            # eviction completeness: formation saw every candidate, so a waiting
+            # request left out was refused for KV after every eligible victim
+            # worse than it (by more than delta) had been evicted; none may remain
+            # resident outside the batch
+            outside = [v for v in range(N) if kv[v] > 0 and v not in members and not done[v]]
+            if outside:
+                waiting = [w for w in range(N) if a[w] <= t0 and not done[w] and kv[w] == 0
+                           and w not in members and w not in evicted]
+                def eligible(v):
+                    if memguard and not oracle.level(sig_of(v, p, dec, signal), k) > guard[v]:
+                        return False
+                    return not (policy == 6 and 5 * dec[v] >= 3 * d[v])
+                for w in waiting:
+                    kw = key_of(policy, w, a, p, d, kv, dec, k, table, signal, t_first)
+                    for v in outside:
+                        kvv = key_of(policy, v, a, p, d, kv, dec, k, table, signal, t_first)
+                        worse = ((kvv, v) > (kw, w)) if isinstance(kvv, tuple) else \
+                            ((kvv - delta_us, v) > (kw, w))
+                        assert not (worse and eligible(v)), (i, w, v)
         # cost model and I1
         ctx = sum(int(kv[r] + n) for r, n in zip(members, ns))
         assert dt == e.iter_base_us + e.iter_tok_us * int(ns.sum()) + ctx // e.iter_ctx_div
@@ -146,7 +205,7 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None):
     assert np.all(o["ttlt"].astype(np.int64) - o["ttft"] >= (d.astype(np.int64) - 1) * e.iter_base_us)
     if policy == 0:  # I7 FCFS dispatches in arrival order
         assert first_dispatch == sorted(first_dispatch)
-    if memguard:  # Phase 3 revision bound per request
+    if memguard and signal == 0:  # Phase 3 revision bound per request (monotone signal)
         for r in range(N):
             bound = 1 + math.floor(math.log2(max(int(p[r] + d[r]), k) / k))
             assert vol_per_req[r] <= bound
@@ -168,6 +227,10 @@ POLICIES = [
     dict(policy=2, k=16, memguard=1, delta_us=20000, gamma=1e-3),
     dict(policy=2, k=1, memguard=0, delta_us=0, gamma=1e-3),
     dict(policy=2, k=32, memguard=1, delta_us=0, gamma=3e-2),
+    dict(policy=7, k=1, gamma=1e-3),  # DistBoost
+    dict(policy=7, k=16, gamma=3e-2),
+    dict(policy=2, k=16, memguard=1, delta_us=20000, gamma=1e-3, signal=1),  # phase-aware signal
+    dict(policy=2, k=1, memguard=0, delta_us=0, gamma=3e-2, signal=1),
 ]
 
 
@@ -179,12 +242,13 @@ def test_replay_invariants(seed, ei, pi):
     pol = POLICIES[pi]
     a, p, d = W.small_random(seed * 10 + ei, 160, rate_per_s=60.0, p_max=400, d_max=200)
     o = oracle.log(a, p, d, e, pol["policy"], k=pol.get("k", 1), memguard=pol.get("memguard", 0),
-                   delta_us=pol.get("delta_us", 0), gamma=pol.get("gamma"))
+                   delta_us=pol.get("delta_us", 0), gamma=pol.get("gamma"),
+                   signal=pol.get("signal", 0))
     assert o["rc"] == 0
     table = (oracle.boost_table(pol["gamma"], pol.get("k", 1), e.tau_us)
-             if pol["policy"] == 2 else None)
+             if pol["policy"] in (2, 7) else None)
     replay(a, p, d, e, o, pol["policy"], k=pol.get("k", 1), memguard=pol.get("memguard", 0),
-           table=table)
+           table=table, signal=pol.get("signal", 0), delta_us=pol.get("delta_us", 0))
 
 
 def test_replay_sees_evictions():
