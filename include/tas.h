@@ -22,7 +22,14 @@
  *                  swap-prevention threshold)
  *       TAS_BOOST  key = a_i - boost_us[level(P_i + dec_i)]    (Phase 2 unified
  *                  key Phi = a - b_gamma(w~) with w~ = max(w, s_pre); Phase 3
- *                  MemGuard quantization level = floor(log2(max(w,k)/k)))
+ *                  MemGuard quantization level = floor(log2(max(w,k)/k)));
+ *                  with signal = 1 the level is that of Algorithm 2's
+ *                  phase-aware signal: P_i before the first token, dec_i after
+ *       TAS_DIST   DistBoost (Phase 1): before its first token a request is
+ *                  in the prefill queue, key a_i - boost_us[level(P_i)]; after
+ *                  it, in the decode queue, key t_first - 2^42, so the decode
+ *                  queue in order of entry fills the batch first and prefill
+ *                  chunks fill the rest
  *   - a greedy pass fills the batch under a sequence cap, a token budget and a
  *     KV-block budget, evicting (recompute preemption) the worst resident when
  *     KV runs out; MemGuard and the hysteresis delta restrict voluntary
@@ -88,7 +95,7 @@ enum {
 };
 
 enum { TAS_FCFS = 0, TAS_SRPT = 1, TAS_BOOST = 2, TAS_SPF = 3, TAS_SJF = 4, TAS_LAS = 5,
-       TAS_TRAIL = 6 };
+       TAS_TRAIL = 6, TAS_DIST = 7 };
 
 #define TAS_LEVELS 24
 
@@ -105,8 +112,8 @@ typedef struct {
 /* One instance: a trace and a policy setting. */
 typedef struct {
     int32_t trace;    /* index into the traces                                 */
-    int32_t policy;   /* one of the TAS_FCFS .. TAS_TRAIL policies above       */
-    int32_t k;        /* MemGuard granularity in tokens (BOOST), >= 1          */
+    int32_t policy;   /* one of the TAS_FCFS .. TAS_DIST policies above        */
+    int32_t k;        /* MemGuard granularity in tokens (BOOST, DIST), >= 1    */
     int32_t memguard; /* 1: a dispatched request is non-evictable until its
                          level passes the level it was dispatched at (BOOST)  */
     int64_t delta_us; /* hysteresis: a voluntary victim's key must exceed the
@@ -175,8 +182,10 @@ size_t tas_workspace_bytes(const tas_traces *traces, const tas_params *params);
  * Returns TAS_EINVAL if: n_req < 1 or >= 2^20; an arrival is negative,
  * >= 2^41 or out of order; P or D < 1; P + D >= 2^24; a trace index is out of
  * range; policy unknown; k < 1 (BOOST); delta < 0; memguard or delta nonzero
- * for a policy other than BOOST; gamma <= 0 without table_given (BOOST); an explicit table not
- * non-increasing or outside [0, 2^42]; ada not 0 or 1; ada = 1 with a policy
+ * for a policy other than BOOST; gamma <= 0 without table_given (BOOST,
+ * DIST); an explicit table not non-increasing or outside [0, 2^42] (DIST:
+ * [0, 2^40], also for a table built from gamma); signal not 0, or 1 for BOOST;
+ * ada not 0 or 1; ada = 1 with a policy
  * other than BOOST, with table_given, or with an ada_* field outside its
  * range; chunk > max_tokens; any engine limit
  * < 1; chunk > 32767; tau <= 0; list_cap < max_seqs + 64 or > 4032.

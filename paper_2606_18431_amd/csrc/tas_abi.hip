@@ -28,6 +28,7 @@ namespace {
 constexpr int64_t kMaxLds = 160 * 1024;  // gfx950 LDS per workgroup
 constexpr int64_t kTwo41 = int64_t(1) << 41;
 constexpr int64_t kTwo42 = int64_t(1) << 42;
+constexpr int64_t kTwo40 = int64_t(1) << 40;  // DistBoost tables: decode keys stay below
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -137,25 +138,30 @@ bool ada_ok(const tas_setting &s) {
            s.ada_min_samples <= s.ada_window && s.ada_grid >= 2 && s.ada_grid <= TAS_ADA_GRID_MAX;
 }
 
-int check_setting(const tas_setting &s, int32_t n_traces) {
+int check_setting(const tas_setting &s, int32_t n_traces, double tau_us) {
     if (s.trace < 0 || s.trace >= n_traces) return TAS_EINVAL;
     if (s.ada != 0 && (s.ada != 1 || !ada_ok(s))) return TAS_EINVAL;
-    if (s.signal != 0) return TAS_EINVAL;  // the phase-aware signal: not built yet
-    if (s.policy < TAS_FCFS || s.policy > TAS_TRAIL) return TAS_EINVAL;
+    if (s.signal != 0 && (s.signal != 1 || s.policy != TAS_BOOST)) return TAS_EINVAL;
+    if (s.policy < TAS_FCFS || s.policy > TAS_DIST) return TAS_EINVAL;
     if (s.delta_us < 0) return TAS_EINVAL;
+    const bool boosted = s.policy == TAS_BOOST || s.policy == TAS_DIST;
     if (s.policy != TAS_BOOST) {
         if (s.memguard != 0 || s.delta_us != 0) return TAS_EINVAL;
-        return TAS_OK;
+        if (!boosted) return TAS_OK;
     }
     if (s.k < 1 || (s.memguard != 0 && s.memguard != 1)) return TAS_EINVAL;
     if (s.delta_us >= kTwo42) return TAS_EINVAL;
+    const int64_t cap = s.policy == TAS_DIST ? kTwo40 : kTwo42;
     if (s.table_given) {
         for (int j = 0; j < TAS_LEVELS; j++) {
-            if (s.boost_us[j] < 0 || s.boost_us[j] > kTwo42) return TAS_EINVAL;
+            if (s.boost_us[j] < 0 || s.boost_us[j] > cap) return TAS_EINVAL;
             if (j && s.boost_us[j] > s.boost_us[j - 1]) return TAS_EINVAL;
         }
     } else if (!(s.gamma > 0.0) || !std::isfinite(s.gamma)) {
         return TAS_EINVAL;
+    } else if (s.policy == TAS_DIST) {
+        int64_t bt[TAS_LEVELS];
+        if (tas_boost_table(s.gamma, s.k, tau_us, bt) || bt[0] > cap) return TAS_EINVAL;
     }
     return TAS_OK;
 }
@@ -218,7 +224,7 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
         if (i % (size_t)N && a < t->arrival_us[i - 1]) return TAS_EINVAL;
     }
     for (int32_t i = 0; i < p->n_inst; i++) {
-        int rc = check_setting(p->inst[i], t->n_traces);
+        int rc = check_setting(p->inst[i], t->n_traces, p->tau_us);
         if (rc) return rc;
     }
     for (size_t i = 0; i < tn; i++) {
@@ -241,15 +247,19 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     c->settings.resize((size_t)p->n_inst);
     c->ada.resize((size_t)n_ada);
     int32_t ai = 0;
+    bool ext = n_ada > 0;  // the extended kernel build is needed
     for (int32_t i = 0; i < p->n_inst; i++) {
         const tas_setting &s = p->inst[i];
         tas::DevSetting &d = c->settings[(size_t)i];
         std::memset(&d, 0, sizeof d);
-        d.trace = s.trace, d.policy = s.policy, d.k = s.policy == TAS_BOOST ? s.k : 1;
+        const bool boosted = s.policy == TAS_BOOST || s.policy == TAS_DIST;
+        d.trace = s.trace, d.policy = s.policy, d.k = boosted ? s.k : 1;
         d.memguard = s.policy == TAS_BOOST ? s.memguard : 0;
         d.delta = s.policy == TAS_BOOST ? s.delta_us : 0;
         d.ada = -1;
-        if (s.policy == TAS_BOOST) {
+        d.signal = s.signal;
+        if (s.signal || s.policy == TAS_DIST) ext = true;
+        if (boosted) {
             if (s.table_given) std::memcpy(d.bt, s.boost_us, sizeof d.bt);
             else tas_boost_table(s.gamma, s.k, p->tau_us, d.bt);
         }
@@ -313,6 +323,7 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     a.gamma_out = (double *)(ws + L.gamma);
     a.switch_out = (int64_t *)(ws + L.switches);
     a.ada_window = wmax;
+    a.ext = ext ? 1 : 0;
     *out = c;
     return TAS_OK;
 }

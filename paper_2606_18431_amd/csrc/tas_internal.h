@@ -24,7 +24,7 @@ struct DevSetting {
     int64_t bt[kLevels];  // boost in us per MemGuard level (non-increasing);
                           // with adaptive gamma, the table of the first grid cell
     int32_t ada;          // index into SimArgs::ada, or -1
-    int32_t pad;
+    int32_t signal;       // BOOST: 1 = Algorithm 2's phase-aware signal
 };
 
 // Adaptive gamma of one instance (host-built): the update constants, the
@@ -78,7 +78,8 @@ struct SimArgs {
     double *gamma_out;   // [n_inst] final adaptive gamma (0 without)
     int64_t *switch_out; // [n_inst] grid-cell changes
     int32_t ada_window;  // largest window over the adaptive instances (LDS), 0 if none
-    int32_t pad;
+    int32_t ext;         // some instance needs the extended build (adaptive gamma,
+                         // the phase-aware signal, DistBoost)
 };
 
 // Bytes of the adaptive-gamma block: its state (gamma, gamma_hat, counters),

@@ -62,8 +62,14 @@ enum { S_OK = 0, S_EOVERFLOW = -5, S_ELIVELOCK = -6, S_ESTATE = -7, S_ECAPACITY 
 // oracle-length SRPT, and the further comparison policies of its Table 1 and
 // evaluation baselines: shortest prompt first (SPF), shortest job first with
 // perfect output-length knowledge (SJF), least attained service (LAS) and
-// SRPT with TRAIL's swap-prevention threshold (TRAIL).
-enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2, P_SPF = 3, P_SJF = 4, P_LAS = 5, P_TRAIL = 6 };
+// SRPT with TRAIL's swap-prevention threshold (TRAIL); and the Phase 1
+// strawman DistBoost (DIST).
+enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2, P_SPF = 3, P_SJF = 4, P_LAS = 5, P_TRAIL = 6,
+       P_DIST = 7 };
+// DistBoost ranks its decode queue (key: the time a request entered it, its
+// first-token time) ahead of its prefill queue: decode keys are shifted down
+// by 2^42, below every prefill key a - bt (boost tables are capped at 2^40).
+constexpr int64_t kDecodeQueueOff = int64_t(1) << 42;
 
 // ------------------------------------------------------------ wave helpers
 
@@ -268,7 +274,7 @@ DEV R permute_rec(const R &x, int dest) {
 // 16-token block gets its own instantiation), -1 otherwise. The policy is a
 // run-time value: one copy of the code serves every policy, so workgroups of
 // different policies on one compute unit share the instruction cache.
-template <int BSH, bool ADA>
+template <int BSH, bool EXT>
 struct Sim {
     const SimArgs &A;
     Lds S;
@@ -306,6 +312,7 @@ struct Sim {
     // the midpoint above grid point j (+infinity beyond)
     const DevAda *ad;
     double bnd;
+    bool phase_signal;  // BOOST with Algorithm 2's signal: P in prefill, dec after
 
     DEV Sim(const SimArgs &a, const DevSetting &st, int i, unsigned char *smem) : A(a) {
         inst = i;
@@ -334,13 +341,14 @@ struct Sim {
         for (int j = lane(); j < kLevels; j += kWave) S.bt[j] = st.bt[j];
         ad = nullptr;
         bnd = 0.0;
-        if constexpr (ADA) {
+        phase_signal = EXT && st.signal == 1;
+        if constexpr (EXT) {
             S.as = (AdaLds *)(smem + o), o += kAdaStateBytes;
             S.wr = (uint32_t *)(smem + o), o += (size_t)a.ada_window * 4;
             S.ws = (uint32_t *)(smem + o);
             ad = st.ada >= 0 ? a.ada + st.ada : nullptr;
         }
-        if (ADA && ad) {  // the table of the first cell is st.bt
+        if (EXT && ad) {  // the table of the first cell is st.bt
             bnd = ad->bound[lane()];
             if (lane() == 0) {
                 AdaLds &G = *S.as;
@@ -373,7 +381,7 @@ struct Sim {
     // within lcap): its grid changes let residents outside the batch pile up,
     // and a list padded with waiting entries costs every pass over it.
     DEV int cap_now() const {
-        if constexpr (ADA) {
+        if constexpr (EXT) {
             return min(lcap, max(M, nR) + 128);
         } else {
             return lcap;
@@ -996,6 +1004,13 @@ struct Sim {
                     if (!(gs & G_FIRST)) {
                         gs |= G_FIRST;
                         tfirst[idx] = t_end;
+                        if constexpr (EXT) {
+                            if (pol == P_DIST && left > 0) {  // enters DistBoost's decode queue
+                                pk = pack(t_end - kDecodeQueueOff, idx);
+                                gs |= G_DIRTY;
+                                chg = true;
+                            }
+                        }
                     } else {
                         // gaps beyond 2^32 overflow TTLT too; tbtw starts at 0
                         __hip_atomic_fetch_max(&tbtw[idx], t32 - tl, __ATOMIC_RELAXED,
@@ -1014,7 +1029,11 @@ struct Sim {
                         chg = true;
                     } else if (pol == P_BOOST) {
                         const int lo_ = (int)((gs >> G_LVL_SHIFT) & 31u);
-                        const int ln = level_of(w, k, lk);
+                        int sig = w;  // P + dec
+                        if constexpr (EXT) {
+                            if (phase_signal) sig = w - Pp[idx];  // dec >= 1 after this token
+                        }
+                        const int ln = level_of(sig, k, lk);
                         if (ln != lo_) {
                             pk = pack(key_of(pk) + S.bt[lo_] - S.bt[ln], idx);
                             gs = (gs & ~G_LVL) | ((uint32_t)ln << G_LVL_SHIFT) | G_DIRTY;
@@ -1042,7 +1061,7 @@ struct Sim {
                 if (lohole == INT32_MAX) lohole = b + ffs0(fm);
                 nd += popc(fm);
                 if (vm_ok && lane() == (b >> 6)) vm_res &= ~fm, vm_ev &= ~fm;
-                if constexpr (ADA) {
+                if constexpr (EXT) {
                     if (ad) {  // end-to-end latencies enter the window in batch order
                         uint32_t lat = 0;
                         if (fin) {
@@ -1304,7 +1323,7 @@ struct Sim {
                 take_arrivals();
                 continue;
             }
-            if constexpr (ADA) {
+            if constexpr (EXT) {
                 if (ad) {
                     ada_update();
                     if (status) break;
@@ -1357,7 +1376,7 @@ struct Sim {
             int64_t *cn = A.counters + (size_t)inst * 8;
             cn[0] = iters, cn[1] = reqiters, cn[2] = tokens, cn[3] = ev_vol;
             cn[4] = ev_forced, cn[5] = t, cn[6] = maxU, cn[7] = idle;
-            if constexpr (ADA) {  // (zero from tas_create for the other build)
+            if constexpr (EXT) {  // (zero from tas_create for the other build)
                 A.gamma_out[inst] = ad ? S.as->gamma : 0.0;
                 A.switch_out[inst] = ad ? S.as->switches : 0;
             }
@@ -1366,23 +1385,24 @@ struct Sim {
     }
 };
 
-template <int BSH, bool ADA>
+template <int BSH, bool EXT>
 DEV void run_instance(const SimArgs &a, const DevSetting &st, int inst, unsigned char *smem) {
-    Sim<BSH, ADA> s(a, st, inst, smem);
+    Sim<BSH, EXT> s(a, st, inst, smem);
     s.run();
 }
 
-// ADA: the build with adaptive gamma, launched when some instance uses it
-// (its extra state costs the fixed-gamma path registers).
-template <bool ADA>
+// EXT: the extended build (adaptive gamma, the phase-aware signal,
+// DistBoost), launched when some instance uses one of them (its extra state
+// and code cost the other policies registers).
+template <bool EXT>
 __global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int inst = blockIdx.x;
     if (inst >= a.n_inst) return;
     if (a.retry && a.status[inst] != S_ECAPACITY) return;
     const DevSetting &st = a.inst[inst];
-    if (a.bs == 16) run_instance<4, ADA>(a, st, inst, smem);
-    else run_instance<-1, ADA>(a, st, inst, smem);
+    if (a.bs == 16) run_instance<4, EXT>(a, st, inst, smem);
+    else run_instance<-1, EXT>(a, st, inst, smem);
 }
 
 }  // namespace
@@ -1391,14 +1411,14 @@ __global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
 int tas_launch_sim(const tas::SimArgs &a, int64_t lds_bytes, void *stream) {
     if (a.n_inst <= 0) return 0;
     hipStream_t s = (hipStream_t)stream;
-    const void *fn = a.ada_window > 0 ? (const void *)tas::sim_kernel<true>
-                                      : (const void *)tas::sim_kernel<false>;
+    const void *fn = a.ext ? (const void *)tas::sim_kernel<true>
+                           : (const void *)tas::sim_kernel<false>;
     if (lds_bytes > 65536) {
         if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)lds_bytes) != hipSuccess)
             return -4;
     }
-    if (a.ada_window > 0)
+    if (a.ext)
         hipLaunchKernelGGL(tas::sim_kernel<true>, dim3((unsigned)a.n_inst), dim3(64),
                            (size_t)lds_bytes, s, a);
     else

@@ -22,7 +22,9 @@ The policy-parameter grid per trace: setting 0 = FCFS, setting 1 = oracle-length
 SRPT, then pairs (UniBoost with MemGuard, vanilla boost) over log-spaced gamma.
 ``make(cfg, grid="comparators")`` instead runs every trace under the paper's
 comparison policies (FCFS, SRPT, SPF, SJF, LAS, TRAIL) beside UniBoost and vanilla
-boost; ``make(cfg, grid="ada")`` runs fixed against adaptive gamma (Phase 4).
+boost; ``make(cfg, grid="ada")`` runs fixed against adaptive gamma (Phase 4);
+``make(cfg, grid="ladder")`` runs the paper's design phases (DistBoost to the
+full UniBoost) and the phase-aware signal.
 """
 from __future__ import annotations
 
@@ -331,13 +333,34 @@ def ada_settings(n_traces: int, ada: dict | None = None) -> np.ndarray:
     return out
 
 
+def ladder_settings(n_traces: int, gamma: float = 1e-3, ada: dict | None = None) -> np.ndarray:
+    """Per trace, 8 settings along the paper's design phases at one gamma:
+    DistBoost (Phase 1, k = 1), UniBoost-Base (Phase 2: k = 1, no MemGuard,
+    hysteresis 0.1 s), + MemGuard (Phase 3: k = 256), + adaptive gamma (the
+    full UniBoost), the Phase 3 setting and vanilla boost with Algorithm 2's
+    phase-aware signal, then FCFS and SRPT. Instance id = trace * 8 + s."""
+    ada = dict(ADA if ada is None else ada)
+    per = [dict(policy=DIST, gamma=gamma, k=1),
+           dict(policy=BOOST, gamma=gamma, k=1, memguard=0, delta_us=100_000),
+           dict(policy=BOOST, gamma=gamma, **UNIBOOST),
+           dict(policy=BOOST, gamma=gamma, ada=ada, **UNIBOOST),
+           dict(policy=BOOST, gamma=gamma, signal=1, **UNIBOOST),
+           dict(policy=BOOST, gamma=gamma, signal=1, **VANILLA),
+           dict(policy=FCFS), dict(policy=SRPT)]
+    out = np.zeros(n_traces * len(per), dtype=SETTING_DTYPE)
+    for t in range(n_traces):
+        for s, kw in enumerate(per):
+            out[t * len(per) + s] = setting(t, **kw)
+    return out
+
+
 def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
          n_req: int | None = None, grid: str = "sweep") -> Workload:
     """Build workload ``cfg``. The optional overrides shrink it (fewer traces,
     settings or requests) for tests; traces keep their seeds, so trace t of a
     shrunk workload equals trace t of the full one when n_req is unchanged.
     ``grid="comparators"`` replaces the settings grid by comparator_settings,
-    ``grid="ada"`` by ada_settings."""
+    ``grid="ada"`` by ada_settings, ``grid="ladder"`` by ladder_settings."""
     T0, S0, N0 = SHAPES[cfg]
     T = T0 if n_traces is None else n_traces
     S = S0 if n_settings is None else n_settings
@@ -353,6 +376,9 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
         S = 8
     elif grid == "ada":
         sets = ada_settings(T)
+        S = 8
+    elif grid == "ladder":
+        sets = ladder_settings(T)
         S = 8
     elif cfg == 0 and S == 8:
         st = [setting(0, FCFS), setting(0, SRPT)]

@@ -68,7 +68,8 @@ def test_hand_worked_on_gpu(torch, case):
     e = W.Engine(**case["engine"])
     tb = case.get("table")
     s = W.setting(0, case["policy"], k=case.get("k", 1), memguard=case.get("memguard", 0),
-                  delta_us=case.get("delta_us", 0), table=tb if tb is not None else None)
+                  delta_us=case.get("delta_us", 0), table=tb if tb is not None else None,
+                  signal=case.get("signal", 0))
     w = W.Workload(case["name"], np.array([case["arrival"]], np.int64),
                    np.array([case["prompt"]], np.int32), np.array([case["decode"]], np.int32),
                    e, np.stack([s]))
