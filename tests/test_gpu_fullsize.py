@@ -75,3 +75,40 @@ def test_full_size_sampled_parity(torch, cfg):
         assert np.array_equal(g["counters"][i], o["counters"][j]), (i, g["counters"][i],
                                                                     o["counters"][j])
         assert np.array_equal(g["pct"][i], o["pct"][j]), (i, g["pct"][i], o["pct"][j])
+
+
+@pytest.mark.parametrize("grid", ["ada", "ladder"])
+def test_full_size_large_sweep_other_grids(torch, grid):
+    """The large-sweep traces (256 x 50,000 requests) under the adaptive-gamma
+    and design-phase settings grids, in the launch `bench.py --grid` times (the
+    extended kernel build, its default list size): every instance TAS_OK, and
+    all eight settings of the first and the last trace exactly equal to the
+    oracle, final adaptive gamma bit for bit."""
+    from paper_2606_18431_amd import tas
+
+    w = W.make(4, grid=grid)
+    print(f"[gpu] full-size large sweep, {grid} grid: {w.n_inst} instances", flush=True)
+    sim = tas.Simulation(w)
+    sim.step()
+    n, m = w.n_inst, w.n_req
+    dev = sim.pct.device
+    lat = [torch.empty((n, m), dtype=torch.int32, device=dev) for _ in range(3)]
+    tas.tas_latencies(sim.ctx, *lat)
+    g = sim.results(latencies=False)
+    assert g["rc"] == 0, tas.tas_strerror(g["rc"])
+    assert (g["status"] == 0).all()
+    sel = np.concatenate([np.arange(8), np.arange(n - 8, n)])
+    idx = torch.as_tensor(sel, device=dev)
+    got = {k: t.index_select(0, idx).cpu().numpy().view(np.uint32)
+           for k, t in zip(("ttft", "ttlt", "tbtmax"), lat)}
+    sim.close()
+    del lat
+    o = oracle.run(w.subset(sel), n_threads=min(16, os.cpu_count() or 1))
+    assert o["rc"] == 0
+    for j, i in enumerate(sel):
+        for key in ("ttft", "ttlt", "tbtmax"):
+            assert np.array_equal(got[key][j], o[key][j]), (i, key)
+        assert np.array_equal(g["counters"][i], o["counters"][j]), i
+        assert np.array_equal(g["pct"][i], o["pct"][j]), i
+        assert g["switches"][i] == o["switches"][j], i
+        assert g["gamma"][i:i + 1].view(np.int64)[0] == o["gamma"][j:j + 1].view(np.int64)[0], i
