@@ -1,0 +1,105 @@
+"""Edge cases of the extended kernel build on the GPU against the CPU oracle
+(through the C ABI): adaptive gamma at the ends of its parameter ranges
+(window 1 and the 2048 maximum, grids of 2 and 64 points, beta 0 and 1, gamma0
+at either bound, min_samples equal to the window), DistBoost and the
+phase-aware signal with the smallest on-chip list (spills, refills and the
+retry pass), and one-request traces under every policy. Exact, the final
+adaptive gamma bit for bit."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_18431_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def gpu_run(w, **kw):
+    from paper_2606_18431_amd import tas
+
+    print(f"[gpu] {w.name} traces={w.n_traces} inst={w.n_inst} n_req={w.n_req} {kw}", flush=True)
+    sim = tas.Simulation(w, **kw)
+    sim.step()
+    out = sim.results()
+    sim.close()
+    return out
+
+
+def assert_parity(g, o):
+    assert np.array_equal(g["status"], o["status"]), (g["status"], o["status"])
+    assert np.all(g["status"] == 0)
+    for key in ("ttft", "ttlt", "tbtmax", "counters", "pct", "switches"):
+        assert np.array_equal(g[key], o[key]), key
+    assert np.array_equal(g["gamma"].view(np.int64), o["gamma"].view(np.int64))
+
+
+def with_settings(base, sets, name):
+    return W.Workload(name, base.arrival_us, base.prompt, base.decode, base.engine,
+                      np.stack(sets))
+
+
+EXTREMES = [
+    dict(W.ADA, window=1, min_samples=1, beta=1.0),
+    dict(W.ADA, window=2048, min_samples=2048, beta=0.3),
+    dict(W.ADA, window=2048, min_samples=16, beta=0.05, grid=64),
+    dict(W.ADA, window=32, min_samples=32, beta=0.0),
+    dict(W.ADA, window=64, min_samples=8, beta=0.5, grid=2, eps_us=1e-3),
+    dict(W.ADA, window=100, min_samples=50, beta=1.0, gamma_min=1e-3, gamma_max=1e-3 * 1.0001,
+         grid=3),
+]
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_ada_parameter_extremes(torch, cfg):
+    base = W.make(cfg, n_traces=1, n_req=3000)
+    sets = []
+    for i, ada in enumerate(EXTREMES):
+        g0 = ada["gamma_min"] if i % 2 == 0 else ada["gamma_max"]
+        mg = dict(W.UNIBOOST) if i % 2 == 0 else dict(W.VANILLA)
+        sets.append(W.setting(0, W.BOOST, gamma=g0, ada=ada, **mg))
+    w = with_settings(base, sets, base.name + " adaptive extremes")
+    g = gpu_run(w)
+    o = oracle.run(w)
+    assert_parity(g, o)
+
+
+@pytest.mark.parametrize("cfg,cap", [(2, 128), (3, 128), (2, 192)])
+def test_phase_variants_smallest_list(torch, cfg, cap):
+    """DistBoost and the phase-aware signal (with and without MemGuard) at the
+    smallest list the engine allows: spills, refills and retries."""
+    base = W.make(cfg, n_traces=1, n_req=3000)
+    sets = [W.setting(0, W.DIST, gamma=1e-3, k=1), W.setting(0, W.DIST, gamma=3e-2, k=16),
+            W.setting(0, W.BOOST, gamma=1e-3, signal=1, **W.UNIBOOST),
+            W.setting(0, W.BOOST, gamma=3e-2, signal=1, **W.VANILLA),
+            W.setting(0, W.BOOST, gamma=1e-3, signal=1, ada=dict(W.ADA, window=40,
+                                                                min_samples=20), **W.UNIBOOST)]
+    w = with_settings(base, sets, base.name + " phase variants")
+    g = gpu_run(w, list_cap=cap)
+    o = oracle.run(w)
+    assert_parity(g, o)
+
+
+def test_one_request_every_policy(torch):
+    e = W.Engine()
+    sets = [W.setting(0, p) for p in (W.FCFS, W.SRPT, W.SPF, W.SJF, W.LAS, W.TRAIL)]
+    sets += [W.setting(0, W.BOOST, gamma=1e-3, **W.UNIBOOST),
+             W.setting(0, W.DIST, gamma=1e-3),
+             W.setting(0, W.BOOST, gamma=1e-3, signal=1, **W.UNIBOOST),
+             W.setting(0, W.BOOST, gamma=1e-3, ada=dict(W.ADA, window=1, min_samples=1),
+                       **W.UNIBOOST)]
+    for P, D in ((1, 1), (5000, 3), (16, 700)):
+        w = W.Workload(f"one request P={P} D={D}", np.array([[123]], np.int64),
+                       np.array([[P]], np.int32), np.array([[D]], np.int32), e, np.stack(sets))
+        g = gpu_run(w)
+        o = oracle.run(w)
+        assert_parity(g, o)
+        assert len(set(g["ttlt"][:, 0].tolist())) == 1  # alone, every policy is the same
