@@ -84,6 +84,11 @@ def main():
                     help="settings grid per trace (default: the gamma sweep)")
     ap.add_argument("--no-ada", action="store_true",
                     help="run the adaptive settings of the grid with gamma fixed at its start")
+    ap.add_argument("--cluster", type=int, default=0,
+                    help="R > 0: clusters of R replicas behind a global router (the workload's "
+                         "traces, R times the rate, split by --dispatch); reports the cluster "
+                         "percentiles pooled over each cluster's replicas")
+    ap.add_argument("--dispatch", default="rr", choices=["rr", "random"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
     ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--list-cap", type=int, default=0,
@@ -114,9 +119,17 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": n, "ok": bool(dst[-1].item() == 1)}))
         return
-    w = W.make(args.workload, n_traces=args.traces, grid=args.grid)
-    name = f"{W.NAMES[args.workload]}: {w.n_traces} traces x {w.meta['n_settings']} settings x " \
-           f"{w.n_req} requests"
+    if args.cluster:
+        R = args.cluster
+        n_cl = args.traces or max(1, W.SHAPES[args.workload][0] // R)
+        w = W.make_cluster(args.workload, n_clusters=n_cl, replicas=R, dispatch=args.dispatch,
+                           n_req=W.SHAPES[args.workload][2] // R)
+        name = f"{W.NAMES[args.workload]}: {n_cl} clusters x {R} replicas ({args.dispatch} " \
+               f"dispatch) x {w.meta['n_settings']} settings x {w.n_req} requests per replica"
+    else:
+        w = W.make(args.workload, n_traces=args.traces, grid=args.grid)
+        name = f"{W.NAMES[args.workload]}: {w.n_traces} traces x {w.meta['n_settings']} " \
+               f"settings x {w.n_req} requests"
     if args.grid != "sweep":
         name += f", {args.grid} settings grid"
     if args.no_ada:
@@ -181,8 +194,18 @@ def main():
                      "kernel": "sim_kernel",
                      "algorithmic_bytes_per_launch": alg_bytes},
     }
+    if args.cluster:  # cluster percentiles pooled over each cluster's replicas
+        gp = sim.group_percentiles(args.cluster).astype(np.int64)
+        S = w.meta["n_settings"]
+        per = gp.reshape(w.meta["n_clusters"], S, 3, 3)
+        res["config"]["cluster_p99_ttlt_us_mean"] = {
+            W.POLICY_NAMES[int(w.settings["policy"][s * args.cluster])] + f"_s{s}":
+            float(per[:, s, 1, 2].mean()) for s in range(S)}
+        res["config"]["cluster_p99_tbt_us_mean"] = {
+            W.POLICY_NAMES[int(w.settings["policy"][s * args.cluster])] + f"_s{s}":
+            float(per[:, s, 2, 2].mean()) for s in range(S)}
     sim.close()
-    if not args.no_cpu:
+    if not args.no_cpu and not args.cluster:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         o, sel, cb = cpu_baseline(w, args.cpu_threads)
         res["cpu_baseline"] = cb

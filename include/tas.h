@@ -205,6 +205,14 @@ int tas_run(tas_ctx *ctx, void *stream);
  * the same stream. */
 int tas_percentiles(tas_ctx *ctx, uint32_t *d_out, void *stream);
 
+/* Nearest-rank percentiles over groups of `group` adjacent instances (the
+ * replicas of one cluster behind a global router; paper: global dispatch
+ * policies and cluster scale): d_out DEVICE uint32 [n_inst/group][3][3], the
+ * value at sorted position ceil(q*m/100) - 1 of the group's m = group*n_req
+ * latencies pooled. Call after tas_run on the same stream. TAS_EINVAL unless
+ * group >= 1 divides n_inst and group*n_req < 2^31. */
+int tas_percentiles_grouped(tas_ctx *ctx, int32_t group, uint32_t *d_out, void *stream);
+
 /* Enqueue device-to-device copies of the per-request latencies, DEVICE
  * uint32 [n_inst][n_req] each, microseconds relative to arrival; any pointer
  * may be NULL to skip that array. */

@@ -208,6 +208,19 @@ def level(w: int, k: int) -> int:
     return int(lib().tas_oracle_level(int(w), int(k)))
 
 
+def group_percentiles(out, group: int) -> np.ndarray:
+    """Nearest-rank percentiles pooled over groups of `group` adjacent
+    instances of an oracle.run() result: [n_inst/group, 3, 3]."""
+    n = out["ttft"].shape[0] // group
+    res = np.zeros((n, 3, 3), np.uint32)
+    for g in range(n):
+        for m, key in enumerate(("ttft", "ttlt", "tbtmax")):
+            pooled = np.ascontiguousarray(out[key][g * group:(g + 1) * group].ravel())
+            for j, q in enumerate((50, 90, 99)):
+                res[g, m, j] = percentile(pooled, q)
+    return res
+
+
 def percentile(values: np.ndarray, q: int) -> int:
     v = np.ascontiguousarray(values, np.uint32)
     return int(lib().tas_oracle_percentile(_p(v), len(v), int(q)))

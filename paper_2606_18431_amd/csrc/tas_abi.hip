@@ -350,6 +350,18 @@ int tas_percentiles(tas_ctx *c, uint32_t *d_out, void *stream) {
                : TAS_OK;
 }
 
+int tas_percentiles_grouped(tas_ctx *c, int32_t group, uint32_t *d_out, void *stream) {
+    if (!c || !d_out || group < 1 || c->n_inst % group != 0 ||
+        (int64_t)c->n_req * group > INT32_MAX)
+        return TAS_EINVAL;
+    c->last_stream = (hipStream_t)stream;
+    // the rows of `group` adjacent instances are one contiguous run of values
+    return tas_launch_pctl(c->args.ttft, c->args.ttlt, c->args.tbtmax, c->n_inst / group,
+                           c->n_req * group, d_out, stream)
+               ? TAS_EHIP
+               : TAS_OK;
+}
+
 int tas_latencies(tas_ctx *c, uint32_t *d_ttft, uint32_t *d_ttlt, uint32_t *d_tbtmax,
                   void *stream) {
     if (!c) return TAS_EINVAL;

@@ -61,7 +61,8 @@ class tas_params(ctypes.Structure):
 
 assert ctypes.sizeof(tas_setting) == W.SETTING_DTYPE.itemsize == 280
 
-EXPORTS = ["tas_workspace_bytes", "tas_create", "tas_run", "tas_percentiles", "tas_latencies",
+EXPORTS = ["tas_workspace_bytes", "tas_create", "tas_run", "tas_percentiles",
+           "tas_percentiles_grouped", "tas_latencies",
            "tas_counters", "tas_gamma", "tas_status", "tas_instance_status", "tas_destroy",
            "tas_strerror", "tas_boost_table", "tas_ada_grid", "tas_instance_table",
            "tas_list_cap"]
@@ -81,12 +82,14 @@ def lib():
         L.tas_workspace_bytes.argtypes = [P, P]
         L.tas_workspace_bytes.restype = ctypes.c_size_t
         L.tas_create.argtypes = [P, P, P, ctypes.c_size_t, ctypes.POINTER(P)]
-        for name in ("tas_create", "tas_run", "tas_percentiles", "tas_latencies", "tas_counters",
+        for name in ("tas_create", "tas_run", "tas_percentiles", "tas_percentiles_grouped",
+                     "tas_latencies", "tas_counters",
                      "tas_gamma", "tas_status", "tas_instance_status", "tas_boost_table",
                      "tas_ada_grid", "tas_instance_table"):
             getattr(L, name).restype = ctypes.c_int
         L.tas_run.argtypes = [P, P]
         L.tas_percentiles.argtypes = [P, P, P]
+        L.tas_percentiles_grouped.argtypes = [P, i32, P, P]
         L.tas_latencies.argtypes = [P, P, P, P, P]
         L.tas_counters.argtypes = [P, P, P]
         L.tas_gamma.argtypes = [P, P, P, P]
@@ -175,6 +178,11 @@ def tas_run(ctx, stream=None):
 
 def tas_percentiles(ctx, out, stream=None):
     _check(lib().tas_percentiles(ctx, _ptr(out), _stream(stream)), "tas_percentiles")
+
+
+def tas_percentiles_grouped(ctx, group: int, out, stream=None):
+    _check(lib().tas_percentiles_grouped(ctx, int(group), _ptr(out), _stream(stream)),
+           "tas_percentiles_grouped")
 
 
 def tas_latencies(ctx, ttft=None, ttlt=None, tbtmax=None, stream=None):
@@ -291,6 +299,15 @@ class Simulation:
         out["status"] = self.status_buf.cpu().numpy()
         out["pct"] = self.pct.cpu().numpy().view(np.uint32)
         return out
+
+    def group_percentiles(self, group: int, stream=None) -> np.ndarray:
+        """Percentiles pooled over groups of `group` adjacent instances
+        [n_inst/group, 3, 3] (synchronises)."""
+        torch = self.torch
+        out = torch.zeros((self.w.n_inst // group, 3, 3), dtype=torch.int32,
+                          device=self.pct.device)
+        tas_percentiles_grouped(self.ctx, group, out, stream)
+        return out.cpu().numpy().view(np.uint32)
 
     def table(self, inst: int) -> np.ndarray:
         return tas_instance_table(self.ctx, inst)

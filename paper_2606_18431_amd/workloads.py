@@ -392,6 +392,62 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
                     meta=dict(cfg=cfg, n_traces=T, n_settings=S, n_req=N, grid=grid))
 
 
+def make_cluster(cfg: int, n_clusters: int, replicas: int, dispatch: str = "rr",
+                 n_req: int | None = None, settings: list | None = None) -> Workload:
+    """Replicas behind a global router (paper: global dispatch policies and
+    cluster scale). Cluster c receives the requests of one global trace: the
+    trace of workload ``cfg`` with ``n_req * replicas`` requests whose time
+    axis is compressed ``replicas`` times (the router sees ``replicas`` times
+    the rate that loads one replica to the workload's utilisation). The
+    router assigns them to replicas, each replica schedules its own requests:
+
+    - ``dispatch="rr"``: round robin, request i goes to replica i mod R;
+    - ``dispatch="random"``: balanced random, each block of R consecutive
+      requests goes to a uniformly random permutation of the replicas (the
+      assignment is drawn here, seeded, and is an input of both sides).
+
+    Every replica receives ``n_req`` requests. Instances are ordered cluster,
+    setting, replica, so the R replicas of a (cluster, setting) are R adjacent
+    instances (``tas_percentiles_grouped`` with group R reduces over them).
+    Traces are ordered cluster, replica. ``settings``: keyword dicts for
+    ``setting`` (default FCFS, UniBoost at gamma 1e-3, vanilla boost)."""
+    T0, _, N0 = SHAPES[cfg]
+    N = N0 if n_req is None else n_req
+    R = int(replicas)
+    eng = _engine(cfg)
+    per = settings if settings is not None else [
+        dict(policy=FCFS), dict(policy=BOOST, gamma=1e-3, **UNIBOOST),
+        dict(policy=BOOST, gamma=1e-3, **VANILLA)]
+    arr = np.empty((n_clusters * R, N), np.int64)
+    pr = np.empty((n_clusters * R, N), np.int32)
+    de = np.empty((n_clusters * R, N), np.int32)
+    assign = np.empty((n_clusters, N * R), np.int32)
+    for c in range(n_clusters):
+        a, p, d = _trace(cfg, c, N * R, eng)
+        a = a // R  # R times the arrival rate
+        if dispatch == "rr":
+            rep = np.arange(N * R, dtype=np.int64) % R
+        elif dispatch == "random":
+            rng = np.random.default_rng([cfg, c, R, 7919])
+            rep = np.concatenate([rng.permutation(R) for _ in range(N)])
+        else:
+            raise ValueError(dispatch)
+        assign[c] = rep
+        for r in range(R):
+            sel = np.nonzero(rep == r)[0]
+            arr[c * R + r], pr[c * R + r], de[c * R + r] = a[sel], p[sel], d[sel]
+    sets = np.zeros(n_clusters * len(per) * R, dtype=SETTING_DTYPE)
+    i = 0
+    for c in range(n_clusters):
+        for kw in per:
+            for r in range(R):
+                sets[i] = setting(c * R + r, **kw)
+                i += 1
+    return Workload(f"{NAMES[cfg]} cluster", arr, pr, de, eng, sets,
+                    meta=dict(cfg=cfg, n_clusters=n_clusters, replicas=R, dispatch=dispatch,
+                              n_settings=len(per), n_req=N, assign=assign))
+
+
 def small_random(seed: int, n_req: int, *, rate_per_s: float = 20.0, p_med=64, d_med=20,
                  p_max=512, d_max=256):
     """A small random trace (for tests): lognormal lengths, Poisson arrivals."""

@@ -70,3 +70,20 @@ def test_distboost_differs_from_boost(torch):
     g = gpu_run(w)
     assert not np.array_equal(g["ttlt"][0], g["ttlt"][1])
     assert not np.array_equal(g["ttlt"][2], g["ttlt"][4])  # signal P + dec vs phase-aware
+
+
+def test_extended_build_deterministic_and_order_independent(torch):
+    """Two runs give identical bytes, and permuting the instances (so other
+    workgroups share a compute unit with each) permutes the results."""
+    w = W.make(2, n_traces=2, n_req=2000, grid="ladder")
+    g1 = gpu_run(w)
+    g2 = gpu_run(w)
+    keys = ("ttft", "ttlt", "tbtmax", "counters", "pct", "switches")
+    for key in keys:
+        assert np.array_equal(g1[key], g2[key])
+    assert np.array_equal(g1["gamma"].view(np.int64), g2["gamma"].view(np.int64))
+    perm = np.random.default_rng(2).permutation(w.n_inst)
+    g3 = gpu_run(w.subset(perm))
+    for key in keys:
+        assert np.array_equal(g3[key], g1[key][perm])
+    assert np.array_equal(g3["gamma"].view(np.int64), g1["gamma"][perm].view(np.int64))
