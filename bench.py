@@ -6,7 +6,7 @@ percentile kernel. Inputs (traces, settings) are resident in HBM before the
 timed region. Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 4]
-                 [--grid sweep|ada|comparators|ladder] [--no-ada]
+                 [--grid sweep|ada|comparators|ladder|cache] [--no-ada]
 
 Roofline: the simulation kernel is counted against HBM bandwidth with
 algorithmic bytes of 32 B per request-iteration (read + write of the request's
@@ -80,7 +80,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", type=int, default=4, choices=[0, 1, 2, 3, 4])
     ap.add_argument("--traces", type=int, default=None, help="shrink the sweep (testing)")
-    ap.add_argument("--grid", default="sweep", choices=["sweep", "ada", "comparators", "ladder"],
+    ap.add_argument("--grid", default="sweep",
+                    choices=["sweep", "ada", "comparators", "ladder", "cache"],
                     help="settings grid per trace (default: the gamma sweep)")
     ap.add_argument("--no-ada", action="store_true",
                     help="run the adaptive settings of the grid with gamma fixed at its start")

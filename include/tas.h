@@ -24,7 +24,12 @@
  *                  key Phi = a - b_gamma(w~) with w~ = max(w, s_pre); Phase 3
  *                  MemGuard quantization level = floor(log2(max(w,k)/k)));
  *                  with signal = 1 the level is that of Algorithm 2's
- *                  phase-aware signal: P_i before the first token, dec_i after
+ *                  phase-aware signal: P_i before the first token, dec_i after;
+ *                  with signal = 2 that of P_i - h_i + dec_i, h_i the expected
+ *                  prefix-cache hit tokens (section "Interaction with other
+ *                  system optimization", prefix/radix caching: effective work
+ *                  max(w, s_pre - h) with cached tokens not counted as
+ *                  processed); the engine still prefills all P_i tokens
  *       TAS_DIST   DistBoost (Phase 1): before its first token a request is
  *                  in the prefill queue, key a_i - boost_us[level(P_i)]; after
  *                  it, in the decode queue, key t_first - 2^42, so the decode
@@ -107,6 +112,9 @@ typedef struct {
     const int64_t *arrival_us;  /* [n_traces*n_req], 0 <= a < 2^41, sorted     */
     const int32_t *prompt;      /* [n_traces*n_req], >= 1                      */
     const int32_t *decode;      /* [n_traces*n_req], >= 1; P + D < 2^24        */
+    const int32_t *cached;      /* [n_traces*n_req] expected prefix-cache hit
+                                   tokens, 0 <= h < P, or NULL; read only by
+                                   settings with signal = 2                    */
 } tas_traces;
 
 /* One instance: a trace and a policy setting. */
@@ -135,7 +143,8 @@ typedef struct {
                                 [1, ada_window]                                */
     int32_t ada_grid;      /* grid points G, in [2, TAS_ADA_GRID_MAX]          */
     int32_t signal;        /* BOOST: 0 = P + dec; 1 = the phase-aware signal of
-                              Algorithm 2 (P in prefill, dec in decode); 0
+                              Algorithm 2 (P in prefill, dec in decode); 2 =
+                              P - h + dec with h from tas_traces.cached; 0
                               for every other policy                          */
 } tas_setting;
 
@@ -184,7 +193,8 @@ size_t tas_workspace_bytes(const tas_traces *traces, const tas_params *params);
  * range; policy unknown; k < 1 (BOOST); delta < 0; memguard or delta nonzero
  * for a policy other than BOOST; gamma <= 0 without table_given (BOOST,
  * DIST); an explicit table not non-increasing or outside [0, 2^42] (DIST:
- * [0, 2^40], also for a table built from gamma); signal not 0, or 1 for BOOST;
+ * [0, 2^40], also for a table built from gamma); signal not 0, or 1 or 2 for
+ * BOOST; signal 2 without traces->cached; a cached value < 0 or >= its P;
  * ada not 0 or 1; ada = 1 with a policy
  * other than BOOST, with table_given, or with an ada_* field outside its
  * range; chunk > max_tokens; any engine limit

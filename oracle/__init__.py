@@ -49,10 +49,10 @@ def lib():
         i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
         L.tas_oracle_boost_table.argtypes = [f64, i32, f64, P]
         L.tas_oracle_boost_table.restype = ctypes.c_int
-        L.tas_oracle_run.argtypes = [i32, i32, P, P, P, i32, P, P, P, P, P, P, P, i64,
+        L.tas_oracle_run.argtypes = [i32, i32, P, P, P, P, i32, P, P, P, P, P, P, P, i64,
                                      P, P, P, P, P, P, P, P, P, P, i32]
         L.tas_oracle_run.restype = ctypes.c_int
-        L.tas_oracle_log.argtypes = [i32, P, P, P, i32, i32, i32, i64, P, P, i32, P, i64, P,
+        L.tas_oracle_log.argtypes = [i32, P, P, P, P, i32, i32, i32, i64, P, P, i32, P, i64, P,
                                      P, P, P, P, i64, P, i64, P, i64, P, P, P]
         L.tas_oracle_ada_grid.argtypes = [P, i32, P, P, P]
         L.tas_oracle_ada_grid.restype = ctypes.c_int
@@ -68,6 +68,15 @@ def lib():
 def _p(a: np.ndarray):
     assert a.flags["C_CONTIGUOUS"]
     return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _cached(h, shape):
+    """Expected prefix-cache hit tokens as a contiguous int32 array, or None."""
+    if h is None:
+        return None
+    h = np.ascontiguousarray(h, np.int32)
+    assert h.shape == shape, (h.shape, shape)
+    return h
 
 
 def boost_table(gamma: float, k: int, tau_us: float = 5000.0) -> np.ndarray:
@@ -134,6 +143,7 @@ def run(w, n_threads: int | None = None, max_iters: int | None = None):
     arr = np.ascontiguousarray(w.arrival_us, np.int64)
     pr = np.ascontiguousarray(w.prompt, np.int32)
     de = np.ascontiguousarray(w.decode, np.int32)
+    ch = _cached(w.cached, de.shape)
     tr = np.ascontiguousarray(s["trace"], np.int32)
     po = np.ascontiguousarray(s["policy"], np.int32)
     kk = np.ascontiguousarray(s["k"], np.int32)
@@ -155,7 +165,8 @@ def run(w, n_threads: int | None = None, max_iters: int | None = None):
     )
     mi = w.engine.max_iters if max_iters is None else max_iters
     nt = n_threads or os.cpu_count() or 1
-    rc = lib().tas_oracle_run(w.n_traces, n_req, _p(arr), _p(pr), _p(de), n_inst, _p(tr),
+    rc = lib().tas_oracle_run(w.n_traces, n_req, _p(arr), _p(pr), _p(de),
+                              None if ch is None else _p(ch), n_inst, _p(tr),
                               _p(po), _p(kk), _p(mg), _p(dl), _p(tb), _p(_eng(w.engine)),
                               int(mi), _p(out["ttft"]), _p(out["ttlt"]), _p(out["tbtmax"]),
                               _p(out["counters"]), _p(out["pct"]), _p(out["status"]), _p(ada),
@@ -165,13 +176,15 @@ def run(w, n_threads: int | None = None, max_iters: int | None = None):
 
 
 def log(arrival, prompt, decode, engine, policy, k=1, memguard=0, delta_us=0, table=None,
-        gamma=None, ada=None, signal=0, max_iters=None, cap_iter=1 << 20, cap_batch=1 << 22,
-        cap_evict=1 << 20):
+        gamma=None, ada=None, signal=0, cached=None, max_iters=None, cap_iter=1 << 20,
+        cap_batch=1 << 22, cap_evict=1 << 20):
     """Run one instance and return its schedule log (see tas_oracle.h). ``ada``:
-    adaptive-gamma parameters as in workloads.ADA (gamma is the start)."""
+    adaptive-gamma parameters as in workloads.ADA (gamma is the start);
+    ``cached``: expected prefix-cache hit tokens per request (signal 2)."""
     arrival = np.ascontiguousarray(arrival, np.int64)
     prompt = np.ascontiguousarray(prompt, np.int32)
     decode = np.ascontiguousarray(decode, np.int32)
+    ch = _cached(cached, decode.shape)
     n = len(arrival)
     if table is None:
         table = (boost_table(gamma, k, engine.tau_us) if gamma is not None
@@ -189,7 +202,8 @@ def log(arrival, prompt, decode, engine, policy, k=1, memguard=0, delta_us=0, ta
     ev = np.zeros((cap_evict, 4), np.int64)
     ni, nb, ne = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     mi = engine.max_iters if max_iters is None else max_iters
-    rc = lib().tas_oracle_log(n, _p(arrival), _p(prompt), _p(decode), policy, k, memguard,
+    rc = lib().tas_oracle_log(n, _p(arrival), _p(prompt), _p(decode),
+                              None if ch is None else _p(ch), policy, k, memguard,
                               int(delta_us), _p(table), _p(prm), int(signal),
                               _p(_eng(engine)), int(mi),
                               _p(o["ttft"]), _p(o["ttlt"]), _p(o["tbtmax"]), _p(o["counters"]),

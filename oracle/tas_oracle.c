@@ -63,6 +63,10 @@
  *   signal 1 (BOOST): the phase-aware signal of Algorithm 2: the prompt length
  *         while in prefill, the decode tokens emitted after it (the level,
  *         the key and MemGuard's guard all use it)
+ *   signal 2 (BOOST): prefix caching (paper: interaction with prefix/radix
+ *         caching): with h expected cached prompt tokens the effective work is
+ *         max(w, P - h), i.e. P - h + dec when cached tokens are not counted as
+ *         processed; the engine itself is unchanged
  *
  * Adaptive gamma (Phase 4, gamma-Ada), for BOOST instances that ask for it:
  *   - the window holds the end-to-end latencies (TTLT, us, capped at 2^32-1)
@@ -113,7 +117,9 @@ typedef struct {
     int32_t M, T, c, Kb, bs, base, tok, div;
     int64_t max_iters;
     const ada_t *ada; /* NULL: gamma fixed */
-    int32_t signal;   /* BOOST: 0 = P + dec, 1 = Algorithm 2's phase-aware signal */
+    int32_t signal;   /* BOOST: 0 = P + dec, 1 = Algorithm 2's phase-aware signal,
+                         2 = P - h + dec (expected prefix-cache hits h) */
+    const int32_t *H; /* expected cached prompt tokens per request, or NULL */
 } inst_t;
 
 typedef struct {
@@ -177,9 +183,10 @@ static int32_t level_of(int64_t w, int32_t k) {
 int32_t tas_oracle_level(int64_t w, int32_t k) { return level_of(w, k); }
 
 /* The boost signal of request r: P + dec, or (signal 1) P during the prefill
- * and the decode tokens emitted after it. */
+ * and the decode tokens emitted after it, or (signal 2) P - h + dec. */
 static int64_t signal_of(const inst_t *I, int32_t r, const req_t *q) {
     if (I->signal == 1) return q->dec == 0 ? I->P[r] : q->dec;
+    if (I->signal == 2) return (int64_t)I->P[r] - I->H[r] + q->dec;
     return (int64_t)I->P[r] + q->dec;
 }
 
@@ -276,9 +283,11 @@ static int simulate(const inst_t *I0, uint32_t *ttft, uint32_t *ttlt, uint32_t *
     const inst_t *I = &J;
     const ada_t *A = I->ada && I->ada->on ? I->ada : NULL;
     const int32_t N = I->N;
+    if (I->signal == 2 && !I->H) return TOR_EINVAL;
     for (int32_t i = 0; i < N; i++) {
         if (I->P[i] < 1 || I->D[i] < 1 || I->a[i] < 0 || (i && I->a[i] < I->a[i - 1]))
             return TOR_EINVAL;
+        if (I->H && (I->H[i] < 0 || I->H[i] >= I->P[i])) return TOR_EINVAL;
         if (blocks((int64_t)I->P[i] + I->D[i] - 1, I->bs) > I->Kb) return TOR_EINFEASIBLE;
     }
     req_t *R = (req_t *)calloc((size_t)N, sizeof *R);
@@ -553,7 +562,7 @@ uint32_t tas_oracle_percentile(const uint32_t *v, int32_t n, int32_t q) {
 typedef struct {
     int32_t n_req, n_inst;
     const int64_t *arrival;
-    const int32_t *prompt, *decode;
+    const int32_t *prompt, *decode, *cached;
     const int32_t *trace, *policy, *k, *memguard;
     const int64_t *delta, *table;
     const int32_t *eng;
@@ -578,6 +587,7 @@ static void fill_inst(inst_t *I, const int32_t *eng, int32_t n_req, const int64_
     I->max_iters = max_iters;
     I->ada = NULL;
     I->signal = 0;
+    I->H = NULL;
 }
 
 static void run_one(job_t *J, int32_t i) {
@@ -591,6 +601,7 @@ static void run_one(job_t *J, int32_t i) {
     ada_t *A = NULL;
     int st = 0;
     if (J->signal) I.signal = J->signal[i];
+    if (J->cached) I.H = J->cached + off;
     if (J->ada && J->ada[(size_t)i * 10] != 0.0) {
         A = (ada_t *)malloc(sizeof *A);
         st = A ? ada_setup(A, J->ada + (size_t)i * 10, J->policy[i], J->k[i]) : TOR_EINVAL;
@@ -622,7 +633,8 @@ static void *worker(void *arg) {
 }
 
 int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
-                   const int32_t *prompt, const int32_t *decode, int32_t n_inst,
+                   const int32_t *prompt, const int32_t *decode, const int32_t *cached,
+                   int32_t n_inst,
                    const int32_t *trace, const int32_t *policy, const int32_t *k,
                    const int32_t *memguard, const int64_t *delta, const int64_t *table,
                    const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
@@ -633,14 +645,15 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
     for (int32_t i = 0; i < n_inst; i++) {
         if (trace[i] < 0 || trace[i] >= n_traces || policy[i] < 0 || policy[i] > 7 || k[i] < 1)
             return TOR_EINVAL;
-        if (signal && signal[i] != 0 && (signal[i] != 1 || policy[i] != P_BOOST))
+        if (signal && signal[i] != 0 &&
+            (signal[i] < 1 || signal[i] > 2 || policy[i] != P_BOOST || (signal[i] == 2 && !cached)))
             return TOR_EINVAL;
     }
     if (eng[0] < 1 || eng[1] < 1 || eng[2] < 1 || eng[2] > eng[1] || eng[3] < 1 || eng[4] < 1 ||
         eng[5] < 1 || eng[6] < 0 || eng[7] < 1)
         return TOR_EINVAL;
     job_t J = {.n_req = n_req, .n_inst = n_inst, .arrival = arrival, .prompt = prompt,
-               .decode = decode, .trace = trace, .policy = policy, .k = k,
+               .decode = decode, .cached = cached, .trace = trace, .policy = policy, .k = k,
                .memguard = memguard, .delta = delta, .table = table, .eng = eng,
                .max_iters = max_iters, .ttft = ttft, .ttlt = ttlt, .tbtmax = tbtmax,
                .pct = pct, .counters = counters, .status = status, .ada = ada,
@@ -661,18 +674,21 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
 }
 
 int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
-                   const int32_t *decode, int32_t policy, int32_t k, int32_t memguard,
+                   const int32_t *decode, const int32_t *cached, int32_t policy, int32_t k,
+                   int32_t memguard,
                    int64_t delta, const int64_t *table, const double *ada, int32_t signal,
                    const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
                    uint32_t *tbtmax, int64_t *counters, int64_t *log_iter, int64_t iter_cap,
                    int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
                    int64_t evict_cap, int64_t *n_iter, int64_t *n_batch, int64_t *n_evict) {
-    if (policy < 0 || policy > 7 || (signal != 0 && (signal != 1 || policy != P_BOOST)))
+    if (policy < 0 || policy > 7 ||
+        (signal != 0 && (signal < 1 || signal > 2 || policy != P_BOOST || (signal == 2 && !cached))))
         return TOR_EINVAL;
     inst_t I;
     fill_inst(&I, eng, n_req, arrival, prompt, decode, policy, k, memguard, delta, table,
               max_iters);
     I.signal = signal;
+    I.H = cached;
     ada_t *A = NULL;
     if (ada && ada[0] != 0.0) {
         A = (ada_t *)malloc(sizeof *A);

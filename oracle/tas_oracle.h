@@ -15,6 +15,8 @@
  * All arguments are host pointers. Arrays are flat, C-contiguous:
  *   arrival [n_traces*n_req] int64 us, non-decreasing within a trace
  *   prompt, decode [n_traces*n_req] int32 tokens, >= 1
+ *   cached [n_traces*n_req] int32 expected prefix-cache hit tokens, 0 <= h < P,
+ *   or NULL (needed only by signal 2)
  *   per instance i: trace[i], policy[i] (0 FCFS, 1 SRPT, 2 BOOST, 3 SPF,
  *   4 SJF, 5 LAS, 6 TRAIL, 7 DIST), k[i] >= 1,
  *   memguard[i] in {0,1}, delta[i] >= 0 us, table[i*24 .. i*24+23] int64 us
@@ -39,7 +41,8 @@
  *
  * signal [n_inst] (NULL: all 0): the boost signal of a BOOST instance, 0 =
  * prompt plus emitted tokens, 1 = Algorithm 2's phase-aware signal (prompt
- * length in prefill, emitted tokens in decode).
+ * length in prefill, emitted tokens in decode), 2 = prompt minus expected
+ * cached tokens plus emitted tokens (prefix caching).
  */
 #ifndef TAS_ORACLE_H
 #define TAS_ORACLE_H
@@ -64,7 +67,8 @@ int tas_oracle_boost_table(double gamma, int32_t k, double tau_us, int64_t *out)
 /* Run all instances on n_threads host threads (instances are independent).
  * Returns 0 if every instance finished, else the first nonzero status. */
 int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
-                   const int32_t *prompt, const int32_t *decode, int32_t n_inst,
+                   const int32_t *prompt, const int32_t *decode, const int32_t *cached,
+                   int32_t n_inst,
                    const int32_t *trace, const int32_t *policy, const int32_t *k,
                    const int32_t *memguard, const int64_t *delta, const int64_t *table,
                    const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
@@ -83,7 +87,8 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
  * Capacities are in records. *n_iter, *n_batch, *n_evict receive the counts.
  * Returns the instance status, or TOR_EINVAL if a log buffer is too small. */
 int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
-                   const int32_t *decode, int32_t policy, int32_t k, int32_t memguard,
+                   const int32_t *decode, const int32_t *cached, int32_t policy, int32_t k,
+                   int32_t memguard,
                    int64_t delta, const int64_t *table, const double *ada, int32_t signal,
                    const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
                    uint32_t *tbtmax, int64_t *counters, int64_t *log_iter, int64_t iter_cap,

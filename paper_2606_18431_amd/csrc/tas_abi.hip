@@ -33,7 +33,7 @@ constexpr int64_t kTwo40 = int64_t(1) << 40;  // DistBoost tables: decode keys s
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-    size_t arrival, prompt, decode, settings, ada, tfirst, tlast, tbtw, ttft, ttlt, tbtmax,
+    size_t arrival, prompt, decode, cached, settings, ada, tfirst, tlast, tbtw, ttft, ttlt, tbtmax,
         counters, status, gamma, switches, spill, ovf, total;
 };
 
@@ -107,6 +107,7 @@ bool layout(const tas_traces *t, const tas_params *p, int32_t rc, int32_t sc, La
     L->arrival = o, o = align256(o + tn * 8);
     L->prompt = o, o = align256(o + tn * 4);
     L->decode = o, o = align256(o + tn * 4);
+    L->cached = o, o = align256(o + (t->cached ? tn * 4 : 0));
     L->settings = o, o = align256(o + (size_t)p->n_inst * sizeof(tas::DevSetting));
     int32_t wmax;
     L->ada = o, o = align256(o + (size_t)ada_count(p, &wmax) * sizeof(tas::DevAda));
@@ -138,10 +139,11 @@ bool ada_ok(const tas_setting &s) {
            s.ada_min_samples <= s.ada_window && s.ada_grid >= 2 && s.ada_grid <= TAS_ADA_GRID_MAX;
 }
 
-int check_setting(const tas_setting &s, int32_t n_traces, double tau_us) {
+int check_setting(const tas_setting &s, int32_t n_traces, double tau_us, bool has_cached) {
     if (s.trace < 0 || s.trace >= n_traces) return TAS_EINVAL;
     if (s.ada != 0 && (s.ada != 1 || !ada_ok(s))) return TAS_EINVAL;
-    if (s.signal != 0 && (s.signal != 1 || s.policy != TAS_BOOST)) return TAS_EINVAL;
+    if (s.signal != 0 && (s.signal < 1 || s.signal > 2 || s.policy != TAS_BOOST)) return TAS_EINVAL;
+    if (s.signal == 2 && !has_cached) return TAS_EINVAL;
     if (s.policy < TAS_FCFS || s.policy > TAS_DIST) return TAS_EINVAL;
     if (s.delta_us < 0) return TAS_EINVAL;
     const bool boosted = s.policy == TAS_BOOST || s.policy == TAS_DIST;
@@ -222,9 +224,10 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
         if (a < 0 || a >= kTwo41 || P < 1 || D < 1 || (int64_t)P + D >= (int64_t(1) << 24))
             return TAS_EINVAL;
         if (i % (size_t)N && a < t->arrival_us[i - 1]) return TAS_EINVAL;
+        if (t->cached && (t->cached[i] < 0 || t->cached[i] >= P)) return TAS_EINVAL;
     }
     for (int32_t i = 0; i < p->n_inst; i++) {
-        int rc = check_setting(p->inst[i], t->n_traces, p->tau_us);
+        int rc = check_setting(p->inst[i], t->n_traces, p->tau_us, t->cached != nullptr);
         if (rc) return rc;
     }
     for (size_t i = 0; i < tn; i++) {
@@ -283,6 +286,8 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     bool ok = hipMemcpy(ws + L.arrival, t->arrival_us, tn * 8, hipMemcpyHostToDevice) == hipSuccess &&
               hipMemcpy(ws + L.prompt, t->prompt, tn * 4, hipMemcpyHostToDevice) == hipSuccess &&
               hipMemcpy(ws + L.decode, t->decode, tn * 4, hipMemcpyHostToDevice) == hipSuccess;
+    if (ok && t->cached)
+        ok = hipMemcpy(ws + L.cached, t->cached, tn * 4, hipMemcpyHostToDevice) == hipSuccess;
     if (ok && p->n_inst > 0)
         ok = hipMemcpy(ws + L.settings, c->settings.data(),
                        c->settings.size() * sizeof(tas::DevSetting),
@@ -301,6 +306,7 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     a.arrival = (const int64_t *)(ws + L.arrival);
     a.prompt = (const int32_t *)(ws + L.prompt);
     a.decode = (const int32_t *)(ws + L.decode);
+    a.cached = t->cached ? (const int32_t *)(ws + L.cached) : nullptr;
     a.inst = (const tas::DevSetting *)(ws + L.settings);
     a.tfirst = (int64_t *)(ws + L.tfirst);
     a.tlast = (int64_t *)(ws + L.tlast);

@@ -24,7 +24,8 @@ struct DevSetting {
     int64_t bt[kLevels];  // boost in us per MemGuard level (non-increasing);
                           // with adaptive gamma, the table of the first grid cell
     int32_t ada;          // index into SimArgs::ada, or -1
-    int32_t signal;       // BOOST: 1 = Algorithm 2's phase-aware signal
+    int32_t signal;       // BOOST: 1 = Algorithm 2's phase-aware signal,
+                          // 2 = P - h + dec (expected prefix-cache hits h)
 };
 
 // Adaptive gamma of one instance (host-built): the update constants, the
@@ -79,7 +80,9 @@ struct SimArgs {
     int64_t *switch_out; // [n_inst] grid-cell changes
     int32_t ada_window;  // largest window over the adaptive instances (LDS), 0 if none
     int32_t ext;         // some instance needs the extended build (adaptive gamma,
-                         // the phase-aware signal, DistBoost)
+                         // the phase-aware or cache-aware signal, DistBoost)
+    const int32_t *cached;  // [n_traces][n_req] expected prefix-cache hits, or
+                            // null (read by the cache-aware signal only)
 };
 
 // Bytes of the adaptive-gamma block: its state (gamma, gamma_hat, counters),

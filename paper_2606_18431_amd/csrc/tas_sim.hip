@@ -313,6 +313,8 @@ struct Sim {
     const DevAda *ad;
     double bnd;
     bool phase_signal;  // BOOST with Algorithm 2's signal: P in prefill, dec after
+    bool cache_signal;  // BOOST with the cache-aware signal P - h + dec
+    const int32_t *Hp;  // expected prefix-cache hits of the trace (cache_signal)
 
     DEV Sim(const SimArgs &a, const DevSetting &st, int i, unsigned char *smem) : A(a) {
         inst = i;
@@ -342,6 +344,8 @@ struct Sim {
         ad = nullptr;
         bnd = 0.0;
         phase_signal = EXT && st.signal == 1;
+        cache_signal = EXT && st.signal == 2;
+        Hp = cache_signal ? a.cached + toff : nullptr;
         if constexpr (EXT) {
             S.as = (AdaLds *)(smem + o), o += kAdaStateBytes;
             S.wr = (uint32_t *)(smem + o), o += (size_t)a.ada_window * 4;
@@ -428,7 +432,12 @@ struct Sim {
         } else if (pol == P_SJF) {
             key = D;  // output length
         } else {
-            lvl = (uint32_t)level_of(P, k, lk);
+            int sig = P;  // the signal before the first token
+            if constexpr (EXT) {
+                // cached tokens are not work (lanes past the trace hold no request)
+                if (cache_signal && idx < N) sig = P - Hp[idx];
+            }
+            lvl = (uint32_t)level_of(sig, k, lk);
             key = a - S.bt[lvl];
         }
         x.gs = lvl << G_LVL_SHIFT;
@@ -1032,6 +1041,7 @@ struct Sim {
                         int sig = w;  // P + dec
                         if constexpr (EXT) {
                             if (phase_signal) sig = w - Pp[idx];  // dec >= 1 after this token
+                            if (cache_signal) sig = w - Hp[idx];  // P - h + dec
                         }
                         const int ln = level_of(sig, k, lk);
                         if (ln != lo_) {
@@ -1391,7 +1401,7 @@ DEV void run_instance(const SimArgs &a, const DevSetting &st, int inst, unsigned
     s.run();
 }
 
-// EXT: the extended build (adaptive gamma, the phase-aware signal,
+// EXT: the extended build (adaptive gamma, the phase-aware and cache-aware signals,
 // DistBoost), launched when some instance uses one of them (its extra state
 // and code cost the other policies registers).
 template <bool EXT>

@@ -34,7 +34,7 @@ class TasError(RuntimeError):
 class tas_traces(ctypes.Structure):
     _fields_ = [("n_traces", ctypes.c_int32), ("n_req", ctypes.c_int32),
                 ("arrival_us", ctypes.c_void_p), ("prompt", ctypes.c_void_p),
-                ("decode", ctypes.c_void_p)]
+                ("decode", ctypes.c_void_p), ("cached", ctypes.c_void_p)]
 
 
 class tas_setting(ctypes.Structure):
@@ -134,15 +134,22 @@ def _check(rc: int, what: str):
         raise TasError(rc, what)
 
 
-def make_traces(arrival_us: np.ndarray, prompt: np.ndarray, decode: np.ndarray):
-    """tas_traces over host arrays [n_traces, n_req]; returns (struct, keepalive)."""
+def make_traces(arrival_us: np.ndarray, prompt: np.ndarray, decode: np.ndarray,
+                cached: np.ndarray | None = None):
+    """tas_traces over host arrays [n_traces, n_req] (``cached``: expected
+    prefix-cache hit tokens, or None); returns (struct, keepalive)."""
     a = np.ascontiguousarray(arrival_us, np.int64)
     p = np.ascontiguousarray(prompt, np.int32)
     d = np.ascontiguousarray(decode, np.int32)
+    h = None if cached is None else np.ascontiguousarray(cached, np.int32)
     if a.ndim == 1:
         a, p, d = a[None], p[None], d[None]
-    t = tas_traces(a.shape[0], a.shape[1], a.ctypes.data, p.ctypes.data, d.ctypes.data)
-    return t, (a, p, d)
+        h = None if h is None else h[None]
+    if h is not None and h.shape != p.shape:
+        raise ValueError(f"cached has shape {h.shape}, prompts {p.shape}")
+    t = tas_traces(a.shape[0], a.shape[1], a.ctypes.data, p.ctypes.data, d.ctypes.data,
+                   None if h is None else h.ctypes.data)
+    return t, (a, p, d, h)
 
 
 def make_params(engine: W.Engine, settings: np.ndarray, list_cap: int = 0, spill_cap: int = 0,
@@ -250,7 +257,7 @@ class Simulation:
 
         self.w = w
         self.torch = torch
-        self._tr, self._keep_t = make_traces(w.arrival_us, w.prompt, w.decode)
+        self._tr, self._keep_t = make_traces(w.arrival_us, w.prompt, w.decode, w.cached)
         self._pa, self._keep_p = make_params(w.engine, w.settings, list_cap, spill_cap,
                                              max_iters, retry_cap)
         self.ws_bytes = tas_workspace_bytes(self._tr, self._pa)

@@ -90,6 +90,9 @@ class Workload:
     engine: Engine
     settings: np.ndarray  # SETTING_DTYPE [n_inst]
     meta: dict = dataclasses.field(default_factory=dict)
+    # expected prefix-cache hit tokens, int32 [n_traces, n_req] with
+    # 0 <= h < prompt, or None; read by settings with signal 2
+    cached: np.ndarray | None = None
 
     @property
     def n_traces(self) -> int:
@@ -116,7 +119,8 @@ def setting(trace, policy, k=1, memguard=0, delta_us=0, gamma=0.0, table=None, a
             signal=0):
     """One instance record. ``ada``: adaptive-gamma parameters (keys of ADA
     without the ``ada_`` prefix, e.g. ``dict(ADA)``), gamma being the start.
-    ``signal`` 1: Algorithm 2's phase-aware boost signal (BOOST)."""
+    ``signal`` 1: Algorithm 2's phase-aware boost signal (BOOST); 2: the
+    cache-aware signal P - h + dec (BOOST; needs the workload's ``cached``)."""
     s = np.zeros((), dtype=SETTING_DTYPE)
     s["trace"], s["policy"], s["k"], s["memguard"] = trace, policy, k, memguard
     s["delta_us"], s["gamma"], s["signal"] = delta_us, gamma, signal
@@ -315,6 +319,39 @@ def _trace(cfg: int, trace: int, n: int, eng: Engine):
     return arr, p, d
 
 
+def cached_tokens(seed, prompt: np.ndarray, share: float = 0.5, new_median: float = 64.0,
+                  new_sigma: float = 1.0) -> np.ndarray:
+    """Expected prefix-cache hit tokens for a multi-turn mix (paper: interaction
+    with prefix/radix caching, where the hits are the earlier turns' tokens). A
+    ``share`` of the requests are follow-up turns whose prompt is the
+    conversation so far plus a new message of lognormal length (median
+    ``new_median`` tokens, clipped to [1, P]); their hits are P minus that
+    message. The other requests are first turns with no hits. Seeded by
+    ``seed`` on a stream of its own, so the traces are unchanged."""
+    rng = np.random.default_rng([104729, *np.atleast_1d(seed).tolist()])
+    p = np.asarray(prompt, np.int64)
+    follow = rng.random(p.shape) < share
+    z = rng.standard_normal(p.shape)
+    new = np.clip(np.rint(np.exp(math.log(new_median) + new_sigma * z)), 1, p)
+    return np.where(follow, p - new, 0).astype(np.int32)
+
+
+def cache_settings(n_traces: int) -> np.ndarray:
+    """Per trace, 8 settings: UniBoost at gamma 1e-3 and 1e-2 and vanilla boost
+    at 1e-3, each with the signal P + dec and with the cache-aware signal
+    P - h + dec, then FCFS and SRPT. Instance id = trace * 8 + s."""
+    per = []
+    for g, var in ((1e-3, UNIBOOST), (1e-2, UNIBOOST), (1e-3, VANILLA)):
+        per.append(dict(policy=BOOST, gamma=g, **var))
+        per.append(dict(policy=BOOST, gamma=g, signal=2, **var))
+    per += [dict(policy=FCFS), dict(policy=SRPT)]
+    out = np.zeros(n_traces * len(per), dtype=SETTING_DTYPE)
+    for t in range(n_traces):
+        for s, kw in enumerate(per):
+            out[t * len(per) + s] = setting(t, **kw)
+    return out
+
+
 def ada_settings(n_traces: int, ada: dict | None = None) -> np.ndarray:
     """Per trace, 8 settings: for gamma0 in (1e-4, 1e-3, 1e-2) UniBoost with that
     fixed gamma and UniBoost with adaptive gamma started there, then vanilla
@@ -360,7 +397,9 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
     settings or requests) for tests; traces keep their seeds, so trace t of a
     shrunk workload equals trace t of the full one when n_req is unchanged.
     ``grid="comparators"`` replaces the settings grid by comparator_settings,
-    ``grid="ada"`` by ada_settings, ``grid="ladder"`` by ladder_settings."""
+    ``grid="ada"`` by ada_settings, ``grid="ladder"`` by ladder_settings and
+    ``grid="cache"`` by cache_settings, with expected prefix-cache hits drawn
+    by cached_tokens for every trace."""
     T0, S0, N0 = SHAPES[cfg]
     T = T0 if n_traces is None else n_traces
     S = S0 if n_settings is None else n_settings
@@ -380,6 +419,9 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
     elif grid == "ladder":
         sets = ladder_settings(T)
         S = 8
+    elif grid == "cache":
+        sets = cache_settings(T)
+        S = 8
     elif cfg == 0 and S == 8:
         st = [setting(0, FCFS), setting(0, SRPT)]
         st += [setting(0, BOOST, gamma=g, **UNIBOOST)
@@ -388,8 +430,12 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
         sets["trace"] = np.repeat(np.arange(T), 8)
     else:
         sets = settings_grid(T, S)
+    cached = None
+    if grid == "cache":
+        cached = np.stack([cached_tokens([cfg, t], pr[t]) for t in range(T)])
     return Workload(NAMES[cfg], arr, pr, de, eng, sets,
-                    meta=dict(cfg=cfg, n_traces=T, n_settings=S, n_req=N, grid=grid))
+                    meta=dict(cfg=cfg, n_traces=T, n_settings=S, n_req=N, grid=grid),
+                    cached=cached)
 
 
 def make_cluster(cfg: int, n_clusters: int, replicas: int, dispatch: str = "rr",

@@ -134,8 +134,8 @@ def small():
     return W.make(1, n_traces=2, n_settings=6, n_req=50)
 
 
-def create_rc(w, settings=None, engine=None, ws_bytes=None, **kw):
-    t, keep_t = tas.make_traces(w.arrival_us, w.prompt, w.decode)
+def create_rc(w, settings=None, engine=None, ws_bytes=None, cached=None, **kw):
+    t, keep_t = tas.make_traces(w.arrival_us, w.prompt, w.decode, cached)
     p, keep_p = tas.make_params(engine or w.engine, w.settings if settings is None else settings,
                                 **kw)
     need = tas.tas_workspace_bytes(t, p)
@@ -226,3 +226,33 @@ def test_rejects_infeasible_request():
 def test_strerror_covers_codes():
     for code in range(-8, 1):
         assert tas.tas_strerror(code) != "unknown error"
+
+
+def test_cache_signal_inputs():
+    """Expected prefix-cache hits: accepted with 0 <= h < P, laid out in the
+    workspace only when given, and required by (only) signal 2 of BOOST."""
+    w = small()
+    h = W.cached_tokens(0, w.prompt)
+    s = w.settings.copy()
+    s[2]["signal"] = 2
+    t0, _ = tas.make_traces(w.arrival_us, w.prompt, w.decode)
+    t1, _ = tas.make_traces(w.arrival_us, w.prompt, w.decode, h)
+    p, _ = tas.make_params(w.engine, s)
+    p0, _ = tas.make_params(w.engine, w.settings)
+    assert tas.tas_workspace_bytes(t1, p0) - tas.tas_workspace_bytes(t0, p0) == \
+        -(-(w.prompt.size * 4) // 256) * 256
+    # valid inputs get as far as the size check of a 1-byte workspace
+    assert create_rc(w, settings=s, cached=h, ws_bytes=1)[0] == tas.TAS_ENOMEM
+    assert create_rc(w, settings=s)[0] == tas.TAS_EINVAL  # signal 2 without hits
+    assert create_rc(w, cached=h, ws_bytes=1)[0] == tas.TAS_ENOMEM  # hits, no signal 2
+    for r, v in ((0, -1), (1, None)):
+        bad = h.copy()
+        bad[r, 3] = int(w.prompt[r, 3]) if v is None else v
+        assert create_rc(w, settings=s, cached=bad)[0] == tas.TAS_EINVAL
+    for pol, sig in ((W.FCFS, 2), (W.DIST, 2), (W.BOOST, 3)):
+        s2 = w.settings.copy()
+        s2[2] = W.setting(int(s2[2]["trace"]), pol, gamma=1e-3)
+        s2[2]["signal"] = sig
+        assert create_rc(w, settings=s2, cached=h)[0] == tas.TAS_EINVAL
+    with pytest.raises(ValueError):
+        tas.make_traces(w.arrival_us, w.prompt, w.decode, h[:1])

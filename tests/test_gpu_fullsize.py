@@ -77,10 +77,11 @@ def test_full_size_sampled_parity(torch, cfg):
         assert np.array_equal(g["pct"][i], o["pct"][j]), (i, g["pct"][i], o["pct"][j])
 
 
-@pytest.mark.parametrize("grid", ["ada", "ladder"])
+@pytest.mark.parametrize("grid", ["ada", "ladder", "cache"])
 def test_full_size_large_sweep_other_grids(torch, grid):
-    """The large-sweep traces (256 x 50,000 requests) under the adaptive-gamma
-    and design-phase settings grids, in the launch `bench.py --grid` times (the
+    """The large-sweep traces (256 x 50,000 requests) under the adaptive-gamma,
+    design-phase and cache-aware settings grids (the last with seeded
+    prefix-cache hits), in the launch `bench.py --grid` times (the
     extended kernel build, its default list size): every instance TAS_OK, and
     all eight settings of the first and the last trace exactly equal to the
     oracle, final adaptive gamma bit for bit."""

@@ -72,7 +72,8 @@ def test_hand_worked_on_gpu(torch, case):
                   signal=case.get("signal", 0))
     w = W.Workload(case["name"], np.array([case["arrival"]], np.int64),
                    np.array([case["prompt"]], np.int32), np.array([case["decode"]], np.int32),
-                   e, np.stack([s]))
+                   e, np.stack([s]),
+                   cached=np.array([case["cached"]], np.int32) if "cached" in case else None)
     g = gpu_run(w)
     assert g["rc"] == 0
     assert g["ttft"][0].tolist() == case["ttft"]

@@ -21,14 +21,17 @@ def blocks(x, bs):
     return -(-x // bs)
 
 
-def sig_of(r, p, dec, signal):
-    """The boost signal: P + dec, or (signal 1) P in prefill and dec in decode."""
+def sig_of(r, p, dec, signal, h=None):
+    """The boost signal: P + dec, or (signal 1) P in prefill and dec in decode,
+    or (signal 2) P - h + dec with h the expected cached prompt tokens."""
     if signal == 1:
         return int(p[r]) if dec[r] == 0 else int(dec[r])
+    if signal == 2:
+        return int(p[r]) - int(h[r]) + int(dec[r])
     return int(p[r] + dec[r])
 
 
-def key_of(policy, r, a, p, d, kv, dec, k, table, signal=0, t_first=None):
+def key_of(policy, r, a, p, d, kv, dec, k, table, signal=0, t_first=None, h=None):
     """Iteration-start priority key of request r (lower is served first)."""
     if policy == 0:
         return int(a[r])  # FCFS: arrival
@@ -45,11 +48,11 @@ def key_of(policy, r, a, p, d, kv, dec, k, table, signal=0, t_first=None):
             return (0, int(t_first[r]))
         lvl = min(23, (max(int(p[r]), k) // k).bit_length() - 1)
         return (1, int(a[r]) - int(table[lvl]))
-    lvl = min(23, (max(sig_of(r, p, dec, signal), k) // k).bit_length() - 1)
+    lvl = min(23, (max(sig_of(r, p, dec, signal, h), k) // k).bit_length() - 1)
     return int(a[r]) - int(table[lvl])  # boost: a - b(quantized signal)
 
 
-def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_us=0):
+def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_us=0, h=None):
     N = len(a)
     bs = e.block_tokens
     kv = np.zeros(N, np.int64)
@@ -80,10 +83,10 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_u
         row += nb
         # iteration-start keys of every active request
         active = [r for r in range(N) if a[r] <= t0 and not done[r]]
-        key0 = {r: key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first) for r in active}
+        key0 = {r: key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first, h) for r in active}
 
         def eligible(x):  # may be a voluntary victim (MemGuard, TRAIL threshold)
-            if memguard and not oracle.level(sig_of(x, p, dec, signal), k) > guard[x]:
+            if memguard and not oracle.level(sig_of(x, p, dec, signal, h), k) > guard[x]:
                 return False
             return not (policy == 6 and 5 * dec[x] >= 3 * d[x])
 
@@ -129,7 +132,7 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_u
         # formation takes candidates in ascending (key, idx) order of the
         # iteration-start keys (batch members were not evicted, so their kv is
         # still the iteration-start value)
-        keys = [(key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first), r)
+        keys = [(key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first, h), r)
                 for r in members]
         assert keys == sorted(keys)
         assert not (set(members) & evicted)
@@ -137,7 +140,7 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_u
             assert a[r] <= t0 and not done[r]
             assert kv[r] < p[r] + dec[r]
             if kv[r] == 0:
-                guard[r] = oracle.level(sig_of(r, p, dec, signal), k)
+                guard[r] = oracle.level(sig_of(r, p, dec, signal, h), k)
                 if r not in first_dispatch:
                     first_dispatch.append(r)
         # no request may wait while the batch still has room (stop rule), except
@@ -155,13 +158,13 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_u
                 waiting = [w for w in range(N) if a[w] <= t0 and not done[w] and kv[w] == 0
                            and w not in members and w not in evicted]
                 def eligible(v):
-                    if memguard and not oracle.level(sig_of(v, p, dec, signal), k) > guard[v]:
+                    if memguard and not oracle.level(sig_of(v, p, dec, signal, h), k) > guard[v]:
                         return False
                     return not (policy == 6 and 5 * dec[v] >= 3 * d[v])
                 for w in waiting:
-                    kw = key_of(policy, w, a, p, d, kv, dec, k, table, signal, t_first)
+                    kw = key_of(policy, w, a, p, d, kv, dec, k, table, signal, t_first, h)
                     for v in outside:
-                        kvv = key_of(policy, v, a, p, d, kv, dec, k, table, signal, t_first)
+                        kvv = key_of(policy, v, a, p, d, kv, dec, k, table, signal, t_first, h)
                         worse = ((kvv, v) > (kw, w)) if isinstance(kvv, tuple) else \
                             ((kvv - delta_us, v) > (kw, w))
                         assert not (worse and eligible(v)), (i, w, v)
@@ -205,9 +208,10 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_u
     assert np.all(o["ttlt"].astype(np.int64) - o["ttft"] >= (d.astype(np.int64) - 1) * e.iter_base_us)
     if policy == 0:  # I7 FCFS dispatches in arrival order
         assert first_dispatch == sorted(first_dispatch)
-    if memguard and signal == 0:  # Phase 3 revision bound per request (monotone signal)
+    if memguard and signal in (0, 2):  # Phase 3 revision bound per request (monotone signal)
+        hh = np.zeros(N, np.int64) if h is None else np.asarray(h, np.int64)
         for r in range(N):
-            bound = 1 + math.floor(math.log2(max(int(p[r] + d[r]), k) / k))
+            bound = 1 + math.floor(math.log2(max(int(p[r] + d[r] - hh[r]), k) / k))
             assert vol_per_req[r] <= bound
     return dict(first_dispatch=first_dispatch, vol=vol_per_req)
 
@@ -231,6 +235,8 @@ POLICIES = [
     dict(policy=7, k=16, gamma=3e-2),
     dict(policy=2, k=16, memguard=1, delta_us=20000, gamma=1e-3, signal=1),  # phase-aware signal
     dict(policy=2, k=1, memguard=0, delta_us=0, gamma=3e-2, signal=1),
+    dict(policy=2, k=16, memguard=1, delta_us=20000, gamma=1e-3, signal=2),  # cache-aware signal
+    dict(policy=2, k=1, memguard=0, delta_us=0, gamma=3e-2, signal=2),
 ]
 
 
@@ -241,14 +247,16 @@ def test_replay_invariants(seed, ei, pi):
     e = ENGINES[ei]
     pol = POLICIES[pi]
     a, p, d = W.small_random(seed * 10 + ei, 160, rate_per_s=60.0, p_max=400, d_max=200)
+    h = W.cached_tokens([seed, ei], p, share=0.6, new_median=8.0) if pol.get("signal") == 2 \
+        else None
     o = oracle.log(a, p, d, e, pol["policy"], k=pol.get("k", 1), memguard=pol.get("memguard", 0),
                    delta_us=pol.get("delta_us", 0), gamma=pol.get("gamma"),
-                   signal=pol.get("signal", 0))
+                   signal=pol.get("signal", 0), cached=h)
     assert o["rc"] == 0
     table = (oracle.boost_table(pol["gamma"], pol.get("k", 1), e.tau_us)
              if pol["policy"] in (2, 7) else None)
     replay(a, p, d, e, o, pol["policy"], k=pol.get("k", 1), memguard=pol.get("memguard", 0),
-           table=table, signal=pol.get("signal", 0), delta_us=pol.get("delta_us", 0))
+           table=table, signal=pol.get("signal", 0), delta_us=pol.get("delta_us", 0), h=h)
 
 
 def test_replay_sees_evictions():
