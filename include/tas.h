@@ -35,6 +35,13 @@
  *                  it, in the decode queue, key t_first - 2^42, so the decode
  *                  queue in order of entry fills the batch first and prefill
  *                  chunks fill the rest
+ *       TAS_SARATHI decode-prioritized continuous batching with round-robin
+ *                  decodes and piggy-backed prefill chunks (the evaluation's
+ *                  baselines, Sarathi): key a_i before the first token, then
+ *                  t_last - 2^42 with t_last the time of the request's latest
+ *                  token, so decodes rotate (longest unserved first) ahead of
+ *                  prefills in arrival order; a waiting request never evicts a
+ *                  resident (only a resident that cannot grow forces one out)
  *   - a greedy pass fills the batch under a sequence cap, a token budget and a
  *     KV-block budget, evicting (recompute preemption) the worst resident when
  *     KV runs out; MemGuard and the hysteresis delta restrict voluntary
@@ -100,7 +107,7 @@ enum {
 };
 
 enum { TAS_FCFS = 0, TAS_SRPT = 1, TAS_BOOST = 2, TAS_SPF = 3, TAS_SJF = 4, TAS_LAS = 5,
-       TAS_TRAIL = 6, TAS_DIST = 7 };
+       TAS_TRAIL = 6, TAS_DIST = 7, TAS_SARATHI = 8 };
 
 #define TAS_LEVELS 24
 
@@ -120,7 +127,7 @@ typedef struct {
 /* One instance: a trace and a policy setting. */
 typedef struct {
     int32_t trace;    /* index into the traces                                 */
-    int32_t policy;   /* one of the TAS_FCFS .. TAS_DIST policies above        */
+    int32_t policy;   /* one of the TAS_FCFS .. TAS_SARATHI policies above     */
     int32_t k;        /* MemGuard granularity in tokens (BOOST, DIST), >= 1    */
     int32_t memguard; /* 1: a dispatched request is non-evictable until its
                          level passes the level it was dispatched at (BOOST)  */

@@ -51,6 +51,15 @@
  *   TRAIL SRPT with perfect knowledge plus the swap-prevention threshold: a
  *         resident that has emitted at least 0.6 D tokens is never a voluntary
  *         victim (5 dec >= 3 D)
+ *   SARATHI decode-prioritized continuous batching with round-robin decodes
+ *         and piggy-backed prefill chunks: a request in its prefill waits in
+ *         arrival order (key = a); once it has emitted a token it is in the
+ *         decode queue, ordered by the time of its latest token (the request
+ *         served longest ago goes first), below every prefill key:
+ *         key = t_last - 2^42. Waiting requests never preempt running ones:
+ *         no voluntary victims, only the forced eviction of a resident that
+ *         cannot grow (the worst other resident, i.e. the latest prefill or
+ *         the most recently served decode, else itself)
  *
  * Phase ladder (paper: Phase 1 DistBoost; Algorithm 2 Signal):
  *   DIST  DistBoost: two queues. A request in its prefill (no token emitted
@@ -93,7 +102,7 @@
 
 enum { PENDING = 0, WAITING = 1, RESIDENT = 2, DONE = 3 };
 enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2, P_SPF = 3, P_SJF = 4, P_LAS = 5, P_TRAIL = 6,
-       P_DIST = 7 };
+       P_DIST = 7, P_SARATHI = 8 };
 #define DECODE_QUEUE_OFFSET ((int64_t)1 << 42) /* decode-queue keys lie below every prefill key */
 
 #define ADA_GRID_MAX 64
@@ -206,6 +215,9 @@ static int64_t key_of(const inst_t *I, int32_t r, const req_t *q) {
     case P_DIST:
         if (q->dec > 0) return q->t_first - DECODE_QUEUE_OFFSET; /* decode queue */
         return I->a[r] - I->bt[level_of(I->P[r], I->k)];         /* prefill queue */
+    case P_SARATHI:
+        if (q->dec > 0) return q->t_last - DECODE_QUEUE_OFFSET; /* round robin */
+        return I->a[r];                                         /* arrival order */
     default:
         return I->a[r] - I->bt[level_of(signal_of(I, r, q), I->k)];
     }
@@ -396,6 +408,7 @@ static int simulate(const inst_t *I0, uint32_t *ttft, uint32_t *ttlt, uint32_t *
                         continue;
                     if (I->policy == P_TRAIL && 5 * (int64_t)p->dec >= 3 * (int64_t)I->D[x])
                         continue; /* past the swap-prevention threshold */
+                    if (I->policy == P_SARATHI) continue; /* no preemption by priority */
                     if (!lex_gt(p->key - I->delta, x, q->key, r)) continue;
                     if (v < 0 || lex_gt(p->key, x, R[v].key, v)) v = x;
                 }
@@ -643,7 +656,7 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
                    int64_t *switch_out, int32_t n_threads) {
     if (n_traces < 1 || n_req < 1 || n_inst < 0) return TOR_EINVAL;
     for (int32_t i = 0; i < n_inst; i++) {
-        if (trace[i] < 0 || trace[i] >= n_traces || policy[i] < 0 || policy[i] > 7 || k[i] < 1)
+        if (trace[i] < 0 || trace[i] >= n_traces || policy[i] < 0 || policy[i] > 8 || k[i] < 1)
             return TOR_EINVAL;
         if (signal && signal[i] != 0 &&
             (signal[i] < 1 || signal[i] > 2 || policy[i] != P_BOOST || (signal[i] == 2 && !cached)))
@@ -681,7 +694,7 @@ int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
                    uint32_t *tbtmax, int64_t *counters, int64_t *log_iter, int64_t iter_cap,
                    int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
                    int64_t evict_cap, int64_t *n_iter, int64_t *n_batch, int64_t *n_evict) {
-    if (policy < 0 || policy > 7 ||
+    if (policy < 0 || policy > 8 ||
         (signal != 0 && (signal < 1 || signal > 2 || policy != P_BOOST || (signal == 2 && !cached))))
         return TOR_EINVAL;
     inst_t I;

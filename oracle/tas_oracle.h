@@ -18,7 +18,7 @@
  *   cached [n_traces*n_req] int32 expected prefix-cache hit tokens, 0 <= h < P,
  *   or NULL (needed only by signal 2)
  *   per instance i: trace[i], policy[i] (0 FCFS, 1 SRPT, 2 BOOST, 3 SPF,
- *   4 SJF, 5 LAS, 6 TRAIL, 7 DIST), k[i] >= 1,
+ *   4 SJF, 5 LAS, 6 TRAIL, 7 DIST, 8 SARATHI), k[i] >= 1,
  *   memguard[i] in {0,1}, delta[i] >= 0 us, table[i*24 .. i*24+23] int64 us
  *   eng[8] = {max_seqs, max_tokens, chunk, kv_blocks, block_tokens,
  *             iter_base_us, iter_tok_us, iter_ctx_div}

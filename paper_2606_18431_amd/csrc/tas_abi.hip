@@ -144,7 +144,7 @@ int check_setting(const tas_setting &s, int32_t n_traces, double tau_us, bool ha
     if (s.ada != 0 && (s.ada != 1 || !ada_ok(s))) return TAS_EINVAL;
     if (s.signal != 0 && (s.signal < 1 || s.signal > 2 || s.policy != TAS_BOOST)) return TAS_EINVAL;
     if (s.signal == 2 && !has_cached) return TAS_EINVAL;
-    if (s.policy < TAS_FCFS || s.policy > TAS_DIST) return TAS_EINVAL;
+    if (s.policy < TAS_FCFS || s.policy > TAS_SARATHI) return TAS_EINVAL;
     if (s.delta_us < 0) return TAS_EINVAL;
     const bool boosted = s.policy == TAS_BOOST || s.policy == TAS_DIST;
     if (s.policy != TAS_BOOST) {
@@ -261,7 +261,7 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
         d.delta = s.policy == TAS_BOOST ? s.delta_us : 0;
         d.ada = -1;
         d.signal = s.signal;
-        if (s.signal || s.policy == TAS_DIST) ext = true;
+        if (s.signal || s.policy == TAS_DIST || s.policy == TAS_SARATHI) ext = true;
         if (boosted) {
             if (s.table_given) std::memcpy(d.bt, s.boost_us, sizeof d.bt);
             else tas_boost_table(s.gamma, s.k, p->tau_us, d.bt);

@@ -65,7 +65,7 @@ enum { S_OK = 0, S_EOVERFLOW = -5, S_ELIVELOCK = -6, S_ESTATE = -7, S_ECAPACITY 
 // SRPT with TRAIL's swap-prevention threshold (TRAIL); and the Phase 1
 // strawman DistBoost (DIST).
 enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2, P_SPF = 3, P_SJF = 4, P_LAS = 5, P_TRAIL = 6,
-       P_DIST = 7 };
+       P_DIST = 7, P_SARATHI = 8 };
 // DistBoost ranks its decode queue (key: the time a request entered it, its
 // first-token time) ahead of its prefill queue: decode keys are shifted down
 // by 2^42, below every prefill key a - bt (boost tables are capped at 2^40).
@@ -423,8 +423,8 @@ struct Sim {
         x.w = P, x.left = D;
         int64_t key;
         uint32_t lvl = 0;
-        if (pol == P_FCFS) {
-            key = a;
+        if (pol == P_FCFS || (EXT && pol == P_SARATHI)) {
+            key = a;  // Sarathi: prefills wait in arrival order
         } else if (pol == P_SRPT || pol == P_TRAIL) {
             key = (int64_t)P + D - 1;  // remaining computed tokens
         } else if (pol == P_SPF || pol == P_LAS) {
@@ -760,6 +760,9 @@ struct Sim {
     // evicted for candidate q (voluntary: MemGuard and hysteresis apply).
     // The list is sorted, so the highest such rank is the worst (key, idx).
     DEV int find_victim(int q, bool voluntary) {
+        if constexpr (EXT) {
+            if (voluntary && pol == P_SARATHI) return -1;  // no preemption by priority
+        }
         if (UNLIKELY(!vm_ok)) build_victim_masks();
         const int v = top_above(voluntary ? vm_ev : vm_res, q);
         if (voluntary && v >= 0 && delta > 0) {
@@ -1034,6 +1037,11 @@ struct Sim {
                     } else if (pol == P_LAS) {
                         // the attained service grew by one token
                         pk = pack((int64_t)w, idx);
+                        gs |= G_DIRTY;
+                        chg = true;
+                    } else if (EXT && pol == P_SARATHI) {
+                        // round robin: back of the decode queue after each token
+                        pk = pack(t_end - kDecodeQueueOff, idx);
                         gs |= G_DIRTY;
                         chg = true;
                     } else if (pol == P_BOOST) {
@@ -1402,7 +1410,7 @@ DEV void run_instance(const SimArgs &a, const DevSetting &st, int inst, unsigned
 }
 
 // EXT: the extended build (adaptive gamma, the phase-aware and cache-aware signals,
-// DistBoost), launched when some instance uses one of them (its extra state
+// DistBoost, Sarathi), launched when some instance uses one of them (its extra state
 // and code cost the other policies registers).
 template <bool EXT>
 __global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {

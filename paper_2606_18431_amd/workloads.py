@@ -21,8 +21,8 @@ Five workloads are defined (``make(cfg)``):
 The policy-parameter grid per trace: setting 0 = FCFS, setting 1 = oracle-length
 SRPT, then pairs (UniBoost with MemGuard, vanilla boost) over log-spaced gamma.
 ``make(cfg, grid="comparators")`` instead runs every trace under the paper's
-comparison policies (FCFS, SRPT, SPF, SJF, LAS, TRAIL) beside UniBoost and vanilla
-boost; ``make(cfg, grid="ada")`` runs fixed against adaptive gamma (Phase 4);
+comparison policies (FCFS, SRPT, SPF, SJF, LAS, TRAIL, Sarathi) beside UniBoost
+and vanilla boost; ``make(cfg, grid="ada")`` runs fixed against adaptive gamma (Phase 4);
 ``make(cfg, grid="ladder")`` runs the paper's design phases (DistBoost to the
 full UniBoost) and the phase-aware signal.
 """
@@ -33,9 +33,9 @@ import math
 
 import numpy as np
 
-FCFS, SRPT, BOOST, SPF, SJF, LAS, TRAIL, DIST = 0, 1, 2, 3, 4, 5, 6, 7
+FCFS, SRPT, BOOST, SPF, SJF, LAS, TRAIL, DIST, SARATHI = 0, 1, 2, 3, 4, 5, 6, 7, 8
 POLICY_NAMES = {FCFS: "fcfs", SRPT: "srpt", BOOST: "boost", SPF: "spf", SJF: "sjf", LAS: "las",
-                TRAIL: "trail", DIST: "distboost"}
+                TRAIL: "trail", DIST: "distboost", SARATHI: "sarathi"}
 LEVELS = 24
 
 # One numpy record per instance; field order mirrors the C struct tas_setting.
@@ -166,11 +166,11 @@ def settings_grid(n_traces: int, n_settings: int) -> np.ndarray:
 
 
 def comparator_settings(n_traces: int, gamma: float = 1e-3) -> np.ndarray:
-    """Per trace, 8 settings: FCFS, SRPT, SPF, SJF, LAS, TRAIL, then UniBoost and
-    vanilla boost at one gamma. Instance id = trace * 8 + s."""
+    """Per trace, 9 settings: FCFS, SRPT, SPF, SJF, LAS, TRAIL, then UniBoost and
+    vanilla boost at one gamma, then Sarathi. Instance id = trace * 9 + s."""
     per = [dict(policy=FCFS), dict(policy=SRPT), dict(policy=SPF), dict(policy=SJF),
            dict(policy=LAS), dict(policy=TRAIL), dict(policy=BOOST, gamma=gamma, **UNIBOOST),
-           dict(policy=BOOST, gamma=gamma, **VANILLA)]
+           dict(policy=BOOST, gamma=gamma, **VANILLA), dict(policy=SARATHI)]
     out = np.zeros(n_traces * len(per), dtype=SETTING_DTYPE)
     for t in range(n_traces):
         for s, kw in enumerate(per):
@@ -412,7 +412,7 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
         arr[t], pr[t], de[t] = _trace(cfg, t, N, eng)
     if grid == "comparators":
         sets = comparator_settings(T)
-        S = 8
+        S = 9
     elif grid == "ada":
         sets = ada_settings(T)
         S = 8

@@ -182,7 +182,8 @@ def test_rejects_invalid_settings():
     w = small()
     cases = []
     s = w.settings.copy(); s[0]["trace"] = 5; cases.append(s)
-    s = w.settings.copy(); s[0]["policy"] = 7; cases.append(s)           # unknown policy
+    s = w.settings.copy(); s[0]["policy"] = 9; cases.append(s)           # unknown policy
+    s = w.settings.copy(); s[0]["policy"] = 8; s[0]["memguard"] = 1; cases.append(s)  # Sarathi
     s = w.settings.copy(); s[0]["policy"] = -1; cases.append(s)
     s = w.settings.copy(); s[0]["policy"] = 5; s[0]["memguard"] = 1; cases.append(s)  # LAS + MemGuard
     s = w.settings.copy(); s[1]["policy"] = 6; s[1]["delta_us"] = 5; cases.append(s)  # TRAIL + delta

@@ -90,15 +90,17 @@ def test_phase_variants_smallest_list(torch, cfg, cap):
 
 def test_one_request_every_policy(torch):
     e = W.Engine()
-    sets = [W.setting(0, p) for p in (W.FCFS, W.SRPT, W.SPF, W.SJF, W.LAS, W.TRAIL)]
+    sets = [W.setting(0, p) for p in (W.FCFS, W.SRPT, W.SPF, W.SJF, W.LAS, W.TRAIL, W.SARATHI)]
     sets += [W.setting(0, W.BOOST, gamma=1e-3, **W.UNIBOOST),
              W.setting(0, W.DIST, gamma=1e-3),
              W.setting(0, W.BOOST, gamma=1e-3, signal=1, **W.UNIBOOST),
              W.setting(0, W.BOOST, gamma=1e-3, ada=dict(W.ADA, window=1, min_samples=1),
-                       **W.UNIBOOST)]
+                       **W.UNIBOOST),
+            W.setting(0, W.BOOST, gamma=1e-3, signal=2, **W.UNIBOOST)]
     for P, D in ((1, 1), (5000, 3), (16, 700)):
         w = W.Workload(f"one request P={P} D={D}", np.array([[123]], np.int64),
-                       np.array([[P]], np.int32), np.array([[D]], np.int32), e, np.stack(sets))
+                       np.array([[P]], np.int32), np.array([[D]], np.int32), e, np.stack(sets),
+                       cached=np.array([[P - 1]], np.int32))
         g = gpu_run(w)
         o = oracle.run(w)
         assert_parity(g, o)

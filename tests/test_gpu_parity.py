@@ -181,7 +181,11 @@ def edge_workload(arrival, prompt, decode, engine, policies=None):
     sets = policies or [W.setting(0, W.FCFS), W.setting(0, W.SRPT),
                         W.setting(0, W.BOOST, gamma=1e-3, **W.UNIBOOST),
                         W.setting(0, W.BOOST, gamma=1e-3, **W.VANILLA)]
-    return W.Workload("edge", a, p, d, engine, np.stack(sets))
+    # expected prefix-cache hits for the cache-aware signal: a seeded draw
+    # that keeps at least one prompt token of work
+    h = W.cached_tokens(len(a[0]), p[0], share=0.7, new_median=4.0)[None] \
+        if any(s["signal"] == 2 for s in sets) else None
+    return W.Workload("edge", a, p, d, engine, np.stack(sets), cached=h)
 
 
 EDGES = {
@@ -211,15 +215,16 @@ EXTENDED = [W.setting(0, W.SPF), W.setting(0, W.SJF), W.setting(0, W.LAS), W.set
             W.setting(0, W.DIST, gamma=1e-3),
             W.setting(0, W.BOOST, gamma=1e-3, signal=1, **W.UNIBOOST),
             W.setting(0, W.BOOST, gamma=1e-3, ada=dict(W.ADA, window=8, min_samples=4),
-                      **W.UNIBOOST)]
+                      **W.UNIBOOST),
+            W.setting(0, W.SARATHI), W.setting(0, W.BOOST, gamma=1e-3, signal=2, **W.UNIBOOST)]
 
 
 @pytest.mark.parametrize("extended", [False, True], ids=["base", "extended"])
 @pytest.mark.parametrize("name", sorted(EDGES))
 def test_edge_cases(torch, name, extended):
     """Each case under the base policies (fixed kernel build) and under the
-    comparators, DistBoost, the phase-aware signal and adaptive gamma (the
-    extended build)."""
+    comparators, DistBoost, Sarathi, the phase-aware and cache-aware signals
+    and adaptive gamma (the extended build)."""
     a, p, d, e = EDGES[name]
     w = edge_workload(a, p, d, e, EXTENDED if extended else None)
     o = oracle.run(w)

@@ -129,10 +129,11 @@ def test_trail_never_preempts_past_threshold():
 @pytest.mark.parametrize("policy,blind,kw", [
     (SPF, True, {}), (LAS, True, {}), (SJF, False, {}),
     (W.DIST, True, dict(k=1, gamma=1e-3)), (W.DIST, True, dict(k=16, gamma=3e-2)),
-    (W.BOOST, True, dict(k=16, memguard=1, delta_us=20000, gamma=1e-3, signal=1))])
+    (W.BOOST, True, dict(k=16, memguard=1, delta_us=20000, gamma=1e-3, signal=1)),
+    (W.SARATHI, True, {})])
 def test_blindness(policy, blind, kw):
-    """SPF, LAS, DistBoost and the boost with the phase-aware signal use no
-    knowledge of the output length (prediction-free): lengthening one
+    """SPF, LAS, DistBoost, Sarathi and the boost with the phase-aware signal
+    use no knowledge of the output length (prediction-free): lengthening one
     request's decode leaves every event before its original completion
     unchanged. SJF reads the length."""
     changed = 0
@@ -155,3 +156,27 @@ def test_blindness(policy, blind, kw):
     if not blind:
         assert changed > 0
 
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_sarathi_is_distboost_without_contention(seed):
+    """With the batch cap above the number of requests and KV to spare, every
+    decode is in every batch, so the order inside the decode queue (latest
+    token for Sarathi, first token for DistBoost) cannot matter: Sarathi
+    equals DistBoost with a zero boost table (prefills in arrival order),
+    bit for bit. Under contention (M = 8, KV pressure) they differ, and
+    Sarathi differs from FCFS (evicted decodes return ahead of prefills)."""
+    a, p, d = W.small_random(seed, 150, rate_per_s=40.0)
+    e = engine(max_seqs=256, kv_blocks=100000, chunk=128, max_tokens=4096)
+    zero = np.zeros(24, np.int64)
+    s = oracle.log(a, p, d, e, W.SARATHI)
+    t = oracle.log(a, p, d, e, W.DIST, table=zero)
+    assert s["rc"] == 0 and t["rc"] == 0
+    for key in ("ttft", "ttlt", "tbtmax", "counters"):
+        assert np.array_equal(s[key], t[key]), key
+    e2 = engine(max_seqs=8, kv_blocks=60, chunk=128, max_tokens=4096)
+    s2 = oracle.log(a, p, d, e2, W.SARATHI)
+    t2 = oracle.log(a, p, d, e2, W.DIST, table=zero)
+    f2 = oracle.log(a, p, d, e2, FCFS)
+    assert not np.array_equal(s2["ttlt"], t2["ttlt"])
+    assert not np.array_equal(s2["ttlt"], f2["ttlt"])

@@ -31,7 +31,8 @@ def sig_of(r, p, dec, signal, h=None):
     return int(p[r] + dec[r])
 
 
-def key_of(policy, r, a, p, d, kv, dec, k, table, signal=0, t_first=None, h=None):
+def key_of(policy, r, a, p, d, kv, dec, k, table, signal=0, t_first=None, h=None,
+           t_last=None):
     """Iteration-start priority key of request r (lower is served first)."""
     if policy == 0:
         return int(a[r])  # FCFS: arrival
@@ -48,6 +49,8 @@ def key_of(policy, r, a, p, d, kv, dec, k, table, signal=0, t_first=None, h=None
             return (0, int(t_first[r]))
         lvl = min(23, (max(int(p[r]), k) // k).bit_length() - 1)
         return (1, int(a[r]) - int(table[lvl]))
+    if policy == 8:  # Sarathi: decodes by their latest token time, then prefills by arrival
+        return (0, int(t_last[r])) if dec[r] > 0 else (1, int(a[r]))
     lvl = min(23, (max(sig_of(r, p, dec, signal, h), k) // k).bit_length() - 1)
     return int(a[r]) - int(table[lvl])  # boost: a - b(quantized signal)
 
@@ -83,9 +86,12 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_u
         row += nb
         # iteration-start keys of every active request
         active = [r for r in range(N) if a[r] <= t0 and not done[r]]
-        key0 = {r: key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first, h) for r in active}
+        key0 = {r: key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first, h, t_last)
+                for r in active}
 
         def eligible(x):  # may be a voluntary victim (MemGuard, TRAIL threshold)
+            if policy == 8:  # Sarathi: waiting requests never preempt residents
+                return False
             if memguard and not oracle.level(sig_of(x, p, dec, signal, h), k) > guard[x]:
                 return False
             return not (policy == 6 and 5 * dec[x] >= 3 * d[x])
@@ -132,7 +138,7 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_u
         # formation takes candidates in ascending (key, idx) order of the
         # iteration-start keys (batch members were not evicted, so their kv is
         # still the iteration-start value)
-        keys = [(key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first, h), r)
+        keys = [(key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first, h, t_last), r)
                 for r in members]
         assert keys == sorted(keys)
         assert not (set(members) & evicted)
@@ -162,9 +168,10 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_u
                         return False
                     return not (policy == 6 and 5 * dec[v] >= 3 * d[v])
                 for w in waiting:
-                    kw = key_of(policy, w, a, p, d, kv, dec, k, table, signal, t_first, h)
+                    kw = key_of(policy, w, a, p, d, kv, dec, k, table, signal, t_first, h, t_last)
                     for v in outside:
-                        kvv = key_of(policy, v, a, p, d, kv, dec, k, table, signal, t_first, h)
+                        kvv = key_of(policy, v, a, p, d, kv, dec, k, table, signal, t_first, h,
+                                     t_last)
                         worse = ((kvv, v) > (kw, w)) if isinstance(kvv, tuple) else \
                             ((kvv - delta_us, v) > (kw, w))
                         assert not (worse and eligible(v)), (i, w, v)
@@ -237,6 +244,7 @@ POLICIES = [
     dict(policy=2, k=1, memguard=0, delta_us=0, gamma=3e-2, signal=1),
     dict(policy=2, k=16, memguard=1, delta_us=20000, gamma=1e-3, signal=2),  # cache-aware signal
     dict(policy=2, k=1, memguard=0, delta_us=0, gamma=3e-2, signal=2),
+    dict(policy=8),  # Sarathi
 ]
 
 
