@@ -54,6 +54,9 @@ def lib():
         L.tas_oracle_run.restype = ctypes.c_int
         L.tas_oracle_log.argtypes = [i32, P, P, P, P, i32, i32, i32, i64, P, P, i32, P, i64, P,
                                      P, P, P, P, i64, P, i64, P, i64, P, P, P]
+        L.tas_oracle_jsq.argtypes = [i32, P, P, P, P, i32, i32, i32, i32, i64, P, P, i32, P,
+                                     i64, P, P, P, P, P, P, P]
+        L.tas_oracle_jsq.restype = ctypes.c_int
         L.tas_oracle_ada_grid.argtypes = [P, i32, P, P, P]
         L.tas_oracle_ada_grid.restype = ctypes.c_int
         L.tas_oracle_log.restype = ctypes.c_int
@@ -238,3 +241,53 @@ def group_percentiles(out, group: int) -> np.ndarray:
 def percentile(values: np.ndarray, q: int) -> int:
     v = np.ascontiguousarray(values, np.uint32)
     return int(lib().tas_oracle_percentile(_p(v), len(v), int(q)))
+
+
+def jsq(w, replicas: int, n_threads: int | None = None, max_iters: int | None = None):
+    """Every instance of workload ``w`` as a cluster of ``replicas`` replicas
+    behind a join-shortest-queue router over the instance's trace (see
+    tas_oracle_jsq). Returns ttft/ttlt/tbtmax and assign [n_inst, n_req],
+    counters [n_inst, replicas, 8], gamma and switches [n_inst, replicas],
+    pct [n_inst, 3, 3] (nearest rank over the whole trace), status [n_inst]."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    s = w.settings
+    n_inst, n_req, R = len(s), w.n_req, int(replicas)
+    tb = np.ascontiguousarray(tables(s, w.engine.tau_us))
+    eng = _eng(w.engine)
+    mi = w.engine.max_iters if max_iters is None else max_iters
+    out = dict(ttft=np.zeros((n_inst, n_req), np.uint32), ttlt=np.zeros((n_inst, n_req), np.uint32),
+               tbtmax=np.zeros((n_inst, n_req), np.uint32),
+               assign=np.zeros((n_inst, n_req), np.int32),
+               counters=np.zeros((n_inst, R, 8), np.int64), gamma=np.zeros((n_inst, R)),
+               switches=np.zeros((n_inst, R), np.int64), pct=np.zeros((n_inst, 3, 3), np.uint32),
+               status=np.zeros(n_inst, np.int32))
+
+    def one(i):
+        t = int(s[i]["trace"])
+        arr = np.ascontiguousarray(w.arrival_us[t], np.int64)
+        pr = np.ascontiguousarray(w.prompt[t], np.int32)
+        de = np.ascontiguousarray(w.decode[t], np.int32)
+        ch = None if w.cached is None else np.ascontiguousarray(w.cached[t], np.int32)
+        prm = np.ascontiguousarray(ada_params(s[i], w.engine.tau_us), np.float64)
+        bufs = [np.zeros(n_req, np.uint32) for _ in range(3)] + [np.zeros(n_req, np.int32),
+                                                                  np.zeros((R, 8), np.int64),
+                                                                  np.zeros(R), np.zeros(R, np.int64)]
+        rc = lib().tas_oracle_jsq(n_req, _p(arr), _p(pr), _p(de), None if ch is None else _p(ch),
+                                  R, int(s[i]["policy"]), int(s[i]["k"]), int(s[i]["memguard"]),
+                                  int(s[i]["delta_us"]), _p(tb[i]), _p(prm), int(s[i]["signal"]),
+                                  _p(eng), int(mi), *[_p(b) for b in bufs])
+        out["status"][i] = rc
+        if rc == 0:
+            for key, b in zip(("ttft", "ttlt", "tbtmax", "assign", "counters", "gamma",
+                               "switches"), bufs):
+                out[key][i] = b
+            for m, key in enumerate(("ttft", "ttlt", "tbtmax")):
+                for j, q in enumerate((50, 90, 99)):
+                    out["pct"][i, m, j] = percentile(bufs[m], q)
+
+    nt = max(1, min(n_threads or os.cpu_count() or 1, n_inst))
+    with ThreadPoolExecutor(nt) as ex:
+        list(ex.map(one, range(n_inst)))
+    out["rc"] = int(next((x for x in out["status"] if x), 0))
+    return out

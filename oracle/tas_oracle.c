@@ -719,3 +719,133 @@ int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
     if (lg.full) return TOR_EINVAL;
     return st;
 }
+
+/* ------------------------------------------------------------ JSQ cluster */
+
+/* Replicas behind a join-shortest-queue router (paper: composability with
+ * global dispatch policies). Request j of the global trace goes, at its
+ * arrival a_j, to the replica holding the fewest requests at that moment
+ * (dispatched to it and not completed by a_j; ties to the lowest replica),
+ * each replica scheduling its own requests as one instance.
+ *
+ * The schedule of a replica up to time a_j depends only on the requests it
+ * received before j (they arrive no later than a_j, and an iteration that
+ * starts before a_j is formed before request j exists). So the count at a_j
+ * is read from a full simulation of the replica over the requests it holds
+ * so far: those whose completion time a + TTLT exceeds a_j are still there.
+ * Only the replica that receives j changes, so it alone is simulated again. */
+int tas_oracle_jsq(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
+                   const int32_t *decode, const int32_t *cached, int32_t replicas,
+                   int32_t policy, int32_t k, int32_t memguard, int64_t delta,
+                   const int64_t *table, const double *ada, int32_t signal, const int32_t *eng,
+                   int64_t max_iters, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
+                   int32_t *assign, int64_t *counters, double *gamma_out, int64_t *switch_out) {
+    if (n_req < 1 || replicas < 1 || policy < 0 || policy > 8 || k < 1 ||
+        (signal != 0 && (signal < 1 || signal > 2 || policy != P_BOOST || (signal == 2 && !cached))))
+        return TOR_EINVAL;
+    for (int32_t j = 1; j < n_req; j++)
+        if (arrival[j] < arrival[j - 1]) return TOR_EINVAL;
+    const int32_t R = replicas;
+    ada_t *A = NULL;
+    if (ada && ada[0] != 0.0) {
+        A = (ada_t *)malloc(sizeof *A);
+        int rc = A ? ada_setup(A, ada, policy, k) : TOR_EINVAL;
+        if (rc) {
+            free(A);
+            return rc;
+        }
+    }
+    /* per replica: the global indices it holds, its gathered trace, and the
+     * outputs of its latest full simulation */
+    int32_t *cnt = (int32_t *)calloc((size_t)R, sizeof(int32_t));
+    int32_t *idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)R * (size_t)n_req);
+    int64_t *ra = (int64_t *)malloc(sizeof(int64_t) * (size_t)R * (size_t)n_req);
+    int32_t *rp = (int32_t *)malloc(sizeof(int32_t) * (size_t)R * (size_t)n_req * 3);
+    uint32_t *out = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)R * (size_t)n_req * 3);
+    int status = 0;
+    if (!cnt || !idx || !ra || !rp || !out) {
+        status = TOR_EINVAL;
+        goto done;
+    }
+    for (int32_t j = 0; j <= n_req && status == 0; j++) {
+        /* route j (skipped after the last request, which only simulates) */
+        int32_t best = -1, best_n = 0;
+        for (int32_t r = 0; r < R && j < n_req; r++) {
+            const size_t o = (size_t)r * (size_t)n_req;
+            int32_t held = 0;
+            for (int32_t m = 0; m < cnt[r]; m++)
+                held += ra[o + m] + (int64_t)out[(o + m) * 3 + 1] > arrival[j];
+            if (best < 0 || held < best_n) best = r, best_n = held;
+        }
+        for (int32_t r = 0; r < R; r++) {
+            if (j < n_req && r != best) continue;
+            if (j == n_req && cnt[r] == 0) continue;
+            const size_t o = (size_t)r * (size_t)n_req;
+            if (j < n_req) {
+                const int32_t m = cnt[r]++;
+                idx[o + m] = j;
+                ra[o + m] = arrival[j];
+                rp[(o + m) * 3] = prompt[j];
+                rp[(o + m) * 3 + 1] = decode[j];
+                rp[(o + m) * 3 + 2] = cached ? cached[j] : 0;
+                assign[j] = r;
+            }
+            /* the replica's trace as plain arrays */
+            const int32_t n = cnt[r];
+            int32_t *P = (int32_t *)malloc(sizeof(int32_t) * (size_t)n * 3);
+            uint32_t *o3 = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)n * 3);
+            if (!P || !o3) {
+                free(P);
+                free(o3);
+                status = TOR_EINVAL;
+                break;
+            }
+            for (int32_t m = 0; m < n; m++) {
+                P[m] = rp[(o + m) * 3];
+                P[n + m] = rp[(o + m) * 3 + 1];
+                P[2 * n + m] = rp[(o + m) * 3 + 2];
+            }
+            inst_t I;
+            fill_inst(&I, eng, n, ra + o, P, P + n, policy, k, memguard, delta, table, max_iters);
+            I.signal = signal;
+            I.H = cached ? P + 2 * n : NULL;
+            I.ada = A;
+            int64_t c8[8];
+            double g = 0.0;
+            int64_t sw = 0;
+            status = simulate(&I, o3, o3 + n, o3 + 2 * n, c8, &g, &sw, NULL);
+            if (status == 0) {
+                for (int32_t m = 0; m < n; m++)
+                    for (int q = 0; q < 3; q++) out[(o + m) * 3 + q] = o3[(size_t)q * n + m];
+                if (j == n_req) { /* final: outputs in global order */
+                    for (int32_t m = 0; m < n; m++) {
+                        ttft[idx[o + m]] = out[(o + m) * 3];
+                        ttlt[idx[o + m]] = out[(o + m) * 3 + 1];
+                        tbtmax[idx[o + m]] = out[(o + m) * 3 + 2];
+                    }
+                    memcpy(counters + (size_t)r * 8, c8, sizeof c8);
+                    if (gamma_out) gamma_out[r] = g;
+                    if (switch_out) switch_out[r] = sw;
+                }
+            }
+            free(P);
+            free(o3);
+            if (status) break;
+        }
+    }
+    if (status == 0)
+        for (int32_t r = 0; r < R; r++)
+            if (cnt[r] == 0) { /* a replica that received nothing */
+                memset(counters + (size_t)r * 8, 0, 8 * sizeof(int64_t));
+                if (gamma_out) gamma_out[r] = A ? A->gamma0 : 0.0;
+                if (switch_out) switch_out[r] = 0;
+            }
+done:
+    free(cnt);
+    free(idx);
+    free(ra);
+    free(rp);
+    free(out);
+    free(A);
+    return status;
+}

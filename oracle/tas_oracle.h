@@ -108,6 +108,21 @@ int32_t tas_oracle_level(int64_t w, int32_t k);
  * ceil(q*n/100) - 1. */
 uint32_t tas_oracle_percentile(const uint32_t *v, int32_t n, int32_t q);
 
+/* Replicas behind a join-shortest-queue router (paper: composability with
+ * global dispatch policies): the n_req requests of one global trace are
+ * dispatched, at their arrival and in index order, to the replica holding
+ * the fewest requests not yet completed (ties to the lowest replica); every
+ * replica runs the one setting given (policy .. signal as for
+ * tas_oracle_log; ada[10] or NULL). Outputs: ttft, ttlt, tbtmax [n_req] in
+ * global order, assign [n_req] (the replica of each request), counters
+ * [replicas*8], gamma_out and switch_out [replicas] (may be NULL). */
+int tas_oracle_jsq(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
+                   const int32_t *decode, const int32_t *cached, int32_t replicas,
+                   int32_t policy, int32_t k, int32_t memguard, int64_t delta,
+                   const int64_t *table, const double *ada, int32_t signal, const int32_t *eng,
+                   int64_t max_iters, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
+                   int32_t *assign, int64_t *counters, double *gamma_out, int64_t *switch_out);
+
 #ifdef __cplusplus
 }
 #endif

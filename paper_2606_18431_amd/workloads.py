@@ -450,7 +450,13 @@ def make_cluster(cfg: int, n_clusters: int, replicas: int, dispatch: str = "rr",
     - ``dispatch="rr"``: round robin, request i goes to replica i mod R;
     - ``dispatch="random"``: balanced random, each block of R consecutive
       requests goes to a uniformly random permutation of the replicas (the
-      assignment is drawn here, seeded, and is an input of both sides).
+      assignment is drawn here, seeded, and is an input of both sides);
+    - ``dispatch="jsq"``: join the shortest queue, decided during the
+      simulation (the replica holding the fewest unfinished requests at the
+      arrival, ties to the lowest). The workload then keeps the global traces
+      whole (trace c = cluster c, R * n_req requests) with one instance per
+      (cluster, setting); ``meta["replicas"]`` tells the simulation how many
+      replicas each instance has.
 
     Every replica receives ``n_req`` requests. Instances are ordered cluster,
     setting, replica, so the R replicas of a (cluster, setting) are R adjacent
@@ -464,6 +470,17 @@ def make_cluster(cfg: int, n_clusters: int, replicas: int, dispatch: str = "rr",
     per = settings if settings is not None else [
         dict(policy=FCFS), dict(policy=BOOST, gamma=1e-3, **UNIBOOST),
         dict(policy=BOOST, gamma=1e-3, **VANILLA)]
+    if dispatch == "jsq":
+        arr = np.empty((n_clusters, N * R), np.int64)
+        pr = np.empty((n_clusters, N * R), np.int32)
+        de = np.empty((n_clusters, N * R), np.int32)
+        for c in range(n_clusters):
+            a, p, d = _trace(cfg, c, N * R, eng)
+            arr[c], pr[c], de[c] = a // R, p, d
+        sets = np.stack([setting(c, **kw) for c in range(n_clusters) for kw in per])
+        return Workload(f"{NAMES[cfg]} cluster", arr, pr, de, eng, sets,
+                        meta=dict(cfg=cfg, n_clusters=n_clusters, replicas=R, dispatch=dispatch,
+                                  n_settings=len(per), n_req=N))
     arr = np.empty((n_clusters * R, N), np.int64)
     pr = np.empty((n_clusters * R, N), np.int32)
     de = np.empty((n_clusters * R, N), np.int32)
