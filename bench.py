@@ -89,7 +89,10 @@ def main():
                     help="R > 0: clusters of R replicas behind a global router (the workload's "
                          "traces, R times the rate, split by --dispatch); reports the cluster "
                          "percentiles pooled over each cluster's replicas")
-    ap.add_argument("--dispatch", default="rr", choices=["rr", "random"])
+    ap.add_argument("--dispatch", default="rr", choices=["rr", "random", "jsq"],
+                    help="global router: round robin, balanced random (both split the traces "
+                         "before the run), or join-shortest-queue (decided during the run, "
+                         "one workgroup per cluster)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
     ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--list-cap", type=int, default=0,
@@ -125,8 +128,9 @@ def main():
         n_cl = args.traces or max(1, W.SHAPES[args.workload][0] // R)
         w = W.make_cluster(args.workload, n_clusters=n_cl, replicas=R, dispatch=args.dispatch,
                            n_req=W.SHAPES[args.workload][2] // R)
+        per_rep = w.n_req // R if args.dispatch == "jsq" else w.n_req
         name = f"{W.NAMES[args.workload]}: {n_cl} clusters x {R} replicas ({args.dispatch} " \
-               f"dispatch) x {w.meta['n_settings']} settings x {w.n_req} requests per replica"
+               f"dispatch) x {w.meta['n_settings']} settings x {per_rep} requests per replica"
     else:
         w = W.make(args.workload, n_traces=args.traces, grid=args.grid)
         name = f"{W.NAMES[args.workload]}: {w.n_traces} traces x {w.meta['n_settings']} " \
@@ -192,18 +196,22 @@ def main():
                    "wall_s": wall, "lds_list_cap": tas.tas_list_cap(sim.ctx)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
-                     "kernel": "sim_kernel",
+                     "kernel": "cluster_kernel" if args.cluster and args.dispatch == "jsq"
+                     else "sim_kernel",
                      "algorithmic_bytes_per_launch": alg_bytes},
     }
     if args.cluster:  # cluster percentiles pooled over each cluster's replicas
-        gp = sim.group_percentiles(args.cluster).astype(np.int64)
         S = w.meta["n_settings"]
+        if args.dispatch == "jsq":  # one instance per (cluster, setting) already
+            gp, stride = out["pct"].astype(np.int64), 1
+        else:
+            gp, stride = sim.group_percentiles(args.cluster).astype(np.int64), args.cluster
         per = gp.reshape(w.meta["n_clusters"], S, 3, 3)
         res["config"]["cluster_p99_ttlt_us_mean"] = {
-            W.POLICY_NAMES[int(w.settings["policy"][s * args.cluster])] + f"_s{s}":
+            W.POLICY_NAMES[int(w.settings["policy"][s * stride])] + f"_s{s}":
             float(per[:, s, 1, 2].mean()) for s in range(S)}
         res["config"]["cluster_p99_tbt_us_mean"] = {
-            W.POLICY_NAMES[int(w.settings["policy"][s * args.cluster])] + f"_s{s}":
+            W.POLICY_NAMES[int(w.settings["policy"][s * stride])] + f"_s{s}":
             float(per[:, s, 2, 2].mean()) for s in range(S)}
     sim.close()
     if not args.no_cpu and not args.cluster:

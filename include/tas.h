@@ -183,7 +183,20 @@ typedef struct {
                               min(4032, max(2048, 4 list_cap)). Beyond it:
                               TAS_ECAPACITY                                    */
     const tas_setting *inst; /* [n_inst]                                       */
+    int32_t jsq_replicas;  /* 0 or 1: every instance is one server. 2 ..
+                              TAS_MAX_REPLICAS: every instance is a cluster of
+                              that many replicas behind a join-shortest-queue
+                              router (section "Composability with Global
+                              Dispatch Policies"): its trace is the global
+                              arrival stream; request j goes, at a_j, to the
+                              replica holding the fewest requests not completed
+                              by a_j (ties to the lowest replica), and each
+                              replica schedules its requests with the
+                              instance's setting. Adaptive gamma is not
+                              available in this mode                          */
 } tas_params;
+
+#define TAS_MAX_REPLICAS 16
 
 typedef struct tas_ctx tas_ctx;
 
@@ -205,7 +218,9 @@ size_t tas_workspace_bytes(const tas_traces *traces, const tas_params *params);
  * ada not 0 or 1; ada = 1 with a policy
  * other than BOOST, with table_given, or with an ada_* field outside its
  * range; chunk > max_tokens; any engine limit
- * < 1; chunk > 32767; tau <= 0; list_cap < max_seqs + 64 or > 4032.
+ * < 1; chunk > 32767; tau <= 0; list_cap < max_seqs + 64 or > 4032;
+ * jsq_replicas < 0 or > TAS_MAX_REPLICAS; jsq_replicas > 1 with an adaptive
+ * setting, or with lists of all replicas beyond the 160 KB of LDS.
  * TAS_EINFEASIBLE if ceil((P + D - 1) / block_tokens) > kv_blocks for some
  * request. TAS_ENOMEM if ws_bytes is too small. TAS_EHIP if a copy fails. */
 int tas_create(const tas_traces *traces, const tas_params *params, void *d_ws, size_t ws_bytes,
@@ -239,7 +254,8 @@ int tas_latencies(tas_ctx *ctx, uint32_t *d_ttft, uint32_t *d_ttlt, uint32_t *d_
 /* Enqueue a copy of the per-instance counters, DEVICE int64 [n_inst][8]:
  * iterations, request-iterations (sum of batch sizes), computed tokens,
  * voluntary evictions, forced evictions, final clock us, peak KV blocks,
- * idle us. */
+ * idle us. For a cluster (jsq_replicas > 1): sums over its replicas, except
+ * the final clock and the peak KV blocks, which are the largest. */
 int tas_counters(tas_ctx *ctx, int64_t *d_out, void *stream);
 
 /* Enqueue copies of the adaptive-gamma state at the end of each instance:
@@ -247,6 +263,13 @@ int tas_counters(tas_ctx *ctx, int64_t *d_out, void *stream);
  * adaptive gamma) and d_switches DEVICE int64 [n_inst] (how often the boost
  * table changed grid point). Either pointer may be NULL. */
 int tas_gamma(tas_ctx *ctx, double *d_gamma, int64_t *d_switches, void *stream);
+
+/* Clusters behind the join-shortest-queue router (jsq_replicas > 1):
+ * enqueue copies of the replica each request went to, d_assign DEVICE int32
+ * [n_inst][n_req], and of each replica's counters (as tas_counters),
+ * d_counters DEVICE int64 [n_inst][jsq_replicas][8]. Either pointer may be
+ * NULL. TAS_EINVAL for a context without replicas. */
+int tas_replicas(tas_ctx *ctx, int32_t *d_assign, int64_t *d_counters, void *stream);
 
 /* Synchronise the stream of the last enqueued call and return TAS_OK or the
  * first per-instance error (lowest instance index), e.g. TAS_ELIVELOCK,

@@ -16,6 +16,7 @@
 
 struct tas_ctx {
     int32_t n_traces = 0, n_req = 0, n_inst = 0, list_cap = 0, spill_cap = 0, retry_cap = 0;
+    int32_t replicas = 1;  // > 1: replicas behind a join-shortest-queue router
     int64_t lds_bytes = 0, lds_retry = 0;
     tas::SimArgs args{};
     std::vector<tas::DevSetting> settings;
@@ -34,8 +35,19 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
     size_t arrival, prompt, decode, cached, settings, ada, tfirst, tlast, tbtw, ttft, ttlt, tbtmax,
-        counters, status, gamma, switches, spill, ovf, total;
+        counters, status, gamma, switches, spill, ovf, jidx, assign, rcounters, total;
 };
+
+// Replicas per instance behind the join-shortest-queue router (1: none).
+int32_t replicas_of(const tas_params *p) { return p->jsq_replicas > 1 ? p->jsq_replicas : 1; }
+
+// Dynamic LDS of a launch: one list per instance, or the router block and
+// one 16-aligned list per replica.
+int64_t launch_lds(int32_t list_cap, int32_t wmax, int32_t replicas) {
+    const int64_t one = tas::lds_bytes_for(list_cap, wmax);
+    if (replicas <= 1) return one;
+    return tas::kJsqLdsBytes + (int64_t)replicas * ((one + 15) & ~int64_t(15));
+}
 
 // Adaptive-gamma instances and their largest window (clamped: an invalid
 // window is rejected by check_setting).
@@ -75,6 +87,7 @@ bool engine_ok(const tas_params *p) {
            p->kv_blocks >= 1 && p->block_tokens >= 1 && p->iter_base_us >= 1 &&
            p->iter_tok_us >= 0 && p->iter_ctx_div >= 1 && p->max_iters >= 1 &&
            p->tau_us > 0.0 && std::isfinite(p->tau_us) && p->n_inst >= 0 &&
+           p->jsq_replicas >= 0 && p->jsq_replicas <= tas::kMaxReplicas &&
            p->list_cap >= 0 && p->spill_cap >= 0 && (p->n_inst == 0 || p->inst != nullptr);
 }
 
@@ -89,10 +102,12 @@ bool caps(const tas_traces *t, const tas_params *p, int32_t *lc, int32_t *rc, in
     const bool adaptive = ada_count(p, &wmax) > 0;
     const int32_t l = p->list_cap ? p->list_cap : default_list_cap(p->max_seqs, adaptive);
     if ((int64_t)l < (int64_t)p->max_seqs + 64 || l > tas::kMaxListCap) return false;
-    if (tas::lds_bytes_for(l, wmax) > kMaxLds) return false;
+    const int32_t nr = replicas_of(p);
+    if (nr > 1 && wmax > 0) return false;  // the router runs with gamma fixed
+    if (launch_lds(l, wmax, nr) > kMaxLds) return false;
     int32_t r = p->retry_cap ? p->retry_cap : default_retry_cap(l);
     if (r < l) r = l;
-    while (r > l && tas::lds_bytes_for(r, wmax) > kMaxLds) r -= 64;  // room for the window
+    while (r > l && launch_lds(r, wmax, nr) > kMaxLds) r -= 64;  // room for the window
     if (r > tas::kMaxListCap || tas::lds_bytes_for(r, wmax) > kMaxLds) return false;
     *lc = l;
     *rc = r;
@@ -121,8 +136,13 @@ bool layout(const tas_traces *t, const tas_params *p, int32_t rc, int32_t sc, La
     L->status = o, o = align256(o + (size_t)p->n_inst * 4);
     L->gamma = o, o = align256(o + (size_t)p->n_inst * 8);
     L->switches = o, o = align256(o + (size_t)p->n_inst * 8);
-    L->spill = o, o = align256(o + (size_t)p->n_inst * (size_t)sc * sizeof(tas::Rec));
-    L->ovf = o, o = align256(o + (size_t)p->n_inst * (size_t)(rc + tas::kStage) * sizeof(tas::Rec));
+    const size_t nr = (size_t)replicas_of(p), slots = (size_t)p->n_inst * nr;
+    L->spill = o, o = align256(o + slots * (size_t)sc * sizeof(tas::Rec));
+    L->ovf = o, o = align256(o + slots * (size_t)(rc + tas::kStage) * sizeof(tas::Rec));
+    const bool cl = nr > 1;  // the router's lists, assignment and per-replica counters
+    L->jidx = o, o = align256(o + (cl ? slots * (size_t)t->n_req * 4 : 0));
+    L->assign = o, o = align256(o + (cl ? in * 4 : 0));
+    L->rcounters = o, o = align256(o + (cl ? slots * 8 * 8 : 0));
     L->total = o;
     return true;
 }
@@ -166,6 +186,13 @@ int check_setting(const tas_setting &s, int32_t n_traces, double tau_us, bool ha
         if (tas_boost_table(s.gamma, s.k, tau_us, bt) || bt[0] > cap) return TAS_EINVAL;
     }
     return TAS_OK;
+}
+
+// The kernel of a pass: one workgroup per instance, or per cluster of
+// replicas behind the router.
+int launch(const tas::SimArgs &a, int64_t lds_bytes, void *stream) {
+    return a.replicas > 1 ? tas_launch_cluster(a, lds_bytes, stream)
+                          : tas_launch_sim(a, lds_bytes, stream);
 }
 
 }  // namespace
@@ -245,8 +272,9 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     c->list_cap = lc, c->spill_cap = sc, c->retry_cap = rc;
     int32_t wmax;
     const int32_t n_ada = ada_count(p, &wmax);
-    c->lds_bytes = tas::lds_bytes_for(lc, wmax);
-    c->lds_retry = tas::lds_bytes_for(rc, wmax);
+    c->replicas = replicas_of(p);
+    c->lds_bytes = launch_lds(lc, wmax, c->replicas);
+    c->lds_retry = launch_lds(rc, wmax, c->replicas);
     c->settings.resize((size_t)p->n_inst);
     c->ada.resize((size_t)n_ada);
     int32_t ai = 0;
@@ -330,19 +358,26 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     a.switch_out = (int64_t *)(ws + L.switches);
     a.ada_window = wmax;
     a.ext = ext ? 1 : 0;
+    a.replicas = c->replicas;
+    a.wave_lds = (int32_t)((tas::lds_bytes_for(lc, 0) + 15) & ~int64_t(15));
+    a.jidx = (int32_t *)(ws + L.jidx);
+    a.assign = (int32_t *)(ws + L.assign);
+    a.rcounters = (int64_t *)(ws + L.rcounters);
     *out = c;
     return TAS_OK;
 }
 
+
 int tas_run(tas_ctx *c, void *stream) {
     if (!c) return TAS_EINVAL;
     c->last_stream = (hipStream_t)stream;
-    if (tas_launch_sim(c->args, c->lds_bytes, stream)) return TAS_EHIP;
+    if (launch(c->args, c->lds_bytes, stream)) return TAS_EHIP;
     if (c->retry_cap > c->list_cap) {  // rerun instances that outgrew the small list
         tas::SimArgs a2 = c->args;
         a2.list_cap = c->retry_cap;
         a2.retry = 1;
-        if (tas_launch_sim(a2, c->lds_retry, stream)) return TAS_EHIP;
+        a2.wave_lds = (int32_t)((tas::lds_bytes_for(c->retry_cap, 0) + 15) & ~int64_t(15));
+        if (launch(a2, c->lds_retry, stream)) return TAS_EHIP;
     }
     return TAS_OK;
 }
@@ -403,6 +438,21 @@ int tas_gamma(tas_ctx *c, double *d_gamma, int64_t *d_switches, void *stream) {
         return TAS_EHIP;
     if (d_switches && hipMemcpyAsync(d_switches, c->args.switch_out, bytes,
                                      hipMemcpyDeviceToDevice, (hipStream_t)stream) != hipSuccess)
+        return TAS_EHIP;
+    return TAS_OK;
+}
+
+int tas_replicas(tas_ctx *c, int32_t *d_assign, int64_t *d_counters, void *stream) {
+    if (!c || c->replicas < 2) return TAS_EINVAL;
+    c->last_stream = (hipStream_t)stream;
+    if (c->n_inst == 0) return TAS_OK;
+    const size_t na = (size_t)c->n_inst * (size_t)c->n_req * 4;
+    const size_t nc = (size_t)c->n_inst * (size_t)c->replicas * 8 * 8;
+    if (d_assign && hipMemcpyAsync(d_assign, c->args.assign, na, hipMemcpyDeviceToDevice,
+                                   (hipStream_t)stream) != hipSuccess)
+        return TAS_EHIP;
+    if (d_counters && hipMemcpyAsync(d_counters, c->args.rcounters, nc, hipMemcpyDeviceToDevice,
+                                     (hipStream_t)stream) != hipSuccess)
         return TAS_EHIP;
     return TAS_OK;
 }

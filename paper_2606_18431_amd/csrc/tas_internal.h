@@ -83,7 +83,16 @@ struct SimArgs {
                          // the phase-aware or cache-aware signal, DistBoost)
     const int32_t *cached;  // [n_traces][n_req] expected prefix-cache hits, or
                             // null (read by the cache-aware signal only)
+    // replicas behind a join-shortest-queue router (cluster_kernel only)
+    int32_t replicas;       // waves per workgroup, one replica each
+    int32_t wave_lds;       // LDS bytes per replica (16-aligned)
+    int32_t *jidx;          // [n_inst][replicas][n_req] global indices per replica
+    int32_t *assign;        // [n_inst][n_req] replica of each request
+    int64_t *rcounters;     // [n_inst][replicas][8] counters per replica
 };
+
+constexpr int kMaxReplicas = 16;
+constexpr int64_t kJsqLdsBytes = kMaxReplicas * 4 * 2 + kMaxReplicas * 8 * 8;
 
 // Bytes of the adaptive-gamma block: its state (gamma, gamma_hat, counters),
 // then the window in completion order and sorted, 4 bytes per latency each.
@@ -109,5 +118,6 @@ constexpr int kMaxListCap = 64 * 64 - kStage;
 
 // Launchers implemented next to the kernels.
 int tas_launch_sim(const tas::SimArgs &a, int64_t lds_bytes, void *stream);
+int tas_launch_cluster(const tas::SimArgs &a, int64_t lds_bytes, void *stream);
 int tas_launch_pctl(const uint32_t *ttft, const uint32_t *ttlt, const uint32_t *tbtmax,
                     int32_t n_inst, int32_t n_req, uint32_t *out, void *stream);

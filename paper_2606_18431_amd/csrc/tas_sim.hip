@@ -274,7 +274,9 @@ DEV R permute_rec(const R &x, int dest) {
 // 16-token block gets its own instantiation), -1 otherwise. The policy is a
 // run-time value: one copy of the code serves every policy, so workgroups of
 // different policies on one compute unit share the instruction cache.
-template <int BSH, bool EXT>
+// CL: one replica of a cluster behind a join-shortest-queue router; its
+// arrivals are the global requests the router has dispatched to it so far.
+template <int BSH, bool EXT, bool CL = false>
 struct Sim {
     const SimArgs &A;
     Lds S;
@@ -294,6 +296,12 @@ struct Sim {
     int64_t pa;
     int pP, pD;
     int64_t iters, reqiters, tokens, ev_vol, ev_forced, maxU, idle;
+    // CL: the replica (wave) index, the global indices dispatched to it in
+    // order (HBM, written and read by this wave only, through L2), how many,
+    // the prefetched global index of each lane, and the completions of the
+    // latest iteration
+    int wv, Nk, pidx, last_done;
+    int32_t *jl;
     // per-iteration formation results
     int cnt, used;
     int64_t sum_ctx;
@@ -316,7 +324,7 @@ struct Sim {
     bool cache_signal;  // BOOST with the cache-aware signal P - h + dec
     const int32_t *Hp;  // expected prefix-cache hits of the trace (cache_signal)
 
-    DEV Sim(const SimArgs &a, const DevSetting &st, int i, unsigned char *smem) : A(a) {
+    DEV Sim(const SimArgs &a, const DevSetting &st, int i, unsigned char *smem, int w = 0) : A(a) {
         inst = i;
         N = a.n_req, M = a.M, T = a.T, c = a.c, Kb = a.Kb, bs = a.bs;
         base = a.base, tok = a.tok, div = a.div, lcap = a.list_cap, scap = a.spill_cap;
@@ -331,8 +339,12 @@ struct Sim {
         arr = a.arrival + toff, Pp = a.prompt + toff, Dp = a.decode + toff;
         const size_t ioff = (size_t)i * (size_t)N;
         tfirst = a.tfirst + ioff, tlast = a.tlast + ioff, tbtw = a.tbtw + ioff;
-        spill = a.spill + (size_t)i * (size_t)scap;
-        ovf = a.ovf + (size_t)i * (size_t)a.ovf_stride;
+        wv = w, Nk = 0, pidx = 0, last_done = 0;
+        jl = nullptr;
+        const size_t slot = CL ? (size_t)i * (size_t)a.replicas + (size_t)w : (size_t)i;
+        spill = a.spill + slot * (size_t)scap;
+        ovf = a.ovf + slot * (size_t)a.ovf_stride;
+        if constexpr (CL) jl = a.jidx + slot * (size_t)N;
         const int cap = lcap + kStage;  // the list may use its overflow region during formation
         size_t o = 0;
         S.q = (uint4 *)(smem + o), o += (size_t)cap * 16;
@@ -409,12 +421,22 @@ struct Sim {
 
     // ---------------------------------------------------------- arrivals
 
+    // requests this instance (replica) may take: the trace, or those
+    // dispatched to the replica so far
+    DEV int n_known() const { return CL ? Nk : N; }
+
     DEV void load_pf() {
         const int r = pf + lane();
-        if (r < N) {
-            pa = arr[r], pP = Pp[r], pD = Dp[r];
+        if (r < n_known()) {
+            if constexpr (CL) {
+                pidx = __hip_atomic_load(&jl[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                pa = arr[pidx], pP = Pp[pidx], pD = Dp[pidx];
+            } else {
+                pa = arr[r], pP = Pp[r], pD = Dp[r];
+            }
         } else {
             pa = INT64_MAX, pP = 1, pD = 1;
+            if constexpr (CL) pidx = 0;
         }
     }
 
@@ -455,10 +477,10 @@ struct Sim {
                 off = 0;
             }
             const int r = pf + lane();
-            const bool arrive = lane() >= off && r < N && pa <= t;
+            const bool arrive = lane() >= off && r < n_known() && pa <= t;
             const int n_arr = popc(ballot(arrive));
             if (LIKELY(n_arr == 0)) return;
-            const R x = new_record(r, pa, pP, pD);
+            const R x = new_record(CL ? pidx : r, pa, pP, pD);
             const R y = off ? shfl_rec(x, min(off + lane(), kWave - 1)) : x;
             nW += n_arr;
             next += n_arr;
@@ -1370,6 +1392,111 @@ struct Sim {
         finish();
     }
 
+    // CL: simulate while the replica has work and its clock is below `limit`,
+    // the next arrival time of the global trace (an iteration that starts
+    // before it is formed without that request); then wait for the router.
+    // With limit = INT64_MAX it runs to the end of what was dispatched.
+    DEV void run_until(int64_t limit) {
+        if (status) return;
+        load_pf();  // the router may have dispatched since the last call
+        take_arrivals();
+        for (;;) {
+            if (status) return;
+            if (UNLIKELY(nW + nR == 0)) {
+                if (spill_n > 0) {
+                    refill();
+                    if (status) return;
+                    if (nW + nR == 0) {
+                        fail(S_ESTATE);
+                        return;
+                    }
+                    continue;
+                }
+                if (next >= Nk) return;  // idle: nothing dispatched yet
+                int off = next - pf;
+                if (off >= kWave) {
+                    pf = next;
+                    load_pf();
+                    off = 0;
+                }
+                const int64_t an = rl64(pa, off);  // <= limit: dispatched requests have arrived
+                idle += an - t;
+                t = an;
+                take_arrivals();
+                continue;
+            }
+            if (t >= limit) return;
+            formation();
+            if (status) return;
+            if (cnt == 0) {
+                fail(S_ESTATE);
+                return;
+            }
+            if (U > maxU) maxU = U;
+            const int64_t dt = (int64_t)base + (int64_t)tok * used + (int64_t)ctx_quot((uint64_t)sum_ctx);
+            const int64_t t_end = t + dt;
+            const int c0 = completed;
+            const int lo_mod = emission(t_end);
+            last_done = completed - c0;
+            t = t_end;
+            iters++;
+            reqiters += cnt;
+            tokens += used;
+            if (iters > max_iters) {
+                fail(S_ELIVELOCK);
+                return;
+            }
+            maintenance(lo_mod);
+        }
+    }
+
+    // CL: requests the replica holds at time aj (dispatched and not completed
+    // by aj). Only the latest iteration can end after aj, and its
+    // completions then have not happened yet.
+    DEV int held_at(int64_t aj) const { return Nk - completed + (t > aj ? last_done : 0); }
+
+    // CL: the router sends global request j to this replica.
+    DEV void dispatch(int j) {
+        if (lane() == 0) {
+            __hip_atomic_store(&jl[Nk], j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            A.assign[(size_t)inst * (size_t)N + (size_t)j] = wv;
+        }
+        Nk++;
+        hbm_fence();
+    }
+
+    // CL: latencies of the replica's requests in global order, its counters
+    // (HBM, and in `cn` for the instance's totals) and status (`st`).
+    DEV void finish_cl(int64_t *cn, int32_t *st) {
+        hbm_fence();
+        if (status == 0 && completed != Nk) fail(S_ESTATE);
+        if (status == 0) {
+            const size_t ioff = (size_t)inst * (size_t)N;
+            bool bad = false;
+            for (int b = 0; b < Nk; b += kWave) {
+                const int kk = b + lane();
+                if (kk < Nk) {
+                    const int i = __hip_atomic_load(&jl[kk], __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+                    const int64_t a = arr[i];
+                    const int64_t f = tfirst[i] - a, l = tlast[i] - a;
+                    if (f < 0 || f > 0xFFFFFFFFll || l < 0 || l > 0xFFFFFFFFll) bad = true;
+                    A.ttft[ioff + i] = (uint32_t)f;
+                    A.ttlt[ioff + i] = (uint32_t)l;
+                    A.tbtmax[ioff + i] =
+                        __hip_atomic_load(&tbtw[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+            if (ballot(bad)) fail(S_EOVERFLOW);
+        }
+        if (lane() == 0) {
+            const int64_t v[8] = {iters, reqiters, tokens, ev_vol, ev_forced, t, maxU, idle};
+            int64_t *rc = A.rcounters + ((size_t)inst * (size_t)A.replicas + (size_t)wv) * 8;
+            for (int q = 0; q < 8; q++) rc[q] = v[q], cn[q] = v[q];
+            *st = status;
+        }
+    }
+
     DEV void finish() {
         hbm_fence();
         if (status == 0 && completed != N) fail(S_ESTATE);
@@ -1409,6 +1536,65 @@ DEV void run_instance(const SimArgs &a, const DevSetting &st, int inst, unsigned
     s.run();
 }
 
+// A cluster of replicas behind a join-shortest-queue router (global dispatch
+// policies): one wavefront per replica, all in one workgroup. For every
+// request of the global trace, in order, each replica first simulates the
+// iterations that start before its arrival; then the request goes to the
+// replica holding the fewest requests at that instant (ties to the lowest
+// replica). Every wave passes the same two barriers per request, whatever
+// its own state, so the workgroup cannot split at a barrier.
+struct JsqLds {
+    int32_t held[kMaxReplicas];
+    int32_t status[kMaxReplicas];
+    int64_t cn[kMaxReplicas][8];
+};
+static_assert(sizeof(JsqLds) == kJsqLdsBytes, "router block size");
+
+template <int BSH>
+DEV void run_cluster(const SimArgs &a, const DevSetting &st, int inst, unsigned char *smem) {
+    JsqLds *J = (JsqLds *)smem;
+    const int R = a.replicas, w = (int)(threadIdx.x >> 6), N = a.n_req;
+    Sim<BSH, true, true> s(a, st, inst, smem + kJsqLdsBytes + (size_t)w * (size_t)a.wave_lds, w);
+    const size_t ioff = (size_t)inst * (size_t)N;
+    for (int i = (int)threadIdx.x; i < N; i += (int)blockDim.x)  // gap maxima start at 0
+        __hip_atomic_store(&a.tbtw[ioff + i], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    hbm_fence();
+    __syncthreads();
+    const int64_t *arr = a.arrival + (size_t)st.trace * (size_t)N;
+    for (int j = 0;; j++) {  // j = N: run what was dispatched to the end
+        const int64_t aj = j < N ? arr[j] : INT64_MAX;
+        s.run_until(aj);
+        if (j == N) break;
+        if (lane() == 0) J->held[w] = s.held_at(aj);
+        __syncthreads();
+        int best = 0, bn = J->held[0];
+        for (int r = 1; r < R; r++) {
+            const int h = J->held[r];
+            if (h < bn) best = r, bn = h;
+        }
+        if (best == w) s.dispatch(j);
+        __syncthreads();
+    }
+    s.finish_cl(J->cn[w], &J->status[w]);
+    __syncthreads();
+    if (w == 0) {  // instance totals: sums, the latest clock, the largest KV peak
+        const int q = lane();
+        if (q < 8) {
+            int64_t v = 0;
+            for (int r = 0; r < R; r++) {
+                const int64_t x = J->cn[r][q];
+                v = (q == 5 || q == 6) ? (x > v ? x : v) : v + x;
+            }
+            a.counters[(size_t)inst * 8 + q] = v;
+        }
+        if (q == 0) {
+            int32_t e = 0;
+            for (int r = 0; r < R && e == 0; r++) e = J->status[r];
+            a.status[inst] = e;
+        }
+    }
+}
+
 // EXT: the extended build (adaptive gamma, the phase-aware and cache-aware signals,
 // DistBoost, Sarathi), launched when some instance uses one of them (its extra state
 // and code cost the other policies registers).
@@ -1423,8 +1609,47 @@ __global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
     else run_instance<-1, EXT>(a, st, inst, smem);
 }
 
+// MAXW: the largest number of waves (replicas) the build serves; 8 leaves
+// each wave twice the registers of 16.
+template <int BSH, int MAXW>
+__global__ __launch_bounds__(64 * MAXW) void cluster_kernel(SimArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int inst = blockIdx.x;
+    if (inst >= a.n_inst) return;
+    if (a.retry && a.status[inst] != S_ECAPACITY) return;
+    run_cluster<BSH>(a, a.inst[inst], inst, smem);
+}
+
 }  // namespace
 }  // namespace tas
+
+int tas_launch_cluster(const tas::SimArgs &a, int64_t lds_bytes, void *stream) {
+    if (a.n_inst <= 0) return 0;
+    if (a.replicas < 2 || a.replicas > tas::kMaxReplicas) return -4;
+    hipStream_t s = (hipStream_t)stream;
+    const bool small = a.replicas <= 8, b16 = a.bs == 16;
+    const void *fn = small ? (b16 ? (const void *)tas::cluster_kernel<4, 8>
+                                  : (const void *)tas::cluster_kernel<-1, 8>)
+                           : (b16 ? (const void *)tas::cluster_kernel<4, tas::kMaxReplicas>
+                                  : (const void *)tas::cluster_kernel<-1, tas::kMaxReplicas>);
+    if (lds_bytes > 65536) {
+        if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lds_bytes) != hipSuccess)
+            return -4;
+    }
+    const dim3 grid((unsigned)a.n_inst), block((unsigned)(64 * a.replicas));
+    if (small && b16)
+        hipLaunchKernelGGL((tas::cluster_kernel<4, 8>), grid, block, (size_t)lds_bytes, s, a);
+    else if (small)
+        hipLaunchKernelGGL((tas::cluster_kernel<-1, 8>), grid, block, (size_t)lds_bytes, s, a);
+    else if (b16)
+        hipLaunchKernelGGL((tas::cluster_kernel<4, tas::kMaxReplicas>), grid, block,
+                           (size_t)lds_bytes, s, a);
+    else
+        hipLaunchKernelGGL((tas::cluster_kernel<-1, tas::kMaxReplicas>), grid, block,
+                           (size_t)lds_bytes, s, a);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}
 
 int tas_launch_sim(const tas::SimArgs &a, int64_t lds_bytes, void *stream) {
     if (a.n_inst <= 0) return 0;

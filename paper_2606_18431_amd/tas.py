@@ -56,7 +56,7 @@ class tas_params(ctypes.Structure):
                 ("max_iters", ctypes.c_int64), ("tau_us", ctypes.c_double),
                 ("list_cap", ctypes.c_int32), ("spill_cap", ctypes.c_int32),
                 ("n_inst", ctypes.c_int32), ("retry_cap", ctypes.c_int32),
-                ("inst", ctypes.c_void_p)]
+                ("inst", ctypes.c_void_p), ("jsq_replicas", ctypes.c_int32)]
 
 
 assert ctypes.sizeof(tas_setting) == W.SETTING_DTYPE.itemsize == 280
@@ -65,7 +65,7 @@ EXPORTS = ["tas_workspace_bytes", "tas_create", "tas_run", "tas_percentiles",
            "tas_percentiles_grouped", "tas_latencies",
            "tas_counters", "tas_gamma", "tas_status", "tas_instance_status", "tas_destroy",
            "tas_strerror", "tas_boost_table", "tas_ada_grid", "tas_instance_table",
-           "tas_list_cap"]
+           "tas_list_cap", "tas_replicas"]
 
 _lib = None
 
@@ -93,6 +93,7 @@ def lib():
         L.tas_latencies.argtypes = [P, P, P, P, P]
         L.tas_counters.argtypes = [P, P, P]
         L.tas_gamma.argtypes = [P, P, P, P]
+        L.tas_replicas.argtypes = [P, P, P, P]
         L.tas_ada_grid.argtypes = [P, f64, P, P, P]
         L.tas_status.argtypes = [P]
         L.tas_instance_status.argtypes = [P, P, P]
@@ -153,15 +154,21 @@ def make_traces(arrival_us: np.ndarray, prompt: np.ndarray, decode: np.ndarray,
 
 
 def make_params(engine: W.Engine, settings: np.ndarray, list_cap: int = 0, spill_cap: int = 0,
-                max_iters: int | None = None, retry_cap: int = 0):
+                max_iters: int | None = None, retry_cap: int = 0, jsq_replicas: int = 0):
     """tas_params for an engine and a SETTING_DTYPE array; returns (struct, keepalive)."""
     s = np.ascontiguousarray(settings, W.SETTING_DTYPE)
     p = tas_params(engine.max_seqs, engine.max_tokens, engine.chunk, engine.kv_blocks,
                    engine.block_tokens, engine.iter_base_us, engine.iter_tok_us,
                    engine.iter_ctx_div, int(engine.max_iters if max_iters is None else max_iters),
                    float(engine.tau_us), int(list_cap), int(spill_cap), len(s), int(retry_cap),
-                   s.ctypes.data if len(s) else None)
+                   s.ctypes.data if len(s) else None, int(jsq_replicas))
     return p, s
+
+
+def jsq_replicas_of(w: W.Workload) -> int:
+    """Replicas behind the join-shortest-queue router for a workload made by
+    make_cluster(dispatch="jsq"), else 0."""
+    return int(w.meta["replicas"]) if w.meta.get("dispatch") == "jsq" else 0
 
 
 def tas_workspace_bytes(traces: tas_traces, params: tas_params) -> int:
@@ -203,6 +210,11 @@ def tas_counters(ctx, out, stream=None):
 
 def tas_gamma(ctx, gamma=None, switches=None, stream=None):
     _check(lib().tas_gamma(ctx, _ptr(gamma), _ptr(switches), _stream(stream)), "tas_gamma")
+
+
+def tas_replicas(ctx, assign=None, counters=None, stream=None):
+    _check(lib().tas_replicas(ctx, _ptr(assign), _ptr(counters), _stream(stream)),
+           "tas_replicas")
 
 
 def tas_ada_grid(setting, tau_us: float = 5000.0):
@@ -258,8 +270,9 @@ class Simulation:
         self.w = w
         self.torch = torch
         self._tr, self._keep_t = make_traces(w.arrival_us, w.prompt, w.decode, w.cached)
+        self.replicas = jsq_replicas_of(w)
         self._pa, self._keep_p = make_params(w.engine, w.settings, list_cap, spill_cap,
-                                             max_iters, retry_cap)
+                                             max_iters, retry_cap, self.replicas)
         self.ws_bytes = tas_workspace_bytes(self._tr, self._pa)
         if self.ws_bytes == 0:
             raise TasError(TAS_EINVAL, "tas_workspace_bytes")
@@ -305,6 +318,12 @@ class Simulation:
         out["switches"] = self.switch_buf.cpu().numpy()
         out["status"] = self.status_buf.cpu().numpy()
         out["pct"] = self.pct.cpu().numpy().view(np.uint32)
+        if self.replicas > 1:  # the router's assignment and the replicas' counters
+            asg = torch.empty((n, self.m), dtype=torch.int32, device=self.pct.device)
+            rc = torch.empty((n, self.replicas, 8), dtype=torch.int64, device=self.pct.device)
+            tas_replicas(self.ctx, asg, rc)
+            out["assign"] = asg.cpu().numpy()
+            out["rcounters"] = rc.cpu().numpy()
         return out
 
     def group_percentiles(self, group: int, stream=None) -> np.ndarray:

@@ -462,14 +462,15 @@ def make_cluster(cfg: int, n_clusters: int, replicas: int, dispatch: str = "rr",
     setting, replica, so the R replicas of a (cluster, setting) are R adjacent
     instances (``tas_percentiles_grouped`` with group R reduces over them).
     Traces are ordered cluster, replica. ``settings``: keyword dicts for
-    ``setting`` (default FCFS, UniBoost at gamma 1e-3, vanilla boost)."""
+    ``setting`` (default FCFS, UniBoost at gamma 1e-3, vanilla boost, Sarathi:
+    the paper compares UniBoost with the Sarathi engine under each router)."""
     T0, _, N0 = SHAPES[cfg]
     N = N0 if n_req is None else n_req
     R = int(replicas)
     eng = _engine(cfg)
     per = settings if settings is not None else [
         dict(policy=FCFS), dict(policy=BOOST, gamma=1e-3, **UNIBOOST),
-        dict(policy=BOOST, gamma=1e-3, **VANILLA)]
+        dict(policy=BOOST, gamma=1e-3, **VANILLA), dict(policy=SARATHI)]
     if dispatch == "jsq":
         arr = np.empty((n_clusters, N * R), np.int64)
         pr = np.empty((n_clusters, N * R), np.int32)

@@ -26,7 +26,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = tas.lib()
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == 17
     for n in names:
         assert hasattr(lib, n), n
     assert set(tas.EXPORTS) <= set(names)
@@ -257,3 +257,26 @@ def test_cache_signal_inputs():
         assert create_rc(w, settings=s2, cached=h)[0] == tas.TAS_EINVAL
     with pytest.raises(ValueError):
         tas.make_traces(w.arrival_us, w.prompt, w.decode, h[:1])
+
+
+def test_jsq_replicas_validation():
+    """Clusters behind the join-shortest-queue router: replica counts in
+    [2, 16], no adaptive gamma, all lists within the LDS; workspace grows with
+    the replicas (spill, lists and the router's arrays per replica)."""
+    w = W.make_cluster(1, n_clusters=1, replicas=4, dispatch="jsq", n_req=30)
+    t, _ = tas.make_traces(w.arrival_us, w.prompt, w.decode)
+    sizes = []
+    for r in (0, 2, 4, 16):
+        p, _ = tas.make_params(w.engine, w.settings, jsq_replicas=r)
+        sizes.append(tas.tas_workspace_bytes(t, p))
+    assert sizes[0] > 0 and sizes[0] < sizes[1] < sizes[2] < sizes[3]
+    for r in (-1, 17):
+        p, _ = tas.make_params(w.engine, w.settings, jsq_replicas=r)
+        assert tas.tas_workspace_bytes(t, p) == 0
+    assert create_rc(w, ws_bytes=1, jsq_replicas=4)[0] == tas.TAS_ENOMEM  # valid so far
+    s = w.settings.copy()
+    s[1] = W.setting(0, W.BOOST, gamma=1e-3, ada=dict(W.ADA))
+    assert create_rc(w, settings=s, jsq_replicas=4)[0] == tas.TAS_EINVAL
+    big = W.Engine(max_seqs=256, max_tokens=16384, kv_blocks=32768)
+    assert create_rc(w, engine=big, jsq_replicas=16)[0] == tas.TAS_EINVAL  # 16 lists > LDS
+    assert create_rc(w, engine=big, ws_bytes=1, jsq_replicas=8)[0] == tas.TAS_ENOMEM
