@@ -78,7 +78,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=2)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", type=int, default=4, choices=[0, 1, 2, 3, 4])
+    ap.add_argument("--workload", type=int, default=4, choices=[0, 1, 2, 3, 4, 5])
     ap.add_argument("--traces", type=int, default=None, help="shrink the sweep (testing)")
     ap.add_argument("--grid", default="sweep",
                     choices=["sweep", "ada", "comparators", "ladder", "cache"],
@@ -213,6 +213,17 @@ def main():
         res["config"]["cluster_p99_tbt_us_mean"] = {
             W.POLICY_NAMES[int(w.settings["policy"][s * stride])] + f"_s{s}":
             float(per[:, s, 2, 2].mean()) for s in range(S)}
+    if args.workload == 5 and not args.cluster:  # short and long requests apart
+        lat = sim.results()["ttlt"].astype(np.float64) / 1e6
+        longm = np.asarray(w.decode)[w.settings["trace"]] == 6000
+        S = w.meta["n_settings"]
+        for cls, m in (("short", ~longm), ("long", longm)):
+            res["config"][f"{cls}_ttlt_s"] = {
+                W.POLICY_NAMES[int(w.settings["policy"][s])] + f"_s{s}": {
+                    "mean": float(np.mean([lat[i][m[i]].mean() for i in range(s, w.n_inst, S)])),
+                    "p99": float(np.mean([np.percentile(lat[i][m[i]], 99, method="inverted_cdf")
+                                          for i in range(s, w.n_inst, S)]))}
+                for s in range(S)}
     sim.close()
     if not args.no_cpu and not args.cluster:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)

@@ -17,6 +17,9 @@ Five workloads are defined (``make(cfg)``):
 2  reasoning-heavy under KV pressure: 64 x 64, 10,000 requests, 8,192 KV blocks.
 3  bursty arrivals + decode-length shift: 128 x 32, 20,000 requests, 2-state MMPP.
 4  large sweep: 256 x 64, 50,000 requests, 60/40 blend of the 1 and 2 laws.
+5  starvation: 32 x 8, 20,000 requests, 90% short (~125 / 100) and 10% long
+   (2000 / 6000) requests, Poisson at utilisation 0.99 (the paper's
+   starvation study), under its policies (UniBoost, Sarathi, SJF, SRPT, ...).
 
 The policy-parameter grid per trace: setting 0 = FCFS, setting 1 = oracle-length
 SRPT, then pairs (UniBoost with MemGuard, vanilla boost) over log-spaced gamma.
@@ -271,13 +274,15 @@ def _engine(cfg: int) -> Engine:
         return Engine(kv_blocks=16384)
     if cfg == 4:
         return Engine(max_seqs=256, max_tokens=16384, kv_blocks=32768)
+    if cfg == 5:
+        return Engine(kv_blocks=32768)
     raise ValueError(cfg)
 
 
 SHAPES = {0: (1, 8, 1000), 1: (64, 64, 10000), 2: (64, 64, 10000), 3: (128, 32, 20000),
-          4: (256, 64, 50000)}
+          4: (256, 64, 50000), 5: (32, 8, 20000)}
 NAMES = {0: "tiny", 1: "chat-heavy", 2: "reasoning-kv-pressure", 3: "bursty-shift",
-         4: "large-sweep"}
+         4: "large-sweep", 5: "starvation"}
 
 
 def _trace(cfg: int, trace: int, n: int, eng: Engine):
@@ -305,6 +310,13 @@ def _trace(cfg: int, trace: int, n: int, eng: Engine):
         lam_b = lam_avg / 3.5  # time-average rate of {1x, 6x} with equal dwell
         arr = _mmpp_arrivals(rng, n, lam_b, 6.0 * lam_b, 30.0e6)
         return arr, p, d
+    elif cfg == 5:
+        # the paper's starvation mix: 90% short (about 125 prompt, 100 output)
+        # and 10% long (2000 prompt, 6000 output) requests, Poisson at 0.99
+        long = rng.random(n) < 0.1
+        p = np.where(long, 2000, _lognormal(rng, n, 125, 0.2, 64, 256)).astype(np.int32)
+        d = np.where(long, 6000, 100).astype(np.int32)
+        rho = 0.99
     elif cfg == 4:
         chat = rng.random(n) < 0.6
         p = np.where(chat, _lognormal(rng, n, 768, 1.0, 16, 4096),
@@ -345,6 +357,21 @@ def cache_settings(n_traces: int) -> np.ndarray:
         per.append(dict(policy=BOOST, gamma=g, **var))
         per.append(dict(policy=BOOST, gamma=g, signal=2, **var))
     per += [dict(policy=FCFS), dict(policy=SRPT)]
+    out = np.zeros(n_traces * len(per), dtype=SETTING_DTYPE)
+    for t in range(n_traces):
+        for s, kw in enumerate(per):
+            out[t * len(per) + s] = setting(t, **kw)
+    return out
+
+
+def starvation_settings(n_traces: int, gamma: float = 1e-3) -> np.ndarray:
+    """Per trace, the policies of the paper's starvation study and their
+    neighbours (8 settings): UniBoost at one gamma, Sarathi, SJF, SRPT, then
+    FCFS, vanilla boost, TRAIL and DistBoost. (LAS starves the long requests
+    past the 32-bit latency range at this load.) Instance id = trace * 8 + s."""
+    per = [dict(policy=BOOST, gamma=gamma, **UNIBOOST), dict(policy=SARATHI), dict(policy=SJF),
+           dict(policy=SRPT), dict(policy=FCFS), dict(policy=BOOST, gamma=gamma, **VANILLA),
+           dict(policy=TRAIL), dict(policy=DIST, gamma=gamma)]
     out = np.zeros(n_traces * len(per), dtype=SETTING_DTYPE)
     for t in range(n_traces):
         for s, kw in enumerate(per):
@@ -421,6 +448,9 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
         S = 8
     elif grid == "cache":
         sets = cache_settings(T)
+        S = 8
+    elif cfg == 5:
+        sets = starvation_settings(T)
         S = 8
     elif cfg == 0 and S == 8:
         st = [setting(0, FCFS), setting(0, SRPT)]

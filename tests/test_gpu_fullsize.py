@@ -42,7 +42,7 @@ def sample_instances(w, n_random=4, seed=0):
     return np.array(sorted(pick), np.int64)
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4, 5])
 def test_full_size_sampled_parity(torch, cfg):
     from paper_2606_18431_amd import tas
 

@@ -88,6 +88,7 @@ def test_hand_worked_on_gpu(torch, case):
     (2, 2, 8, 3000),      # KV pressure: many evictions
     (3, 2, 8, 5000),      # bursts and a length shift
     (4, 1, 8, 6000),      # max_seqs 256, 16384-token budget
+    (5, 2, 8, 4000),      # the starvation mix under its policies (Sarathi: extended build)
 ])
 def test_parity_reduced_configs(torch, cfg, n_traces, n_settings, n_req):
     w = W.make(cfg, n_traces=n_traces, n_settings=n_settings, n_req=n_req)
