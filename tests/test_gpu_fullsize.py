@@ -113,3 +113,66 @@ def test_full_size_large_sweep_other_grids(torch, grid):
         assert np.array_equal(g["pct"][i], o["pct"][j]), i
         assert g["switches"][i] == o["switches"][j], i
         assert g["gamma"][i:i + 1].view(np.int64)[0] == o["gamma"][j:j + 1].view(np.int64)[0], i
+
+
+def replay_router_fast(arrival, assign, ttlt, R):
+    """Every request went to a replica holding the fewest requests not
+    completed by its arrival (ties to the lowest), checked for all N at once:
+    at a_j replica r holds the requests dispatched to it before j minus those
+    of them completed by a_j (a completion is never before its arrival, so
+    none of the later ones has completed by then)."""
+    a = np.asarray(arrival, np.int64)
+    done = a + np.asarray(ttlt, np.int64)
+    n = len(a)
+    held = np.zeros((R, n), np.int64)
+    for r in range(R):
+        mine = assign == r
+        before = np.concatenate([[0], np.cumsum(mine)[:-1]])
+        fin = np.sort(done[mine])
+        held[r] = before - np.searchsorted(fin, a, side="right")
+    return bool(np.all(np.argmin(held, axis=0) == assign))
+
+
+def test_full_size_jsq_clusters(torch):
+    """The JSQ bench configuration (large-sweep law, 32 clusters x 8 replicas,
+    50,000 requests per cluster, FCFS / UniBoost / vanilla boost / Sarathi) in
+    its launch: every instance TAS_OK; on the first and the last cluster,
+    every routing decision agrees with the GPU's own completion times, and
+    every replica's requests, simulated by the oracle as a plain instance,
+    give exactly the GPU's latencies and the replica's counters."""
+    from paper_2606_18431_amd import tas
+
+    R = 8
+    w = W.make_cluster(4, n_clusters=32, replicas=R, dispatch="jsq", n_req=50000 // R)
+    print(f"[gpu] full-size jsq: {w.n_inst} clusters x {R} replicas x {w.n_req} requests",
+          flush=True)
+    sim = tas.Simulation(w)
+    sim.step()
+    g = sim.results()
+    sim.close()
+    assert g["rc"] == 0, tas.tas_strerror(g["rc"])
+    assert (g["status"] == 0).all()
+    S = w.meta["n_settings"]
+    sel = list(range(S)) + list(range(w.n_inst - S, w.n_inst))
+    jobs = []
+    for i in sel:
+        t = int(w.settings["trace"][i])
+        assert replay_router_fast(w.arrival_us[t], g["assign"][i], g["ttlt"][i], R), i
+        for r in range(R):
+            idx = np.nonzero(g["assign"][i] == r)[0]
+            jobs.append((i, r, idx))
+    def check(job):
+        i, r, idx = job
+        t = int(w.settings["trace"][i])
+        one = W.Workload("replica", w.arrival_us[t][idx][None], w.prompt[t][idx][None],
+                         w.decode[t][idx][None], w.engine, w.settings[i:i + 1].copy())
+        o = oracle.run(one, n_threads=1)
+        assert o["rc"] == 0, (i, r)
+        for key in ("ttft", "ttlt", "tbtmax"):
+            assert np.array_equal(o[key][0], g[key][i][idx]), (i, r, key)
+        assert np.array_equal(o["counters"][0], g["rcounters"][i, r]), (i, r)
+
+    from concurrent.futures import ThreadPoolExecutor
+
+    with ThreadPoolExecutor(min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(check, jobs))
