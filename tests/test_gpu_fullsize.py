@@ -164,8 +164,10 @@ def test_full_size_jsq_clusters(torch):
     def check(job):
         i, r, idx = job
         t = int(w.settings["trace"][i])
+        st = w.settings[i:i + 1].copy()
+        st["trace"] = 0  # the replica's requests are the one trace of `one`
         one = W.Workload("replica", w.arrival_us[t][idx][None], w.prompt[t][idx][None],
-                         w.decode[t][idx][None], w.engine, w.settings[i:i + 1].copy())
+                         w.decode[t][idx][None], w.engine, st)
         o = oracle.run(one, n_threads=1)
         assert o["rc"] == 0, (i, r)
         for key in ("ttft", "ttlt", "tbtmax"):
