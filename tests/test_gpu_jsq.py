@@ -107,3 +107,16 @@ def test_jsq_large_sweep_law(torch):
     o = oracle.jsq(w, 8)
     g = gpu_run(w)
     assert_parity(g, o)
+
+
+def test_parity_jsq_cache_signal(torch):
+    """The cache-aware signal behind the router: each replica reads the hits
+    of the global requests it received."""
+    R = 4
+    w = W.make_cluster(2, n_clusters=2, replicas=R, dispatch="jsq", n_req=300,
+                       settings=[dict(policy=W.BOOST, gamma=1e-3, signal=2, **W.UNIBOOST),
+                                 dict(policy=W.BOOST, gamma=1e-2, signal=2, **W.VANILLA)])
+    w.cached = np.stack([W.cached_tokens([7, c], w.prompt[c]) for c in range(w.n_traces)])
+    o = oracle.jsq(w, R)
+    g = gpu_run(w)
+    assert_parity(g, o)
