@@ -192,8 +192,8 @@ typedef struct {
                               replica holding the fewest requests not completed
                               by a_j (ties to the lowest replica), and each
                               replica schedules its requests with the
-                              instance's setting. Adaptive gamma is not
-                              available in this mode                          */
+                              instance's setting (an adaptive setting adapts
+                              gamma per replica)                              */
 } tas_params;
 
 #define TAS_MAX_REPLICAS 16
@@ -219,8 +219,8 @@ size_t tas_workspace_bytes(const tas_traces *traces, const tas_params *params);
  * other than BOOST, with table_given, or with an ada_* field outside its
  * range; chunk > max_tokens; any engine limit
  * < 1; chunk > 32767; tau <= 0; list_cap < max_seqs + 64 or > 4032;
- * jsq_replicas < 0 or > TAS_MAX_REPLICAS; jsq_replicas > 1 with an adaptive
- * setting, or with lists of all replicas beyond the 160 KB of LDS.
+ * jsq_replicas < 0 or > TAS_MAX_REPLICAS; jsq_replicas > 1 with the lists
+ * (and adaptive-gamma windows) of all replicas beyond the 160 KB of LDS.
  * TAS_EINFEASIBLE if ceil((P + D - 1) / block_tokens) > kv_blocks for some
  * request. TAS_ENOMEM if ws_bytes is too small. TAS_EHIP if a copy fails. */
 int tas_create(const tas_traces *traces, const tas_params *params, void *d_ws, size_t ws_bytes,
@@ -266,10 +266,13 @@ int tas_gamma(tas_ctx *ctx, double *d_gamma, int64_t *d_switches, void *stream);
 
 /* Clusters behind the join-shortest-queue router (jsq_replicas > 1):
  * enqueue copies of the replica each request went to, d_assign DEVICE int32
- * [n_inst][n_req], and of each replica's counters (as tas_counters),
- * d_counters DEVICE int64 [n_inst][jsq_replicas][8]. Either pointer may be
+ * [n_inst][n_req], of each replica's counters (as tas_counters), d_counters
+ * DEVICE int64 [n_inst][jsq_replicas][8], and of each replica's final
+ * adaptive gamma and grid-cell changes (as tas_gamma), d_gamma DEVICE double
+ * and d_switches DEVICE int64 [n_inst][jsq_replicas]. Any pointer may be
  * NULL. TAS_EINVAL for a context without replicas. */
-int tas_replicas(tas_ctx *ctx, int32_t *d_assign, int64_t *d_counters, void *stream);
+int tas_replicas(tas_ctx *ctx, int32_t *d_assign, int64_t *d_counters, double *d_gamma,
+                 int64_t *d_switches, void *stream);
 
 /* Synchronise the stream of the last enqueued call and return TAS_OK or the
  * first per-instance error (lowest instance index), e.g. TAS_ELIVELOCK,

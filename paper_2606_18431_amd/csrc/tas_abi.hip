@@ -35,7 +35,8 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
     size_t arrival, prompt, decode, cached, settings, ada, tfirst, tlast, tbtw, ttft, ttlt, tbtmax,
-        counters, status, gamma, switches, spill, ovf, jidx, assign, rcounters, total;
+        counters, status, gamma, switches, spill, ovf, jidx, assign, rcounters, rgamma, rswitches,
+        total;
 };
 
 // Replicas per instance behind the join-shortest-queue router (1: none).
@@ -103,7 +104,6 @@ bool caps(const tas_traces *t, const tas_params *p, int32_t *lc, int32_t *rc, in
     const int32_t l = p->list_cap ? p->list_cap : default_list_cap(p->max_seqs, adaptive);
     if ((int64_t)l < (int64_t)p->max_seqs + 64 || l > tas::kMaxListCap) return false;
     const int32_t nr = replicas_of(p);
-    if (nr > 1 && wmax > 0) return false;  // the router runs with gamma fixed
     if (launch_lds(l, wmax, nr) > kMaxLds) return false;
     int32_t r = p->retry_cap ? p->retry_cap : default_retry_cap(l);
     if (r < l) r = l;
@@ -143,6 +143,8 @@ bool layout(const tas_traces *t, const tas_params *p, int32_t rc, int32_t sc, La
     L->jidx = o, o = align256(o + (cl ? slots * (size_t)t->n_req * 4 : 0));
     L->assign = o, o = align256(o + (cl ? in * 4 : 0));
     L->rcounters = o, o = align256(o + (cl ? slots * 8 * 8 : 0));
+    L->rgamma = o, o = align256(o + (cl ? slots * 8 : 0));
+    L->rswitches = o, o = align256(o + (cl ? slots * 8 : 0));
     L->total = o;
     return true;
 }
@@ -359,10 +361,12 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     a.ada_window = wmax;
     a.ext = ext ? 1 : 0;
     a.replicas = c->replicas;
-    a.wave_lds = (int32_t)((tas::lds_bytes_for(lc, 0) + 15) & ~int64_t(15));
+    a.wave_lds = (int32_t)((tas::lds_bytes_for(lc, wmax) + 15) & ~int64_t(15));
     a.jidx = (int32_t *)(ws + L.jidx);
     a.assign = (int32_t *)(ws + L.assign);
     a.rcounters = (int64_t *)(ws + L.rcounters);
+    a.rgamma = (double *)(ws + L.rgamma);
+    a.rswitches = (int64_t *)(ws + L.rswitches);
     *out = c;
     return TAS_OK;
 }
@@ -376,7 +380,8 @@ int tas_run(tas_ctx *c, void *stream) {
         tas::SimArgs a2 = c->args;
         a2.list_cap = c->retry_cap;
         a2.retry = 1;
-        a2.wave_lds = (int32_t)((tas::lds_bytes_for(c->retry_cap, 0) + 15) & ~int64_t(15));
+        a2.wave_lds = (int32_t)((tas::lds_bytes_for(c->retry_cap, c->args.ada_window) + 15) &
+                                ~int64_t(15));
         if (launch(a2, c->lds_retry, stream)) return TAS_EHIP;
     }
     return TAS_OK;
@@ -442,17 +447,20 @@ int tas_gamma(tas_ctx *c, double *d_gamma, int64_t *d_switches, void *stream) {
     return TAS_OK;
 }
 
-int tas_replicas(tas_ctx *c, int32_t *d_assign, int64_t *d_counters, void *stream) {
+int tas_replicas(tas_ctx *c, int32_t *d_assign, int64_t *d_counters, double *d_gamma,
+                 int64_t *d_switches, void *stream) {
     if (!c || c->replicas < 2) return TAS_EINVAL;
     c->last_stream = (hipStream_t)stream;
     if (c->n_inst == 0) return TAS_OK;
+    const hipStream_t s = (hipStream_t)stream;
+    const size_t slots = (size_t)c->n_inst * (size_t)c->replicas;
     const size_t na = (size_t)c->n_inst * (size_t)c->n_req * 4;
-    const size_t nc = (size_t)c->n_inst * (size_t)c->replicas * 8 * 8;
-    if (d_assign && hipMemcpyAsync(d_assign, c->args.assign, na, hipMemcpyDeviceToDevice,
-                                   (hipStream_t)stream) != hipSuccess)
-        return TAS_EHIP;
-    if (d_counters && hipMemcpyAsync(d_counters, c->args.rcounters, nc, hipMemcpyDeviceToDevice,
-                                     (hipStream_t)stream) != hipSuccess)
+    if ((d_assign && hipMemcpyAsync(d_assign, c->args.assign, na, hipMemcpyDeviceToDevice, s)) ||
+        (d_counters && hipMemcpyAsync(d_counters, c->args.rcounters, slots * 64,
+                                      hipMemcpyDeviceToDevice, s)) ||
+        (d_gamma && hipMemcpyAsync(d_gamma, c->args.rgamma, slots * 8, hipMemcpyDeviceToDevice, s)) ||
+        (d_switches && hipMemcpyAsync(d_switches, c->args.rswitches, slots * 8,
+                                      hipMemcpyDeviceToDevice, s)))
         return TAS_EHIP;
     return TAS_OK;
 }

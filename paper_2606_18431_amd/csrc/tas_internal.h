@@ -89,6 +89,8 @@ struct SimArgs {
     int32_t *jidx;          // [n_inst][replicas][n_req] global indices per replica
     int32_t *assign;        // [n_inst][n_req] replica of each request
     int64_t *rcounters;     // [n_inst][replicas][8] counters per replica
+    double *rgamma;         // [n_inst][replicas] final adaptive gamma (0 without)
+    int64_t *rswitches;     // [n_inst][replicas] grid-cell changes
 };
 
 constexpr int kMaxReplicas = 16;

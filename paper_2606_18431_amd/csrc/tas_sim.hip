@@ -1426,6 +1426,10 @@ struct Sim {
                 continue;
             }
             if (t >= limit) return;
+            if (ad) {  // each replica adapts its own gamma
+                ada_update();
+                if (status) return;
+            }
             formation();
             if (status) return;
             if (cnt == 0) {
@@ -1491,8 +1495,11 @@ struct Sim {
         }
         if (lane() == 0) {
             const int64_t v[8] = {iters, reqiters, tokens, ev_vol, ev_forced, t, maxU, idle};
-            int64_t *rc = A.rcounters + ((size_t)inst * (size_t)A.replicas + (size_t)wv) * 8;
+            const size_t slot = (size_t)inst * (size_t)A.replicas + (size_t)wv;
+            int64_t *rc = A.rcounters + slot * 8;
             for (int q = 0; q < 8; q++) rc[q] = v[q], cn[q] = v[q];
+            A.rgamma[slot] = ad ? S.as->gamma : 0.0;
+            A.rswitches[slot] = ad ? S.as->switches : 0;
             *st = status;
         }
     }

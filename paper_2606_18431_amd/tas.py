@@ -93,7 +93,7 @@ def lib():
         L.tas_latencies.argtypes = [P, P, P, P, P]
         L.tas_counters.argtypes = [P, P, P]
         L.tas_gamma.argtypes = [P, P, P, P]
-        L.tas_replicas.argtypes = [P, P, P, P]
+        L.tas_replicas.argtypes = [P, P, P, P, P, P]
         L.tas_ada_grid.argtypes = [P, f64, P, P, P]
         L.tas_status.argtypes = [P]
         L.tas_instance_status.argtypes = [P, P, P]
@@ -212,9 +212,9 @@ def tas_gamma(ctx, gamma=None, switches=None, stream=None):
     _check(lib().tas_gamma(ctx, _ptr(gamma), _ptr(switches), _stream(stream)), "tas_gamma")
 
 
-def tas_replicas(ctx, assign=None, counters=None, stream=None):
-    _check(lib().tas_replicas(ctx, _ptr(assign), _ptr(counters), _stream(stream)),
-           "tas_replicas")
+def tas_replicas(ctx, assign=None, counters=None, gamma=None, switches=None, stream=None):
+    _check(lib().tas_replicas(ctx, _ptr(assign), _ptr(counters), _ptr(gamma), _ptr(switches),
+                              _stream(stream)), "tas_replicas")
 
 
 def tas_ada_grid(setting, tau_us: float = 5000.0):
@@ -321,9 +321,13 @@ class Simulation:
         if self.replicas > 1:  # the router's assignment and the replicas' counters
             asg = torch.empty((n, self.m), dtype=torch.int32, device=self.pct.device)
             rc = torch.empty((n, self.replicas, 8), dtype=torch.int64, device=self.pct.device)
-            tas_replicas(self.ctx, asg, rc)
+            rg = torch.empty((n, self.replicas), dtype=torch.float64, device=self.pct.device)
+            rs = torch.empty((n, self.replicas), dtype=torch.int64, device=self.pct.device)
+            tas_replicas(self.ctx, asg, rc, rg, rs)
             out["assign"] = asg.cpu().numpy()
             out["rcounters"] = rc.cpu().numpy()
+            out["rgamma"] = rg.cpu().numpy()
+            out["rswitches"] = rs.cpu().numpy()
         return out
 
     def group_percentiles(self, group: int, stream=None) -> np.ndarray:

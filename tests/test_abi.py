@@ -261,7 +261,7 @@ def test_cache_signal_inputs():
 
 def test_jsq_replicas_validation():
     """Clusters behind the join-shortest-queue router: replica counts in
-    [2, 16], no adaptive gamma, all lists within the LDS; workspace grows with
+    [2, 16], all lists and adaptive windows within the LDS; workspace grows with
     the replicas (spill, lists and the router's arrays per replica)."""
     w = W.make_cluster(1, n_clusters=1, replicas=4, dispatch="jsq", n_req=30)
     t, _ = tas.make_traces(w.arrival_us, w.prompt, w.decode)
@@ -275,8 +275,10 @@ def test_jsq_replicas_validation():
         assert tas.tas_workspace_bytes(t, p) == 0
     assert create_rc(w, ws_bytes=1, jsq_replicas=4)[0] == tas.TAS_ENOMEM  # valid so far
     s = w.settings.copy()
-    s[1] = W.setting(0, W.BOOST, gamma=1e-3, ada=dict(W.ADA))
-    assert create_rc(w, settings=s, jsq_replicas=4)[0] == tas.TAS_EINVAL
+    s[1] = W.setting(0, W.BOOST, gamma=1e-3, ada=dict(W.ADA))  # gamma adapts per replica
+    assert create_rc(w, settings=s, ws_bytes=1, jsq_replicas=4)[0] == tas.TAS_ENOMEM
+    s[1] = W.setting(0, W.BOOST, gamma=1e-3, ada=dict(W.ADA, window=2048, min_samples=64))
+    assert create_rc(w, settings=s, jsq_replicas=8)[0] == tas.TAS_EINVAL  # windows > LDS
     big = W.Engine(max_seqs=256, max_tokens=16384, kv_blocks=32768)
     assert create_rc(w, engine=big, jsq_replicas=16)[0] == tas.TAS_EINVAL  # 16 lists > LDS
     assert create_rc(w, engine=big, ws_bytes=1, jsq_replicas=8)[0] == tas.TAS_ENOMEM

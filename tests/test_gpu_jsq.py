@@ -60,6 +60,9 @@ def assert_parity(g, o):
                                  f"oracle {o[key][tuple(bad)]}")
     assert np.array_equal(g["rcounters"], o["counters"])
     assert np.array_equal(g["counters"], totals(o["counters"]))
+    # per-replica adaptive gamma, bit for bit, and its grid-cell changes
+    assert np.array_equal(g["rgamma"].view(np.int64), o["gamma"].view(np.int64))
+    assert np.array_equal(g["rswitches"], o["switches"])
 
 
 @pytest.mark.parametrize("c", GOLDEN, ids=[c["name"] for c in GOLDEN])
@@ -120,3 +123,18 @@ def test_parity_jsq_cache_signal(torch):
     o = oracle.jsq(w, R)
     g = gpu_run(w)
     assert_parity(g, o)
+
+
+@pytest.mark.parametrize("cfg,R", [(2, 4), (3, 2)])
+def test_parity_jsq_adaptive_gamma(torch, cfg, R):
+    """Adaptive gamma behind the router: every replica runs its own estimate
+    from its own completions (small windows, so gamma crosses many cells)."""
+    ada = dict(W.ADA, window=40, min_samples=20, beta=0.2)
+    w = W.make_cluster(cfg, n_clusters=1, replicas=R, dispatch="jsq", n_req=300,
+                       settings=[dict(policy=W.BOOST, gamma=1e-3, ada=ada, **W.UNIBOOST),
+                                 dict(policy=W.BOOST, gamma=1e-2, ada=ada, **W.VANILLA),
+                                 dict(policy=W.FCFS)])
+    o = oracle.jsq(w, R)
+    g = gpu_run(w)
+    assert_parity(g, o)
+    assert np.all(o["switches"][:2] > 0)
