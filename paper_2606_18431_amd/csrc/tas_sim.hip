@@ -1178,7 +1178,43 @@ struct Sim {
         return nx;
     }
 
+    // Whether the entries from rank `from` on, completed ones aside, are in
+    // ascending order; if so, their re-keyed entries stay where they are
+    // (their flags are cleared). No holes lie below `from`.
+    DEV bool settle_in_place(int from) {
+        const int start = (from >> 6) << 6;
+        uint64_t pmax = start > 0 ? uniu(S.k[start - 1]) : 0ull;
+        for (int b = start; b < L; b += kWave) {
+            const int r = b + lane();
+            const bool v = r < L && !(S.q[r].x & G_DONE);
+            const uint64_t pk = r < L ? S.k[r] : 0ull;
+            const uint64_t inc = scan_maxu(v ? pk : 0ull);
+            uint64_t exc = prev_lane_u64(inc, 0ull);
+            if (pmax > exc) exc = pmax;
+            if (ballot(v && pk < exc)) return false;
+            const uint64_t cm = rlu(inc, 63);
+            if (cm > pmax) pmax = cm;
+        }
+        for (int b = start; b < L; b += kWave) {
+            const int r = b + lane();
+            if (r < L) {
+                const uint32_t g = S.q[r].x;
+                if (g & G_DIRTY) S.q[r].x = g & ~G_DIRTY;
+            }
+        }
+        wsync();
+        return true;
+    }
+
     DEV void maintenance(int lo_mod) {
+        if constexpr (EXT) {
+            // Sarathi moves every decode that emitted to the same, latest key:
+            // when all decodes were in the batch (steady decoding) the list
+            // is still in order and nothing needs re-inserting
+            if (pol == P_SARATHI && lo_mod < L && n_holes < kHoleLimit && L <= cap_now() &&
+                settle_in_place(min(lo_mod, lo_hole)))
+                lo_mod = L;
+        }
         if (UNLIKELY(lo_mod < L || n_holes >= kHoleLimit || L > cap_now())) {
             const int nx = compact_extract(min(min(lo_mod, lo_hole), L));
             if (nx > kStage) hbm_fence();
