@@ -218,10 +218,12 @@ def main():
         # 100 (M_pi(p) / M_UniBoost(p) - 1)), TTLT at P50 / P90 / P99
         S = w.meta["n_settings"]
         pct = out["pct"].astype(np.float64).reshape(-1, S, 3, 3)[:, :, 1, :]
+        ok = (out["status"] == 0).reshape(-1, S)
         uni = next(s for s in range(S) if int(w.settings["policy"][s]) == W.BOOST)
-        res["config"]["ttlt_slowdown_vs_uniboost_pct"] = {
+        res["config"]["ttlt_slowdown_vs_uniboost_pct"] = {  # traces where both finished
             W.POLICY_NAMES[int(w.settings["policy"][s])] + f"_s{s}":
-            [float(v) for v in (100.0 * (pct[:, s] / pct[:, uni] - 1.0)).mean(axis=0)]
+            [float(v) for v in (100.0 * (pct[:, s] / pct[:, uni] - 1.0))[ok[:, s] & ok[:, uni]]
+             .mean(axis=0)]
             for s in range(S) if s != uni}
     if args.workload == 5 and not args.cluster:  # short and long requests apart
         lat = sim.results()["ttlt"].astype(np.float64) / 1e6
