@@ -19,6 +19,7 @@ settings (a bounded sample of the same sweep).
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -81,8 +82,11 @@ def main():
     ap.add_argument("--workload", type=int, default=4, choices=[0, 1, 2, 3, 4, 5])
     ap.add_argument("--traces", type=int, default=None, help="shrink the sweep (testing)")
     ap.add_argument("--grid", default="sweep",
-                    choices=["sweep", "ada", "comparators", "ladder", "cache"],
+                    choices=["sweep", "ada", "comparators", "ladder", "cache", "sensitivity"],
                     help="settings grid per trace (default: the gamma sweep)")
+    ap.add_argument("--chunk", type=int, default=0,
+                    help="prefill chunk in tokens instead of the workload's (the paper's chunk "
+                         "sensitivity: 128 / 512 / 1024 / 2048)")
     ap.add_argument("--no-ada", action="store_true",
                     help="run the adaptive settings of the grid with gamma fixed at its start")
     ap.add_argument("--cluster", type=int, default=0,
@@ -140,6 +144,9 @@ def main():
     if args.no_ada:
         w.settings["ada"] = 0
         name += " with gamma fixed"
+    if args.chunk:
+        w.engine = dataclasses.replace(w.engine, chunk=args.chunk)
+        name += f", chunk {args.chunk}"
     print(f"[bench] building {name}", file=sys.stderr, flush=True)
     sim = tas.Simulation(w, device=dev, list_cap=args.list_cap)
     stream = torch.cuda.current_stream()

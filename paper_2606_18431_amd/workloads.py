@@ -379,6 +379,23 @@ def starvation_settings(n_traces: int, gamma: float = 1e-3) -> np.ndarray:
     return out
 
 
+def sensitivity_settings(n_traces: int, gamma: float = 1e-3) -> np.ndarray:
+    """Per trace, the paper's sensitivity study (UniBoost at one gamma): the
+    bin size k in {64, 256, 512, 1024} tokens at delta 0.1 s, then the
+    hysteresis delta in {0, 0.3, 0.5} s at k = 256, then FCFS (8 settings).
+    Instance id = trace * 8 + s."""
+    per = [dict(policy=BOOST, gamma=gamma, k=k, memguard=1, delta_us=100_000)
+           for k in (64, 256, 512, 1024)]
+    per += [dict(policy=BOOST, gamma=gamma, k=256, memguard=1, delta_us=d)
+            for d in (0, 300_000, 500_000)]
+    per.append(dict(policy=FCFS))
+    out = np.zeros(n_traces * len(per), dtype=SETTING_DTYPE)
+    for t in range(n_traces):
+        for s, kw in enumerate(per):
+            out[t * len(per) + s] = setting(t, **kw)
+    return out
+
+
 def ada_settings(n_traces: int, ada: dict | None = None) -> np.ndarray:
     """Per trace, 8 settings: for gamma0 in (1e-4, 1e-3, 1e-2) UniBoost with that
     fixed gamma and UniBoost with adaptive gamma started there, then vanilla
@@ -426,7 +443,8 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
     ``grid="comparators"`` replaces the settings grid by comparator_settings,
     ``grid="ada"`` by ada_settings, ``grid="ladder"`` by ladder_settings and
     ``grid="cache"`` by cache_settings, with expected prefix-cache hits drawn
-    by cached_tokens for every trace."""
+    by cached_tokens for every trace, ``grid="sensitivity"`` by
+    sensitivity_settings."""
     T0, S0, N0 = SHAPES[cfg]
     T = T0 if n_traces is None else n_traces
     S = S0 if n_settings is None else n_settings
@@ -448,6 +466,9 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
         S = 8
     elif grid == "cache":
         sets = cache_settings(T)
+        S = 8
+    elif grid == "sensitivity":
+        sets = sensitivity_settings(T)
         S = 8
     elif cfg == 5:
         sets = starvation_settings(T)

@@ -301,3 +301,24 @@ def test_deterministic_and_order_independent(torch):
     g3 = gpu_run(w.subset(perm))
     for key in ("ttft", "ttlt", "tbtmax", "counters", "pct"):
         assert np.array_equal(g3[key], g1[key][perm])
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_parity_sensitivity_grid(torch, cfg):
+    """The paper's sensitivity study: UniBoost over k and delta beside FCFS."""
+    w = W.make(cfg, n_traces=2, n_req=3000, grid="sensitivity")
+    o = oracle.run(w)
+    assert o["rc"] == 0
+    assert_parity(w, gpu_run(w), o)
+
+
+@pytest.mark.parametrize("chunk", [128, 512, 2048])
+def test_parity_chunk_sizes(torch, chunk):
+    """The prefill chunk of the paper's chunk-size study."""
+    import dataclasses
+
+    w = W.make(2, n_traces=1, n_settings=8, n_req=3000)
+    w = dataclasses.replace(w, engine=dataclasses.replace(w.engine, chunk=chunk))
+    o = oracle.run(w)
+    assert o["rc"] == 0
+    assert_parity(w, gpu_run(w), o)
