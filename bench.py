@@ -172,7 +172,12 @@ def main():
     pct_ms = float(np.mean([b.elapsed_time(c) for _, b, c in ev]))
     step_ms = float(np.mean([a.elapsed_time(c) for a, _, c in ev]))
     out = sim.results(latencies=False)
-    if out["rc"] != 0:
+    # LAS can starve a long request past the 32-bit latency range at full load;
+    # the comparator grid reports those instances instead of failing
+    overflowed = int(np.sum(out["status"] == tas.TAS_EOVERFLOW))
+    tolerated = args.grid == "comparators" and bool(
+        np.all(np.isin(out["status"], (0, tas.TAS_EOVERFLOW))))
+    if out["rc"] != 0 and not tolerated:
         print(f"[bench] device error {out['rc']}: {tas.tas_strerror(out['rc'])}", file=sys.stderr)
         sys.exit(1)
     reqiters = int(out["counters"][:, 1].sum())
@@ -200,7 +205,8 @@ def main():
                    "max_seqs": w.engine.max_seqs, "max_tokens": w.engine.max_tokens,
                    "kv_blocks": w.engine.kv_blocks, "request_iterations": reqiters,
                    "iterations": iters, "sim_kernel_ms": sim_ms, "pctl_kernel_ms": pct_ms,
-                   "wall_s": wall, "lds_list_cap": tas.tas_list_cap(sim.ctx)},
+                   "wall_s": wall, "lds_list_cap": tas.tas_list_cap(sim.ctx),
+                   "overflowed_instances": overflowed},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "kernel": "cluster_kernel" if args.cluster and args.dispatch == "jsq"
