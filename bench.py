@@ -226,6 +226,21 @@ def main():
         res["config"]["cluster_p99_tbt_us_mean"] = {
             W.POLICY_NAMES[int(w.settings["policy"][s * stride])] + f"_s{s}":
             float(per[:, s, 2, 2].mean()) for s in range(S)}
+    if not args.cluster:
+        # P99 TTFT / TTLT / TBT (us) per setting, averaged over the traces where
+        # it finished; the 64-setting sweep shows FCFS, SRPT and the UniBoost /
+        # vanilla pair nearest gamma = 1e-3
+        S = w.meta["n_settings"]
+        p99 = out["pct"].astype(np.float64).reshape(-1, S, 3, 3)[:, :, :, 2]
+        ok = (out["status"] == 0).reshape(-1, S)
+        pick = list(range(S))
+        if S > 9:
+            g = np.abs(np.log10(w.settings["gamma"][2:S]) + 3.0)
+            s0 = 2 + 2 * (int(np.argmin(g)) // 2)
+            pick = [0, 1, s0, s0 + 1]
+        res["config"]["p99_us_ttft_ttlt_tbt"] = {
+            W.POLICY_NAMES[int(w.settings["policy"][s])] + f"_s{s}":
+            [float(v) for v in p99[ok[:, s], s].mean(axis=0)] for s in pick if ok[:, s].any()}
     if args.grid == "comparators" and not args.cluster:
         # percentile slowdown against UniBoost on the same trace (the paper's
         # 100 (M_pi(p) / M_UniBoost(p) - 1)), TTLT at P50 / P90 / P99
