@@ -228,7 +228,11 @@ int tas_create(const tas_traces *traces, const tas_params *params, void *d_ws, s
 
 /* Enqueue the simulation of every instance on `stream` (one workgroup per
  * instance), followed by the retry pass for instances that outgrew list_cap.
- * Per-request latencies, counters and errors land in the workspace. */
+ * Per-request latencies, counters and errors land in the workspace. From the
+ * second call on (up to 16384 instances, without replicas) the workgroups
+ * take the instances longest first, by the durations the previous call
+ * recorded: a launch lasts until its last instance ends. The results do not
+ * depend on the order. */
 int tas_run(tas_ctx *ctx, void *stream);
 
 /* Enqueue the nearest-rank percentile reduction: d_out DEVICE uint32
@@ -278,6 +282,14 @@ int tas_replicas(tas_ctx *ctx, int32_t *d_assign, int64_t *d_counters, double *d
  * first per-instance error (lowest instance index), e.g. TAS_ELIVELOCK,
  * TAS_EOVERFLOW, TAS_ECAPACITY; TAS_EHIP if the stream reports a failure. */
 int tas_status(tas_ctx *ctx);
+
+/* The schedule of the latest tas_run: d_dur DEVICE int64 [n_inst], each
+ * instance's wall-clock time on the GPU in 100 MHz ticks (0 before the first
+ * run), and d_order DEVICE int32 [n_inst], the instance each workgroup took
+ * (a permutation; the index order on the first run). Either pointer may be
+ * NULL. TAS_EINVAL where no order is kept (replicas, or more than 16384
+ * instances). */
+int tas_schedule(tas_ctx *ctx, int64_t *d_dur, int32_t *d_order, void *stream);
 
 /* Per-instance status codes, DEVICE int32 [n_inst] (enqueued copy). */
 int tas_instance_status(tas_ctx *ctx, int32_t *d_out, void *stream);

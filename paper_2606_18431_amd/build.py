@@ -9,7 +9,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libtas.so")
-SOURCES = ["tas_abi.hip", "tas_sim.hip", "tas_pctl.hip"]
+SOURCES = ["tas_abi.hip", "tas_sim.hip", "tas_pctl.hip", "tas_order.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 

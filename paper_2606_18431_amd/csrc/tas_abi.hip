@@ -17,6 +17,7 @@
 struct tas_ctx {
     int32_t n_traces = 0, n_req = 0, n_inst = 0, list_cap = 0, spill_cap = 0, retry_cap = 0;
     int32_t replicas = 1;  // > 1: replicas behind a join-shortest-queue router
+    bool ordered = false;  // a run has recorded durations: order the next one
     int64_t lds_bytes = 0, lds_retry = 0;
     tas::SimArgs args{};
     std::vector<tas::DevSetting> settings;
@@ -36,7 +37,7 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 struct Layout {
     size_t arrival, prompt, decode, cached, settings, ada, tfirst, tlast, tbtw, ttft, ttlt, tbtmax,
         counters, status, gamma, switches, spill, ovf, jidx, assign, rcounters, rgamma, rswitches,
-        total;
+        dur, order, total;
 };
 
 // Replicas per instance behind the join-shortest-queue router (1: none).
@@ -145,6 +146,8 @@ bool layout(const tas_traces *t, const tas_params *p, int32_t rc, int32_t sc, La
     L->rcounters = o, o = align256(o + (cl ? slots * 8 * 8 : 0));
     L->rgamma = o, o = align256(o + (cl ? slots * 8 : 0));
     L->rswitches = o, o = align256(o + (cl ? slots * 8 : 0));
+    L->dur = o, o = align256(o + (size_t)p->n_inst * 8);
+    L->order = o, o = align256(o + (size_t)p->n_inst * 4);
     L->total = o;
     return true;
 }
@@ -325,6 +328,13 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     if (ok && n_ada > 0)
         ok = hipMemcpy(ws + L.ada, c->ada.data(), c->ada.size() * sizeof(tas::DevAda),
                        hipMemcpyHostToDevice) == hipSuccess;
+    if (ok && p->n_inst > 0) {  // the first launch runs the instances in index order
+        std::vector<int32_t> iota((size_t)p->n_inst);
+        for (int32_t i = 0; i < p->n_inst; i++) iota[(size_t)i] = i;
+        ok = hipMemcpy(ws + L.order, iota.data(), iota.size() * 4, hipMemcpyHostToDevice) ==
+                 hipSuccess &&
+             hipMemset(ws + L.dur, 0, (size_t)p->n_inst * 8) == hipSuccess;
+    }
     // the fixed-gamma kernel build leaves the adaptive outputs alone: zero them
     if (ok && p->n_inst > 0)
         ok = hipMemset(ws + L.gamma, 0, L.spill - L.gamma) == hipSuccess;
@@ -367,6 +377,9 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     a.rcounters = (int64_t *)(ws + L.rcounters);
     a.rgamma = (double *)(ws + L.rgamma);
     a.rswitches = (int64_t *)(ws + L.rswitches);
+    const bool orderable = c->replicas == 1 && p->n_inst <= tas::kMaxOrdered;
+    a.order = orderable ? (const int32_t *)(ws + L.order) : nullptr;
+    a.dur = orderable ? (int64_t *)(ws + L.dur) : nullptr;
     *out = c;
     return TAS_OK;
 }
@@ -375,7 +388,11 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
 int tas_run(tas_ctx *c, void *stream) {
     if (!c) return TAS_EINVAL;
     c->last_stream = (hipStream_t)stream;
+    if (c->ordered && c->args.order &&
+        tas_launch_order(c->args.dur, const_cast<int32_t *>(c->args.order), c->n_inst, stream))
+        return TAS_EHIP;
     if (launch(c->args, c->lds_bytes, stream)) return TAS_EHIP;
+    c->ordered = c->args.order != nullptr;
     if (c->retry_cap > c->list_cap) {  // rerun instances that outgrew the small list
         tas::SimArgs a2 = c->args;
         a2.list_cap = c->retry_cap;
@@ -461,6 +478,18 @@ int tas_replicas(tas_ctx *c, int32_t *d_assign, int64_t *d_counters, double *d_g
         (d_gamma && hipMemcpyAsync(d_gamma, c->args.rgamma, slots * 8, hipMemcpyDeviceToDevice, s)) ||
         (d_switches && hipMemcpyAsync(d_switches, c->args.rswitches, slots * 8,
                                       hipMemcpyDeviceToDevice, s)))
+        return TAS_EHIP;
+    return TAS_OK;
+}
+
+int tas_schedule(tas_ctx *c, int64_t *d_dur, int32_t *d_order, void *stream) {
+    if (!c || !c->args.order) return TAS_EINVAL;
+    c->last_stream = (hipStream_t)stream;
+    if (c->n_inst == 0) return TAS_OK;
+    const hipStream_t s = (hipStream_t)stream;
+    const size_t n = (size_t)c->n_inst;
+    if ((d_dur && hipMemcpyAsync(d_dur, c->args.dur, n * 8, hipMemcpyDeviceToDevice, s)) ||
+        (d_order && hipMemcpyAsync(d_order, c->args.order, n * 4, hipMemcpyDeviceToDevice, s)))
         return TAS_EHIP;
     return TAS_OK;
 }

@@ -1644,12 +1644,15 @@ DEV void run_cluster(const SimArgs &a, const DevSetting &st, int inst, unsigned 
 template <bool EXT>
 __global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const int inst = blockIdx.x;
-    if (inst >= a.n_inst) return;
+    if ((int)blockIdx.x >= a.n_inst) return;
+    const int inst = a.order ? a.order[blockIdx.x] : (int)blockIdx.x;
     if (a.retry && a.status[inst] != S_ECAPACITY) return;
     const DevSetting &st = a.inst[inst];
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
     if (a.bs == 16) run_instance<4, EXT>(a, st, inst, smem);
     else run_instance<-1, EXT>(a, st, inst, smem);
+    if (a.dur && !a.retry && lane() == 0)  // for the next launch's order
+        a.dur[inst] = (int64_t)(__builtin_amdgcn_s_memrealtime() - t0);
 }
 
 // MAXW: the largest number of waves (replicas) the build serves; 8 leaves

@@ -65,7 +65,7 @@ EXPORTS = ["tas_workspace_bytes", "tas_create", "tas_run", "tas_percentiles",
            "tas_percentiles_grouped", "tas_latencies",
            "tas_counters", "tas_gamma", "tas_status", "tas_instance_status", "tas_destroy",
            "tas_strerror", "tas_boost_table", "tas_ada_grid", "tas_instance_table",
-           "tas_list_cap", "tas_replicas"]
+           "tas_list_cap", "tas_replicas", "tas_schedule"]
 
 _lib = None
 
@@ -94,6 +94,7 @@ def lib():
         L.tas_counters.argtypes = [P, P, P]
         L.tas_gamma.argtypes = [P, P, P, P]
         L.tas_replicas.argtypes = [P, P, P, P, P, P]
+        L.tas_schedule.argtypes = [P, P, P, P]
         L.tas_ada_grid.argtypes = [P, f64, P, P, P]
         L.tas_status.argtypes = [P]
         L.tas_instance_status.argtypes = [P, P, P]
@@ -215,6 +216,10 @@ def tas_gamma(ctx, gamma=None, switches=None, stream=None):
 def tas_replicas(ctx, assign=None, counters=None, gamma=None, switches=None, stream=None):
     _check(lib().tas_replicas(ctx, _ptr(assign), _ptr(counters), _ptr(gamma), _ptr(switches),
                               _stream(stream)), "tas_replicas")
+
+
+def tas_schedule(ctx, dur=None, order=None, stream=None):
+    _check(lib().tas_schedule(ctx, _ptr(dur), _ptr(order), _stream(stream)), "tas_schedule")
 
 
 def tas_ada_grid(setting, tau_us: float = 5000.0):

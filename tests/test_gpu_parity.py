@@ -322,3 +322,32 @@ def test_parity_chunk_sizes(torch, chunk):
     o = oracle.run(w)
     assert o["rc"] == 0
     assert_parity(w, gpu_run(w), o)
+
+
+def test_launch_order_follows_previous_durations(torch):
+    """From the second run on, the workgroups take the instances longest first
+    by the previous run's durations (a permutation), and every run gives the
+    same results, equal to the oracle."""
+    from paper_2606_18431_amd import tas
+
+    w = W.make(2, n_traces=3, n_settings=8, n_req=2000)
+    o = oracle.run(w)
+    sim = tas.Simulation(w)
+    n = w.n_inst
+    dur = torch.zeros(n, dtype=torch.int64, device="cuda")
+    order = torch.zeros(n, dtype=torch.int32, device="cuda")
+    prev = None
+    for k in range(3):
+        print(f"[gpu] launch order, run {k}", flush=True)
+        sim.step()
+        g = sim.results()
+        assert_parity(w, g, o)
+        tas.tas_schedule(sim.ctx, dur, order)
+        d, od = dur.cpu().numpy(), order.cpu().numpy()
+        assert np.all(d > 0) and sorted(od.tolist()) == list(range(n))
+        if prev is None:
+            assert od.tolist() == list(range(n))
+        else:  # longest first, ties by index
+            assert od.tolist() == sorted(range(n), key=lambda i: (-int(prev[i]), i))
+        prev = d.copy()
+    sim.close()
