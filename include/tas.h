@@ -232,7 +232,8 @@ int tas_create(const tas_traces *traces, const tas_params *params, void *d_ws, s
  * second call on (up to 16384 instances, without replicas) the workgroups
  * take the instances longest first, by the durations the previous call
  * recorded: a launch lasts until its last instance ends. The results do not
- * depend on the order. */
+ * depend on the order. Calls on one context share its workspace: a call on
+ * another stream must be ordered after the previous one by the caller. */
 int tas_run(tas_ctx *ctx, void *stream);
 
 /* Enqueue the nearest-rank percentile reduction: d_out DEVICE uint32
