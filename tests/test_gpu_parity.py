@@ -351,3 +351,36 @@ def test_launch_order_follows_previous_durations(torch):
             assert od.tolist() == sorted(range(n), key=lambda i: (-int(prev[i]), i))
         prev = d.copy()
     sim.close()
+
+
+@pytest.mark.parametrize("n", [1000, 16383, 16384])
+def test_launch_order_permutation_at_size(torch, n):
+    """The order kernel at up to its largest size (one LDS sort of 16384):
+    every run's order is a permutation of the instances, longest previous
+    duration first; results of the ordered run equal the oracle on a sample."""
+    from paper_2606_18431_amd import tas
+
+    w = W.make(1, n_traces=256, n_settings=64, n_req=100).subset(np.arange(n))
+    sim = tas.Simulation(w)
+    dur = torch.zeros(n, dtype=torch.int64, device="cuda")
+    order = torch.zeros(n, dtype=torch.int32, device="cuda")
+    prev = None
+    for k in range(2):
+        print(f"[gpu] launch order at {n} instances, run {k}", flush=True)
+        sim.step()
+        tas.tas_schedule(sim.ctx, dur, order)
+        d, od = dur.cpu().numpy(), order.cpu().numpy()
+        assert np.array_equal(np.sort(od), np.arange(n)) and np.all(d > 0)
+        if prev is not None:
+            assert np.array_equal(od, np.lexsort((np.arange(n), -prev)))
+        prev = d.copy()
+    g = sim.results()
+    sim.close()
+    assert g["rc"] == 0
+    sel = np.unique(np.concatenate([np.arange(8), np.arange(n - 8, n),
+                                    np.random.default_rng(n).choice(n, 16, replace=False)]))
+    o = oracle.run(w.subset(sel))
+    for j, i in enumerate(sel):
+        for key in ("ttft", "ttlt", "tbtmax"):
+            assert np.array_equal(g[key][i], o[key][j]), (i, key)
+        assert np.array_equal(g["counters"][i], o["counters"][j]), i
