@@ -107,7 +107,8 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this path runs on one GPU; --gpus {args.gpus} is not supported "
-              "(instances are independent; see the multi-GPU note in DESIGN.md)", file=sys.stderr)
+              "(instances are independent: several GPUs would each take a block of traces)",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
