@@ -282,3 +282,11 @@ def test_jsq_replicas_validation():
     big = W.Engine(max_seqs=256, max_tokens=16384, kv_blocks=32768)
     assert create_rc(w, engine=big, jsq_replicas=16)[0] == tas.TAS_EINVAL  # 16 lists > LDS
     assert create_rc(w, engine=big, ws_bytes=1, jsq_replicas=8)[0] == tas.TAS_ENOMEM
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py runs one GPU; asked for more it exits with a message before
+    touching the GPU."""
+    r = subprocess.run([os.environ.get("PYTHON", "python3"), os.path.join(ROOT, "bench.py"),
+                        "--gpus", "2"], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr

@@ -104,3 +104,23 @@ def test_jsq_rejects():
     assert oracle.jsq(w, 0)["rc"] != 0
     bad = one_trace([5, 0], [4, 4], [2, 2], [W.setting(0, W.FCFS)])
     assert oracle.jsq(bad, 2)["rc"] != 0
+
+
+def test_fast_router_replay_agrees_with_the_slow_one():
+    """The vectorised replay that checks the full-size GPU clusters accepts
+    the oracle's routing and rejects any single changed decision."""
+    from test_gpu_fullsize import replay_router_fast
+
+    R = 4
+    w = cluster(2, R, 200, [dict(policy=W.FCFS), dict(policy=W.BOOST, gamma=1e-3, **W.UNIBOOST)])
+    o = oracle.jsq(w, R)
+    a = w.arrival_us[0]
+    rng = np.random.default_rng(3)
+    for i in range(w.n_inst):
+        asg, ttlt = o["assign"][i], o["ttlt"][i]
+        replay_router(a, asg, ttlt, R)
+        assert replay_router_fast(a, asg, ttlt, R)
+        for j in rng.choice(len(a), 20, replace=False):
+            bad = asg.copy()
+            bad[j] = (bad[j] + 1 + rng.integers(R - 1)) % R
+            assert not replay_router_fast(a, bad, ttlt, R), j
