@@ -35,7 +35,7 @@ constexpr int64_t kTwo40 = int64_t(1) << 40;  // DistBoost tables: decode keys s
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-    size_t arrival, prompt, decode, cached, settings, ada, tfirst, tlast, tbtw, ttft, ttlt, tbtmax,
+    size_t arrival, prompt, decode, cached, settings, ada, tfirst, tlast, ttft, ttlt, tbtmax,
         counters, status, gamma, switches, spill, ovf, jidx, assign, rcounters, rgamma, rswitches,
         dur, order, total;
 };
@@ -44,11 +44,24 @@ struct Layout {
 int32_t replicas_of(const tas_params *p) { return p->jsq_replicas > 1 ? p->jsq_replicas : 1; }
 
 // Dynamic LDS of a launch: one list per instance, or the router block and
-// one 16-aligned list per replica.
-int64_t launch_lds(int32_t list_cap, int32_t wmax, int32_t replicas) {
+// one 16-aligned list per replica (replicas use four-word slots).
+int64_t launch_lds(int32_t list_cap, int32_t wmax, int32_t replicas, bool compact) {
+    if (replicas <= 1) return tas::lds_bytes_for(list_cap, wmax, compact);
     const int64_t one = tas::lds_bytes_for(list_cap, wmax);
-    if (replicas <= 1) return one;
     return tas::kJsqLdsBytes + (int64_t)replicas * ((one + 15) & ~int64_t(15));
+}
+
+// Compact list slots (24 LDS bytes per entry instead of 32) hold w = P + dec
+// and kv in 16 bits and left - 1 in 15: usable when every request has
+// P + D <= 65535 and D <= 32768, and the instance is a single server.
+bool compact_ok(const tas_traces *t, const tas_params *p) {
+    if (replicas_of(p) > 1) return false;
+    const size_t tn = (size_t)t->n_traces * (size_t)t->n_req;
+    for (size_t i = 0; i < tn; i++) {
+        const int64_t P = t->prompt[i], D = t->decode[i];
+        if (P + D > tas::kCompactMaxPD || D > tas::kCompactMaxD) return false;
+    }
+    return true;
 }
 
 // Adaptive-gamma instances and their largest window (clamped: an invalid
@@ -67,16 +80,32 @@ int32_t ada_count(const tas_params *p, int32_t *wmax) {
 // First pass: room for about max_seqs residents plus a window of waiting
 // entries, small enough for several instances per compute unit. Instances
 // that hold more residents than that rerun in a second pass with a large list.
+// The kernel is bound by each wavefront's dependent instruction chain, so the
+// number of instances sharing a compute unit (its LDS divided by an
+// instance's) matters more than the last waiting entries on chip: the list
+// holds max_seqs + 128 entries, shrunk (not below max_seqs + 64, in steps of
+// 8) to the largest size at which 16, or else 12, instances fit. (On the
+// large sweep, 256 sequences: 352 compact entries, 16 per compute unit.)
 // With adaptive gamma every grid change reorders the queue; requests admitted
 // under the old order keep their KV until the budget binds, so residents
 // outside the batch accumulate (beyond 3 max_seqs on the large sweep):
-// launches with adaptive instances start with 640 more entries, so that a
+// launches with adaptive instances start with 768 more entries, so that a
 // rerun is rare (the adaptive build keeps only residents + 128 on chip, so
 // the larger list costs occupancy, not longer passes).
-int32_t default_list_cap(int32_t max_seqs, bool adaptive) {
-    int64_t lc = (int64_t)max_seqs + (adaptive ? 768 : 128);
-    lc = (lc + 63) / 64 * 64;
-    return (int32_t)std::min<int64_t>(lc, tas::kMaxListCap);
+int32_t default_list_cap(int32_t max_seqs, bool adaptive, bool compact) {
+    if (adaptive) {
+        const int64_t lc = ((int64_t)max_seqs + 768 + 63) / 64 * 64;
+        return (int32_t)std::min<int64_t>(lc, tas::kMaxListCap);
+    }
+    const int64_t lo = (int64_t)max_seqs + 64, hi = (int64_t)max_seqs + 128;
+    for (const int64_t per_cu : {16, 12}) {
+        int64_t l = hi;
+        while (l >= lo && tas::lds_bytes_for((int32_t)std::min<int64_t>(l, tas::kMaxListCap), 0,
+                                             compact) * per_cu > kMaxLds)
+            l = (l - 1) / 8 * 8;
+        if (l >= lo) return (int32_t)std::min<int64_t>(l, tas::kMaxListCap);
+    }
+    return (int32_t)std::min<int64_t>(hi, tas::kMaxListCap);
 }
 int32_t default_retry_cap(int32_t list_cap) {
     return (int32_t)std::min<int64_t>(std::max<int64_t>(4 * (int64_t)list_cap, 2048),
@@ -98,21 +127,26 @@ bool shape_ok(const tas_traces *t) {
            t->prompt && t->decode;
 }
 
-// Effective capacities; false if invalid. *rc == *lc means no second pass.
-bool caps(const tas_traces *t, const tas_params *p, int32_t *lc, int32_t *rc, int32_t *sc) {
+// Effective capacities and slot layout; false if invalid. *rc == *lc means
+// no second pass.
+bool caps(const tas_traces *t, const tas_params *p, int32_t *lc, int32_t *rc, int32_t *sc,
+          bool *cp) {
     int32_t wmax;
     const bool adaptive = ada_count(p, &wmax) > 0;
-    const int32_t l = p->list_cap ? p->list_cap : default_list_cap(p->max_seqs, adaptive);
+    const bool compact = compact_ok(t, p);
+    const int32_t l =
+        p->list_cap ? p->list_cap : default_list_cap(p->max_seqs, adaptive, compact);
     if ((int64_t)l < (int64_t)p->max_seqs + 64 || l > tas::kMaxListCap) return false;
     const int32_t nr = replicas_of(p);
-    if (launch_lds(l, wmax, nr) > kMaxLds) return false;
+    if (launch_lds(l, wmax, nr, compact) > kMaxLds) return false;
     int32_t r = p->retry_cap ? p->retry_cap : default_retry_cap(l);
     if (r < l) r = l;
-    while (r > l && launch_lds(r, wmax, nr) > kMaxLds) r -= 64;  // room for the window
-    if (r > tas::kMaxListCap || tas::lds_bytes_for(r, wmax) > kMaxLds) return false;
+    while (r > l && launch_lds(r, wmax, nr, compact) > kMaxLds) r -= 64;  // room for the window
+    if (r > tas::kMaxListCap || tas::lds_bytes_for(r, wmax, compact) > kMaxLds) return false;
     *lc = l;
     *rc = r;
     *sc = p->spill_cap ? p->spill_cap : t->n_req;
+    *cp = compact;
     return true;
 }
 
@@ -129,7 +163,6 @@ bool layout(const tas_traces *t, const tas_params *p, int32_t rc, int32_t sc, La
     L->ada = o, o = align256(o + (size_t)ada_count(p, &wmax) * sizeof(tas::DevAda));
     L->tfirst = o, o = align256(o + in * 8);
     L->tlast = o, o = align256(o + in * 8);
-    L->tbtw = o, o = align256(o + in * 4);
     L->ttft = o, o = align256(o + in * 4);
     L->ttlt = o, o = align256(o + in * 4);
     L->tbtmax = o, o = align256(o + in * 4);
@@ -234,7 +267,8 @@ int tas_ada_grid(const tas_setting *s, double tau_us, double *grid, double *boun
 size_t tas_workspace_bytes(const tas_traces *t, const tas_params *p) {
     if (!shape_ok(t) || !p || !engine_ok(p)) return 0;
     int32_t lc, rc, sc;
-    if (!caps(t, p, &lc, &rc, &sc)) return 0;
+    bool cp;
+    if (!caps(t, p, &lc, &rc, &sc, &cp)) return 0;
     Layout L;
     layout(t, p, rc, sc, &L);
     return L.total;
@@ -246,7 +280,8 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     *out = nullptr;
     if (!shape_ok(t) || !p || !engine_ok(p)) return TAS_EINVAL;
     int32_t lc, rc, sc;
-    if (!caps(t, p, &lc, &rc, &sc)) return TAS_EINVAL;
+    bool cp;
+    if (!caps(t, p, &lc, &rc, &sc, &cp)) return TAS_EINVAL;
     const int32_t N = t->n_req;
     const size_t tn = (size_t)t->n_traces * (size_t)N;
     // traces: sorted, in range; P, D >= 1; P + D < 2^24
@@ -278,8 +313,8 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     int32_t wmax;
     const int32_t n_ada = ada_count(p, &wmax);
     c->replicas = replicas_of(p);
-    c->lds_bytes = launch_lds(lc, wmax, c->replicas);
-    c->lds_retry = launch_lds(rc, wmax, c->replicas);
+    c->lds_bytes = launch_lds(lc, wmax, c->replicas, cp);
+    c->lds_retry = launch_lds(rc, wmax, c->replicas, cp);
     c->settings.resize((size_t)p->n_inst);
     c->ada.resize((size_t)n_ada);
     int32_t ai = 0;
@@ -350,7 +385,6 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     a.inst = (const tas::DevSetting *)(ws + L.settings);
     a.tfirst = (int64_t *)(ws + L.tfirst);
     a.tlast = (int64_t *)(ws + L.tlast);
-    a.tbtw = (uint32_t *)(ws + L.tbtw);
     a.ttft = (uint32_t *)(ws + L.ttft);
     a.ttlt = (uint32_t *)(ws + L.ttlt);
     a.tbtmax = (uint32_t *)(ws + L.tbtmax);
@@ -370,6 +404,7 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     a.switch_out = (int64_t *)(ws + L.switches);
     a.ada_window = wmax;
     a.ext = ext ? 1 : 0;
+    a.cp = cp ? 1 : 0;
     a.replicas = c->replicas;
     a.wave_lds = (int32_t)((tas::lds_bytes_for(lc, wmax) + 15) & ~int64_t(15));
     a.jidx = (int32_t *)(ws + L.jidx);

@@ -48,7 +48,7 @@ struct Rec {
     int32_t kv;    // tokens with resident KV
     uint32_t gs;   // flags, guard, level and this iteration's chunk (see the kernel)
     uint32_t tl;   // time of the last emitted token, modulo 2^32 (us)
-    uint32_t unused;
+    uint32_t gm;   // largest inter-token gap so far (us)
 };
 
 struct SimArgs {
@@ -58,10 +58,9 @@ struct SimArgs {
     const DevSetting *inst;  // [n_inst]
     int64_t *tfirst;         // [n_inst][n_req] absolute time of the first token
     int64_t *tlast;          // [n_inst][n_req] absolute time of the last token
-    uint32_t *tbtw;          // [n_inst][n_req] max gap, raised by atomic max
     uint32_t *ttft;          // [n_inst][n_req] outputs, relative to arrival
     uint32_t *ttlt;
-    uint32_t *tbtmax;
+    uint32_t *tbtmax;        // written at completion from the on-chip running maximum
     int64_t *counters;       // [n_inst][8]
     int32_t *status;         // [n_inst]
     Rec *spill;              // [n_inst][spill_cap]
@@ -81,6 +80,7 @@ struct SimArgs {
     int32_t ada_window;  // largest window over the adaptive instances (LDS), 0 if none
     int32_t ext;         // some instance needs the extended build (adaptive gamma,
                          // the phase-aware or cache-aware signal, DistBoost)
+    int32_t cp;          // compact list slots: every request has P + D < 2^16, D <= 2^15
     const int32_t *cached;  // [n_traces][n_req] expected prefix-cache hits, or
                             // null (read by the cache-aware signal only)
     // replicas behind a join-shortest-queue router (cluster_kernel only)
@@ -109,13 +109,22 @@ inline int64_t ada_lds_bytes(int32_t window) {
     return window > 0 ? kAdaStateBytes + int64_t(window) * 8 : 0;
 }
 
-// Dynamic LDS bytes per workgroup for a list capacity and the largest
-// adaptive-gamma window (0: none).
-inline int64_t lds_bytes_for(int32_t list_cap, int32_t ada_window = 0) {
+// LDS bytes per candidate-list slot: the packed key (8 B), the last token
+// time and gap maximum (8 B), and the state {gs, w, kv, left} in 16 B, or in
+// 8 B with compact slots.
+constexpr int64_t kSlotBytes = 8 + 8 + 16;
+constexpr int64_t kCompactSlotBytes = 8 + 8 + 8;
+constexpr int32_t kCompactMaxPD = (1 << 16) - 1;  // compact slots: P + D <= this
+constexpr int32_t kCompactMaxD = 1 << 15;         // and D <= this
+
+// Dynamic LDS bytes per workgroup for a list capacity, the largest
+// adaptive-gamma window (0: none) and the slot layout.
+inline int64_t lds_bytes_for(int32_t list_cap, int32_t ada_window = 0, bool compact = false) {
     const int64_t cap = int64_t(list_cap) + kStage;  // the list and its overflow region
-    // pk (8 B) + gs, w, kv, left, tl (4 B) per slot; alignment of the boost
-    // table; the boost table; the adaptive-gamma block
-    return cap * (8 + 5 * 4) + 8 + kLevels * 8 + ada_lds_bytes(ada_window);
+    // the slots; alignment of the boost table; the boost table; the
+    // adaptive-gamma block
+    return cap * (compact ? kCompactSlotBytes : kSlotBytes) + 8 + kLevels * 8 +
+           ada_lds_bytes(ada_window);
 }
 constexpr int kMaxChunk = (1 << 15) - 1;  // the chunk size lives in 15 bits of the flag word
 // At most 64 chunks of 64 entries (list + overflow region): chunk bitmaps are

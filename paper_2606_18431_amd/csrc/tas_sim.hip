@@ -53,8 +53,8 @@ constexpr uint32_t G_DIRTY = 1u << 10;   // key moved: re-insert
 constexpr uint32_t G_MARK = 1u << 11;    // selected for spilling
 constexpr int G_LVL_SHIFT = 12;          // current MemGuard level (5 bits)
 constexpr uint32_t G_LVL = 0x1fu << G_LVL_SHIFT;
-constexpr int G_N_SHIFT = 17;            // tokens scheduled this iteration (15 bits)
-constexpr uint32_t G_LOW = (1u << G_N_SHIFT) - 1;
+constexpr uint32_t G_FLAGS = 0x1ffffu;   // the flags and levels: bits 0..16
+constexpr int kLeftShift = 17;           // compact slots: left - 1 in bits 17..31
 constexpr int kHoleLimit = 16;           // compact once this many holes accumulate
 
 enum { S_OK = 0, S_EOVERFLOW = -5, S_ELIVELOCK = -6, S_ESTATE = -7, S_ECAPACITY = -8 };
@@ -179,15 +179,21 @@ DEV int level_of(int w, int k, int lk) {
 
 // ------------------------------------------------------------ LDS layout
 
-// LDS holds the candidate list as three parallel arrays: a 16-byte quad
-// {gs, w, kv, left} (what formation reads, one 128-bit load per lane), the
-// packed key (searches and merges) and the last token time tl (emission
-// only). The maximum inter-token gap lives in HBM, raised by atomic max, so
-// an entry takes 28 bytes of LDS.
+// LDS holds the candidate list as three parallel arrays: the slot state
+// {gs, w, kv, left} (what formation reads, one load per lane), the packed
+// key (searches and merges) and the pair {tl, gm} of the last token time and
+// the largest inter-token gap so far (emission only). The gap maximum stays
+// on chip until the request completes, so the per-token work touches no HBM.
+// The slot state takes 16 bytes, or 8 in the compact layout used when every
+// request has P + D < 2^16 and D <= 2^15: w and kv in 16 bits each, left - 1
+// in the flag word's bits 17..31 (the flags use bits 0..16). An entry is then
+// 24 bytes instead of 32, which lets 16 instead of 12 instances share a
+// compute unit's LDS at the large sweep's list size.
 struct Lds {
-    uint4 *q;
+    uint4 *q;   // four-word slots
+    uint2 *q2;  // compact slots
     uint64_t *k;
-    uint32_t *tl;
+    uint2 *tg;
     int64_t *bt;
     struct AdaLds *as;  // adaptive gamma: state, then the window in completion
     uint32_t *wr, *ws;  // order (a ring) and sorted
@@ -206,28 +212,17 @@ static_assert(sizeof(AdaLds) == kAdaStateBytes, "adaptive-gamma LDS block");
 struct R {  // one candidate-list record in registers
     uint64_t pk = 0;
     int w = 0, left = 0, kv = 0;
-    uint32_t gs = 0, tl = 0;
+    uint32_t gs = 0, tl = 0, gm = 0;
 };
 
-DEV void ldr(const Lds &S, int i, R &x) {
-    const uint4 q = S.q[i];
-    x.gs = q.x, x.w = (int)q.y, x.kv = (int)q.z, x.left = (int)q.w;
-    x.pk = S.k[i];
-    x.tl = S.tl[i];
-}
-DEV void str(const Lds &S, int i, const R &x) {
-    S.q[i] = make_uint4(x.gs, (uint32_t)x.w, (uint32_t)x.kv, (uint32_t)x.left);
-    S.k[i] = x.pk;
-    S.tl[i] = x.tl;
-}
 DEV R from_rec(const Rec &r) {
     R x;
-    x.pk = r.pk, x.w = r.w, x.left = r.left, x.kv = r.kv, x.gs = r.gs, x.tl = r.tl;
+    x.pk = r.pk, x.w = r.w, x.left = r.left, x.kv = r.kv, x.gs = r.gs, x.tl = r.tl, x.gm = r.gm;
     return x;
 }
 DEV Rec to_rec(const R &x) {
     Rec r;
-    r.pk = x.pk, r.w = x.w, r.left = x.left, r.kv = x.kv, r.gs = x.gs, r.tl = x.tl, r.unused = 0;
+    r.pk = x.pk, r.w = x.w, r.left = x.left, r.kv = x.kv, r.gs = x.gs, r.tl = x.tl, r.gm = x.gm;
     return r;
 }
 DEV R shfl_rec(const R &x, int src) {
@@ -238,6 +233,7 @@ DEV R shfl_rec(const R &x, int src) {
     y.kv = __shfl(x.kv, src);
     y.gs = (uint32_t)__shfl((int)x.gs, src);
     y.tl = (uint32_t)__shfl((int)x.tl, src);
+    y.gm = (uint32_t)__shfl((int)x.gm, src);
     return y;
 }
 DEV bool is_waiting(uint32_t g) { return (g & (G_RES | G_DONE)) == 0; }
@@ -265,6 +261,7 @@ DEV R permute_rec(const R &x, int dest) {
     y.kv = (int)perm32(dest, (uint32_t)x.kv);
     y.gs = perm32(dest, x.gs);
     y.tl = perm32(dest, x.tl);
+    y.gm = perm32(dest, x.gm);
     return y;
 }
 
@@ -276,7 +273,8 @@ DEV R permute_rec(const R &x, int dest) {
 // different policies on one compute unit share the instruction cache.
 // CL: one replica of a cluster behind a join-shortest-queue router; its
 // arrivals are the global requests the router has dispatched to it so far.
-template <int BSH, bool EXT, bool CL = false>
+// CP: compact slots (see Lds).
+template <int BSH, bool EXT, bool CL = false, bool CP = false>
 struct Sim {
     const SimArgs &A;
     Lds S;
@@ -287,7 +285,7 @@ struct Sim {
     const int64_t *arr;
     const int32_t *Pp, *Dp;
     int64_t *tfirst, *tlast;
-    uint32_t *tbtw;
+    uint32_t *tbo;  // the instance's max-gap outputs, written at completion
     Rec *spill, *ovf;
     // state
     int64_t t;
@@ -307,6 +305,12 @@ struct Sim {
     int64_t sum_ctx;
     uint64_t emit_chunks;  // 64-entry chunks holding batch members or evictions
     bool emit_all;         // ranks moved during formation: visit every chunk
+    // Repeated batch: the next iteration's formation would select every
+    // resident with one token each and nothing else (see run), so it is
+    // skipped. Emission reports whether every batch member emitted a token
+    // and how many new KV blocks the members need for their next token.
+    bool rep, all_emit;
+    int du_next;
     // entries extracted by compact_extract, lanes [0, min(count, kStage));
     // the rest go to the per-instance HBM overflow
     R stage;
@@ -338,7 +342,7 @@ struct Sim {
         const size_t toff = (size_t)st.trace * (size_t)N;
         arr = a.arrival + toff, Pp = a.prompt + toff, Dp = a.decode + toff;
         const size_t ioff = (size_t)i * (size_t)N;
-        tfirst = a.tfirst + ioff, tlast = a.tlast + ioff, tbtw = a.tbtw + ioff;
+        tfirst = a.tfirst + ioff, tlast = a.tlast + ioff, tbo = a.tbtmax + ioff;
         wv = w, Nk = 0, pidx = 0, last_done = 0;
         jl = nullptr;
         const size_t slot = CL ? (size_t)i * (size_t)a.replicas + (size_t)w : (size_t)i;
@@ -347,10 +351,11 @@ struct Sim {
         if constexpr (CL) jl = a.jidx + slot * (size_t)N;
         const int cap = lcap + kStage;  // the list may use its overflow region during formation
         size_t o = 0;
-        S.q = (uint4 *)(smem + o), o += (size_t)cap * 16;
+        S.q = nullptr, S.q2 = nullptr;
+        if constexpr (CP) S.q2 = (uint2 *)(smem + o), o += (size_t)cap * 8;
+        else S.q = (uint4 *)(smem + o), o += (size_t)cap * 16;
         S.k = (uint64_t *)(smem + o), o += (size_t)cap * 8;
-        S.tl = (uint32_t *)(smem + o), o += (size_t)cap * 4;
-        o = (o + 7) & ~(size_t)7;
+        S.tg = (uint2 *)(smem + o), o += (size_t)cap * 8;
         S.bt = (int64_t *)(smem + o), o += (size_t)kLevels * 8;
         for (int j = lane(); j < kLevels; j += kWave) S.bt[j] = st.bt[j];
         ad = nullptr;
@@ -384,6 +389,8 @@ struct Sim {
         sum_ctx = 0;
         emit_chunks = 0;
         emit_all = false;
+        rep = all_emit = false;
+        du_next = 0;
         vm_res = vm_ev = 0;
         vm_ok = false;
         wsync();
@@ -391,6 +398,59 @@ struct Sim {
 
     DEV void fail(int code) {
         if (status == 0) status = code;
+    }
+
+    // ---------------------------------------------------------- slots
+
+    // The state of slot i as loaded: the flag word in .x (compact: with
+    // left - 1 above the flags), the rest unpacked by sw / skv / sleft.
+    DEV uint4 ldq(int i) const {
+        if constexpr (CP) {
+            const uint2 v = S.q2[i];
+            return make_uint4(v.x, v.y, 0u, 0u);
+        } else {
+            return S.q[i];
+        }
+    }
+    DEV int sw(const uint4 &v) const { return CP ? (int)(v.y & 0xffffu) : (int)v.y; }
+    DEV int skv(const uint4 &v) const { return CP ? (int)(v.y >> 16) : (int)v.z; }
+    DEV int sleft(const uint4 &v) const {
+        return CP ? (int)(v.x >> kLeftShift) + 1 : (int)v.w;
+    }
+    DEV void stq(int i, uint32_t x, int w, int kv, int left) const {
+        if constexpr (CP) {
+            S.q2[i] = make_uint2((x & G_FLAGS) | ((uint32_t)(left - 1) << kLeftShift),
+                                 (uint32_t)w | ((uint32_t)kv << 16));
+        } else {
+            S.q[i] = make_uint4(x, (uint32_t)w, (uint32_t)kv, (uint32_t)left);
+        }
+    }
+    // the flag word alone (flag edits keep the compact layout's left bits)
+    DEV uint32_t ldx(int i) const { return CP ? S.q2[i].x : S.q[i].x; }
+    DEV void stx(int i, uint32_t x) const {
+        if constexpr (CP) S.q2[i].x = x;
+        else S.q[i].x = x;
+    }
+    // the flag word (as loaded, flags edited) and kv of a slot whose w is w
+    DEV void stxkv(int i, uint32_t x, int w, int kv) const {
+        if constexpr (CP) {
+            S.q2[i] = make_uint2(x, (uint32_t)w | ((uint32_t)kv << 16));
+        } else {
+            S.q[i].x = x;
+            S.q[i].z = (uint32_t)kv;
+        }
+    }
+    DEV void ldr(int i, R &x) const {
+        const uint4 q = ldq(i);
+        x.gs = q.x, x.w = sw(q), x.kv = skv(q), x.left = sleft(q);
+        x.pk = S.k[i];
+        const uint2 tg = S.tg[i];
+        x.tl = tg.x, x.gm = tg.y;
+    }
+    DEV void str(int i, const R &x) const {
+        stq(i, x.gs, x.w, x.kv, x.left);
+        S.k[i] = x.pk;
+        S.tg[i] = make_uint2(x.tl, x.gm);
     }
     // Entries the list keeps before spilling waiting ones. The adaptive build
     // sizes the waiting window from the residents (max(M, residents) + 128,
@@ -530,13 +590,13 @@ struct Sim {
                 const bool go = mv && sh > 0;
                 if (ballot(go)) vm_ok = false;
                 R y;
-                if (go) ldr(S, r, y);
+                if (go) ldr(r, y);
                 wsync();
-                if (go) str(S, r + sh, y);
+                if (go) str(r + sh, y);
                 wsync();
             }
         }
-        if (act) str(S, minpos + pos_in + rn, x);
+        if (act) str(minpos + pos_in + rn, x);
         wsync();
         L += K;
     }
@@ -549,13 +609,13 @@ struct Sim {
             const int r = b + lane();
             const bool v = r >= from && r < L;
             R y;
-            if (v) ldr(S, r, y);
+            if (v) ldr(r, y);
             const bool keep = v && !(y.gs & mask);
             const uint64_t km = ballot(keep);
             wsync();
             if (keep) {
                 const int d = out + mbcnt(km);
-                if (d != r) str(S, d, y);
+                if (d != r) str(d, y);
             }
             wsync();
             out += popc(km);
@@ -585,15 +645,15 @@ struct Sim {
         int found = 0, lowest = L;
         for (int b = ((L - 1) >> 6) << 6; b >= 0 && found < E; b -= kWave) {
             const int r = b + lane();
-            const bool isw = r < L && is_waiting(S.q[r].x);
+            const bool isw = r < L && is_waiting(ldx(r));
             const uint64_t m = ballot(isw);
             const int above = popc(m) - mbcnt(m) - 1;
             const bool take = isw && above < E - found;
             if (take) {
                 R y;
-                ldr(S, r, y);
+                ldr(r, y);
                 spill[spill_n + found + above] = to_rec(y);
-                S.q[r].x = y.gs | G_MARK;
+                stx(r, y.gs | G_MARK);
             }
             const uint64_t tm = ballot(take);
             found += popc(tm);
@@ -725,7 +785,7 @@ struct Sim {
         vm_res = vm_ev = 0;
         for (int c = 0; c < nch; c++) {
             const int r = c * kWave + lane();
-            const uint32_t g = r < L ? S.q[r].x : 0u;
+            const uint32_t g = r < L ? ldx(r) : 0u;
             const bool rs = (g & G_RES) != 0;
             bool ev = rs;
             if (memguard) ev = rs && ((g >> G_LVL_SHIFT) & 31u) > (g & G_GUARD);
@@ -736,7 +796,7 @@ struct Sim {
                 if (rs) {
                     const int idx = idx_of(S.k[r]);
                     Dv = idx < N ? Dp[idx] : 0;
-                    lv = (int)S.q[r].w;
+                    lv = CP ? (int)(g >> kLeftShift) + 1 : (int)S.q[r].w;
                 }
                 ev = rs && !(2 * Dv >= 5 * lv);
             }
@@ -797,14 +857,12 @@ struct Sim {
     }
 
     DEV void do_evict(int v) {
-        const uint4 qv = S.q[v];
-        const int kvv = uni((int)qv.z);
+        const uint4 qv = ldq(v);
+        const int kvv = uni(skv(qv)), wv_ = uni(sw(qv));
         const uint32_t g = (uint32_t)uni((int)qv.x);
         wsync();
-        if (lane() == 0) {
-            S.q[v].x = (g & ~G_RES) | G_EVI | (pol == P_SRPT || pol == P_TRAIL ? G_DIRTY : 0u);
-            S.q[v].z = 0;
-        }
+        if (lane() == 0)
+            stxkv(v, (g & ~G_RES) | G_EVI | (pol == P_SRPT || pol == P_TRAIL ? G_DIRTY : 0u), wv_, 0);
         wsync();
         U -= blocks(kvv);
         nW++;
@@ -813,12 +871,14 @@ struct Sim {
         vm_set(v, false);
     }
 
-    DEV void admit_one(int q, uint32_t g, int n, int du, int kvv) {
+    // Admission of candidate q with n tokens: its KV advances now (emission
+    // finds the tokens scheduled this iteration already counted).
+    DEV void admit_one(int q, uint32_t g, int n, int du, int kvv, int wq) {
         const bool res = (g & G_RES) != 0;
         if (lane() == 0) {
-            uint32_t g2 = (g & G_LOW) | G_INB | ((uint32_t)n << G_N_SHIFT);
+            uint32_t g2 = g | G_INB;
             if (!res) g2 = (g2 & ~G_GUARD) | G_RES | ((g >> G_LVL_SHIFT) & 31u);
-            S.q[q].x = g2;
+            stxkv(q, g2, wq, kvv + n);
         }
         wsync();
         cnt++;
@@ -834,12 +894,13 @@ struct Sim {
 
     // Candidate q did not fit: evictions, or closing admissions. r_ahead
     // counts residents at ranks > q.
-    // (g, n, du, kvv: its flag word, chunk size, KV blocks and KV tokens)
-    DEV void slow_path(int q, uint32_t g, int n, int du, int kvv, bool &closed, int &r_ahead) {
+    // (g, n, du, kvv, wq: its flag word, chunk size, KV blocks, KV tokens and w)
+    DEV void slow_path(int q, uint32_t g, int n, int du, int kvv, int wq, bool &closed,
+                       int &r_ahead) {
         const bool res = (g & G_RES) != 0;
         for (int it = 0; it <= L + 1; it++) {
             if (U + du <= Kb) {
-                admit_one(q, g, n, du, kvv);
+                admit_one(q, g, n, du, kvv, wq);
                 return;
             }
             int v = find_victim(q, true);
@@ -919,12 +980,12 @@ struct Sim {
             uint4 qr = nx;
             if (!have_nx) {
                 qr = make_uint4(0u, 0u, 0u, 0u);
-                if (r < lim) qr = S.q[r];
+                if (r < lim) qr = ldq(r);
             }
-            if (r + kWave < lim) nx = S.q[r + kWave];
+            if (r + kWave < lim) nx = ldq(r + kWave);
             const uint32_t g = valid ? qr.x : 0u;
-            const int w = (int)qr.y;
-            const int kvv = (int)qr.z;
+            const int w = sw(qr);
+            const int kvv = skv(qr);
             const bool res = (g & G_RES) != 0;
             const bool cand = valid && !(g & (G_EVI | G_DONE)) && (res || !closed);
             // one round of scans: the candidates admitted from this chunk
@@ -948,10 +1009,10 @@ struct Sim {
             const uint64_t am = ballot(adm);
             const uint64_t okm = bad ? (am & ((1ull << ffs0(bad)) - 1ull)) : am;
             const bool ok = ((okm >> lane()) & 1ull) != 0;
-            if (ok) {
-                uint32_t g2 = (g & G_LOW) | G_INB | ((uint32_t)n << G_N_SHIFT);
+            if (ok) {  // admitted: the KV advances by this iteration's chunk now
+                uint32_t g2 = g | G_INB;
                 if (!res) g2 = (g2 & ~G_GUARD) | G_RES | ((g >> G_LVL_SHIFT) & 31u);
-                S.q[r].x = g2;
+                stxkv(r, g2, w, kvv + n);
             }
             if (okm) {
                 const int last = fls0(okm);
@@ -983,7 +1044,7 @@ struct Sim {
                 // waiting entries admitted in this chunk sit below q
                 r_ahead -= popc(resm & (ql == 63 ? ~0ull : ((2ull << ql) - 1ull)));
                 slow_path(p + ql, (uint32_t)rl((int)g, ql), rl(n, ql), rl(du, ql), rl(kvv, ql),
-                          closed, r_ahead);
+                          rl(w, ql), closed, r_ahead);
                 if (status) return;
                 p = p + ql + 1;
                 have_nx = false;
@@ -998,10 +1059,15 @@ struct Sim {
 
     // ---------------------------------------------------------- execute
 
-    // Returns the lowest rank whose key moved (INT32_MAX if none).
-    DEV int emission(int64_t t_end) {
+    // Returns the lowest rank whose key moved (INT32_MAX if none). Batch
+    // members are the entries whose flags meet `mem` (G_INB; in a repeated
+    // batch also G_RES), with `n1` added to their scheduled tokens (1 in a
+    // repeated batch, whose entries carry no token count).
+    DEV int emission(int64_t t_end, uint32_t mem, int n1) {
         int lo = INT32_MAX, lohole = INT32_MAX, nd = 0, ufree = 0;
         bool bad_idx = false;
+        uint64_t noemit = 0;  // batch members that emitted no token
+        int dnext = 0;        // members whose next token opens a KV block
         const uint32_t t32 = (uint32_t)t_end;
         const int nch = (L + kWave - 1) >> 6;
         uint64_t todo = emit_all ? (nch >= 64 ? ~0ull : ((1ull << nch) - 1ull)) : emit_chunks;
@@ -1012,22 +1078,24 @@ struct Sim {
         todo &= todo - 1;
         uint4 q = make_uint4(0u, 0u, 0u, 0u);
         uint64_t pk = 0;
-        uint32_t tl = 0;
-        if (b + lane() < L) q = S.q[b + lane()], pk = S.k[b + lane()], tl = S.tl[b + lane()];
+        uint2 tg = make_uint2(0u, 0u);
+        if (b + lane() < L) q = ldq(b + lane()), pk = S.k[b + lane()], tg = S.tg[b + lane()];
         for (;;) {
             const int bn = todo ? ffs0(todo) * kWave : -1;
             todo &= todo - 1;
             uint4 qn = make_uint4(0u, 0u, 0u, 0u);
             uint64_t pkn = 0;
-            uint32_t tln = 0;
+            uint2 tgn = make_uint2(0u, 0u);
             if (bn >= 0 && bn + lane() < L)
-                qn = S.q[bn + lane()], pkn = S.k[bn + lane()], tln = S.tl[bn + lane()];
+                qn = ldq(bn + lane()), pkn = S.k[bn + lane()], tgn = S.tg[bn + lane()];
             const int r = b + lane();
             const uint32_t g = q.x;
-            bool chg = false, fin = false;
-            if (g & G_INB) {
-                int w = (int)q.y, kv = (int)q.z + (int)(g >> G_N_SHIFT), left = (int)q.w;
-                uint32_t gs = g & G_LOW & ~G_INB;
+            bool chg = false, fin = false, mute = false, opens = false;
+            if (g & mem) {
+                // kv includes this iteration's chunk (added at admission)
+                int w = sw(q), kv = skv(q) + n1, left = sleft(q);
+                uint32_t gs = g & ~G_INB;
+                uint32_t gm = tg.y;
                 const int idx = idx_of(pk);
                 if (idx >= N) bad_idx = true;
                 bool emit = false;
@@ -1046,15 +1114,17 @@ struct Sim {
                             }
                         }
                     } else {
-                        // gaps beyond 2^32 overflow TTLT too; tbtw starts at 0
-                        __hip_atomic_fetch_max(&tbtw[idx], t32 - tl, __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_WORKGROUP);
+                        // times are kept modulo 2^32: a gap of 2^32 us or more
+                        // overflows the request's TTLT too
+                        const uint32_t gap = t32 - tg.x;
+                        gm = gap > gm ? gap : gm;
                     }
                     if (left == 0) {
                         gs = (gs | G_DONE) & ~G_RES;
                         ufree += blocks(kv);
                         kv = 0;
                         tlast[idx] = t_end;
+                        tbo[idx] = gm;
                         fin = true;
                     } else if (pol == P_LAS) {
                         // the attained service grew by one token
@@ -1085,17 +1155,21 @@ struct Sim {
                     pk = pack((int64_t)w + left - 1 - kv, idx);
                     chg = true;
                 }
-                S.q[r] = make_uint4(gs, (uint32_t)w, (uint32_t)kv, (uint32_t)left);
+                mute = !emit;
+                opens = emit && !fin && blocks(kv + 1) != blocks(kv);
+                stq(r, gs, w, kv, left);
                 if (chg) S.k[r] = pk;
-                if (emit) S.tl[r] = t32;
+                if (emit) S.tg[r] = make_uint2(t32, gm);
             } else if (g & G_EVI) {
                 if (pol == P_SRPT || pol == P_TRAIL) {
-                    S.k[r] = pack((int64_t)(int)q.y + (int)q.w - 1, idx_of(pk));
+                    S.k[r] = pack((int64_t)sw(q) + sleft(q) - 1, idx_of(pk));
                     chg = true;
                 }
-                S.q[r].x = g & ~G_EVI;
+                stx(r, g & ~G_EVI);
             }
             const uint64_t cm = ballot(chg), fm = ballot(fin);
+            noemit |= ballot(mute);
+            dnext += popc(ballot(opens));
             if (cm && lo == INT32_MAX) lo = b + ffs0(cm);
             if (fm) {
                 if (lohole == INT32_MAX) lohole = b + ffs0(fm);
@@ -1114,10 +1188,12 @@ struct Sim {
                 }
             }
             if (bn < 0) break;
-            b = bn, q = qn, pk = pkn, tl = tln;
+            b = bn, q = qn, pk = pkn, tg = tgn;
         }
         wsync();
         if (ballot(bad_idx)) fail(S_ESTATE);
+        all_emit = noemit == 0;
+        du_next = dnext;
         if (nd) {
             U -= wsum(ufree);
             completed += nd;
@@ -1141,7 +1217,7 @@ struct Sim {
             const int r = b + lane();
             const bool v = r < L;
             R y;
-            if (v) ldr(S, r, y);
+            if (v) ldr(r, y);
             const bool dead = v && (y.gs & G_DONE);
             const bool dirty = v && (y.gs & G_DIRTY);
             const uint64_t val = (v && !dead && !dirty) ? y.pk : 0ull;
@@ -1154,7 +1230,7 @@ struct Sim {
             wsync();
             if (keep) {
                 const int d = out + mbcnt(km);
-                if (d != r) str(S, d, y);
+                if (d != r) str(d, y);
             }
             if (ext) {
                 y.gs &= ~G_DIRTY;
@@ -1186,7 +1262,7 @@ struct Sim {
         uint64_t pmax = start > 0 ? uniu(S.k[start - 1]) : 0ull;
         for (int b = start; b < L; b += kWave) {
             const int r = b + lane();
-            const bool v = r < L && !(S.q[r].x & G_DONE);
+            const bool v = r < L && !(ldx(r) & G_DONE);
             const uint64_t pk = r < L ? S.k[r] : 0ull;
             const uint64_t inc = scan_maxu(v ? pk : 0ull);
             uint64_t exc = prev_lane_u64(inc, 0ull);
@@ -1198,8 +1274,8 @@ struct Sim {
         for (int b = start; b < L; b += kWave) {
             const int r = b + lane();
             if (r < L) {
-                const uint32_t g = S.q[r].x;
-                if (g & G_DIRTY) S.q[r].x = g & ~G_DIRTY;
+                const uint32_t g = ldx(r);
+                if (g & G_DIRTY) stx(r, g & ~G_DIRTY);
             }
         }
         wsync();
@@ -1341,12 +1417,12 @@ struct Sim {
         for (int b = 0; b < L; b += kWave) {
             const int r = b + lane();
             if (r < L) {
-                const uint32_t g = S.q[r].x;
+                const uint32_t g = ldx(r);
                 if (!(g & G_DONE)) {
                     const int lv = min((int)((g >> G_LVL_SHIFT) & 31u), kLevels - 1);
                     const uint64_t pk = S.k[r];
                     S.k[r] = pack(key_of(pk) + S.bt[lv] - nt[lv], idx_of(pk));
-                    S.q[r].x = g | G_DIRTY;
+                    stx(r, g | G_DIRTY);
                 }
             }
         }
@@ -1371,7 +1447,6 @@ struct Sim {
     // ---------------------------------------------------------- driver
 
     DEV void run() {
-        for (int i = lane(); i < N; i += kWave) tbtw[i] = 0u;
         load_pf();
         take_arrivals();
         for (;;) {
@@ -1405,16 +1480,31 @@ struct Sim {
                     if (status) break;
                 }
             }
-            formation();
-            if (status) break;
-            if (cnt == 0) {
-                fail(S_ESTATE);
-                break;
+            const int64_t ev0 = ev_vol + ev_forced;
+            const bool rp = rep;
+            if (rp) {
+                // the previous batch again: every resident, one token each
+                // (its context grows by one token per member)
+                U += du_next;
+                cnt = nR;
+                used = nR;
+                sum_ctx += nR;
+            } else {
+                formation();
+                if (status) break;
+                if (cnt == 0) {
+                    fail(S_ESTATE);
+                    break;
+                }
             }
+            // formation evicted nothing, refilled nothing, stopped short of
+            // the token budget and took every resident
+            const bool rep_form = ev_vol + ev_forced == ev0 && !emit_all && used < T && cnt == nR;
             if (U > maxU) maxU = U;
             const int64_t dt = (int64_t)base + (int64_t)tok * used + (int64_t)ctx_quot((uint64_t)sum_ctx);
             const int64_t t_end = t + dt;
-            const int lo_mod = emission(t_end);
+            const int c0 = completed;
+            const int lo_mod = emission(t_end, rp ? (G_INB | G_RES) : G_INB, rp ? 1 : 0);
             t = t_end;
             iters++;
             reqiters += cnt;
@@ -1423,7 +1513,22 @@ struct Sim {
                 fail(S_ELIVELOCK);
                 break;
             }
+            // Every member emitted (so every resident needs one token), none
+            // completed or moved, the list needs no repair and the next
+            // step's KV growth fits: then the next formation takes the same
+            // residents and nothing else, as long as no request arrives. A
+            // waiting candidate it meets with admissions open met them in
+            // this formation too, did not fit and found no eligible victim;
+            // the KV held by the members before it has not shrunk, its own
+            // chunk has not shrunk, and the residents after it are the same
+            // with the same keys and eligibility, so it closes admissions
+            // again. (Adaptive gamma may re-key at the next step: excluded.)
+            bool nrep = rep_form && all_emit && completed == c0 && lo_mod == INT32_MAX &&
+                        L <= cap_now() && U + du_next <= Kb;
+            if constexpr (EXT) nrep = nrep && ad == nullptr;
+            const int next0 = next;
             maintenance(lo_mod);
+            rep = nrep && next == next0;
         }
         finish();
     }
@@ -1476,7 +1581,7 @@ struct Sim {
             const int64_t dt = (int64_t)base + (int64_t)tok * used + (int64_t)ctx_quot((uint64_t)sum_ctx);
             const int64_t t_end = t + dt;
             const int c0 = completed;
-            const int lo_mod = emission(t_end);
+            const int lo_mod = emission(t_end, G_INB, 0);
             last_done = completed - c0;
             t = t_end;
             iters++;
@@ -1523,8 +1628,6 @@ struct Sim {
                     if (f < 0 || f > 0xFFFFFFFFll || l < 0 || l > 0xFFFFFFFFll) bad = true;
                     A.ttft[ioff + i] = (uint32_t)f;
                     A.ttlt[ioff + i] = (uint32_t)l;
-                    A.tbtmax[ioff + i] =
-                        __hip_atomic_load(&tbtw[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
             if (ballot(bad)) fail(S_EOVERFLOW);
@@ -1554,8 +1657,6 @@ struct Sim {
                     if (f < 0 || f > 0xFFFFFFFFll || l < 0 || l > 0xFFFFFFFFll) bad = true;
                     A.ttft[ioff + i] = (uint32_t)f;
                     A.ttlt[ioff + i] = (uint32_t)l;
-                    A.tbtmax[ioff + i] =
-                        __hip_atomic_load(&tbtw[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
             if (ballot(bad)) fail(S_EOVERFLOW);
@@ -1573,9 +1674,9 @@ struct Sim {
     }
 };
 
-template <int BSH, bool EXT>
+template <int BSH, bool EXT, bool CP>
 DEV void run_instance(const SimArgs &a, const DevSetting &st, int inst, unsigned char *smem) {
-    Sim<BSH, EXT> s(a, st, inst, smem);
+    Sim<BSH, EXT, false, CP> s(a, st, inst, smem);
     s.run();
 }
 
@@ -1598,11 +1699,6 @@ DEV void run_cluster(const SimArgs &a, const DevSetting &st, int inst, unsigned 
     JsqLds *J = (JsqLds *)smem;
     const int R = a.replicas, w = (int)(threadIdx.x >> 6), N = a.n_req;
     Sim<BSH, true, true> s(a, st, inst, smem + kJsqLdsBytes + (size_t)w * (size_t)a.wave_lds, w);
-    const size_t ioff = (size_t)inst * (size_t)N;
-    for (int i = (int)threadIdx.x; i < N; i += (int)blockDim.x)  // gap maxima start at 0
-        __hip_atomic_store(&a.tbtw[ioff + i], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    hbm_fence();
-    __syncthreads();
     const int64_t *arr = a.arrival + (size_t)st.trace * (size_t)N;
     for (int j = 0;; j++) {  // j = N: run what was dispatched to the end
         const int64_t aj = j < N ? arr[j] : INT64_MAX;
@@ -1640,8 +1736,8 @@ DEV void run_cluster(const SimArgs &a, const DevSetting &st, int inst, unsigned 
 
 // EXT: the extended build (adaptive gamma, the phase-aware and cache-aware signals,
 // DistBoost, Sarathi), launched when some instance uses one of them (its extra state
-// and code cost the other policies registers).
-template <bool EXT>
+// and code cost the other policies registers). CP: compact list slots.
+template <bool EXT, bool CP>
 __global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     if ((int)blockIdx.x >= a.n_inst) return;
@@ -1649,8 +1745,8 @@ __global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
     if (a.retry && a.status[inst] != S_ECAPACITY) return;
     const DevSetting &st = a.inst[inst];
     const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-    if (a.bs == 16) run_instance<4, EXT>(a, st, inst, smem);
-    else run_instance<-1, EXT>(a, st, inst, smem);
+    if (a.bs == 16) run_instance<4, EXT, CP>(a, st, inst, smem);
+    else run_instance<-1, EXT, CP>(a, st, inst, smem);
     if (a.dur && !a.retry && lane() == 0)  // for the next launch's order
         a.dur[inst] = (int64_t)(__builtin_amdgcn_s_memrealtime() - t0);
 }
@@ -1700,18 +1796,15 @@ int tas_launch_cluster(const tas::SimArgs &a, int64_t lds_bytes, void *stream) {
 int tas_launch_sim(const tas::SimArgs &a, int64_t lds_bytes, void *stream) {
     if (a.n_inst <= 0) return 0;
     hipStream_t s = (hipStream_t)stream;
-    const void *fn = a.ext ? (const void *)tas::sim_kernel<true>
-                           : (const void *)tas::sim_kernel<false>;
+    void (*const fns[2][2])(tas::SimArgs) = {
+        {tas::sim_kernel<false, false>, tas::sim_kernel<false, true>},
+        {tas::sim_kernel<true, false>, tas::sim_kernel<true, true>}};
+    void (*fn)(tas::SimArgs) = fns[a.ext ? 1 : 0][a.cp ? 1 : 0];
     if (lds_bytes > 65536) {
-        if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+        if (hipFuncSetAttribute((const void *)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)lds_bytes) != hipSuccess)
             return -4;
     }
-    if (a.ext)
-        hipLaunchKernelGGL(tas::sim_kernel<true>, dim3((unsigned)a.n_inst), dim3(64),
-                           (size_t)lds_bytes, s, a);
-    else
-        hipLaunchKernelGGL(tas::sim_kernel<false>, dim3((unsigned)a.n_inst), dim3(64),
-                           (size_t)lds_bytes, s, a);
+    hipLaunchKernelGGL(fn, dim3((unsigned)a.n_inst), dim3(64), (size_t)lds_bytes, s, a);
     return hipGetLastError() == hipSuccess ? 0 : -4;
 }
