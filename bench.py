@@ -56,20 +56,50 @@ def measured_traffic(workload: str):
     return d.get("hbm_bytes_per_launch")
 
 
+def host_cpus():
+    """(logical CPUs of the host, CPUs this process may run on, CPU model)."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        allowed = len(os.sched_getaffinity(0))
+    except AttributeError:
+        allowed = os.cpu_count() or 1
+    return os.cpu_count() or 1, allowed, model
+
+
+def default_cpu_threads() -> int:
+    # every CPU this process may use, up to 16 (a one-GPU share of the host)
+    return max(1, min(16, host_cpus()[1]))
+
+
+def cpu_sample(w):
+    """The CPU baseline's sample: the first three traces under every setting."""
+    traces = np.unique(w.settings["trace"])[:3]
+    return traces, np.nonzero(np.isin(w.settings["trace"], traces))[0]
+
+
 def cpu_baseline(w, n_threads: int):
     import oracle
 
     oracle.build()
-    # the first three traces under every setting: 10-20 s of oracle work on 16 threads
-    traces = np.unique(w.settings["trace"])[:3]
-    sel = np.nonzero(np.isin(w.settings["trace"], traces))[0]
+    # 10-20 s of oracle work on 16 threads at the large sweep
+    traces, sel = cpu_sample(w)
     sub = w.subset(sel)
     tic = time.perf_counter()
     o = oracle.run(sub, n_threads=n_threads)
     dt = time.perf_counter() - tic
     reqit = int(o["counters"][:, 1].sum())
+    nproc, allowed, model = host_cpus()
     return o, sel, dict(value=reqit / dt, unit="request-iterations/s", cores=n_threads,
-                        kind="oracle", seconds=round(dt, 3),
+                        kind="oracle", seconds=round(dt, 3), host_cpus=nproc,
+                        cpus_allowed=allowed, cpu_model=model,
                         sample=f"traces {', '.join(str(int(t)) for t in traces)} under every setting "
                                f"({len(sel)} of {w.n_inst} instances, {reqit} request-iterations)")
 
@@ -98,7 +128,8 @@ def main():
                          "before the run), or join-shortest-queue (decided during the run, "
                          "one workgroup per cluster)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
-    ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="oracle threads (default: every CPU this process may use, up to 16)")
     ap.add_argument("--list-cap", type=int, default=0,
                     help="on-chip candidate list per instance (0: the library default)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -152,9 +183,16 @@ def main():
     sim = tas.Simulation(w, device=dev, list_cap=args.list_cap)
     stream = torch.cuda.current_stream()
 
+    first_ms = None  # the first launch: instances in the launch order estimated from the inputs
     for i in range(args.warmup):
-        sim.step(stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        sim.run(stream)
+        e1.record(stream)
+        sim.percentiles(stream)
         torch.cuda.synchronize()
+        if i == 0:
+            first_ms = float(e0.elapsed_time(e1))
         print(f"[bench] warmup {i} done", file=sys.stderr, flush=True)
 
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
@@ -206,6 +244,7 @@ def main():
                    "max_seqs": w.engine.max_seqs, "max_tokens": w.engine.max_tokens,
                    "kv_blocks": w.engine.kv_blocks, "request_iterations": reqiters,
                    "iterations": iters, "sim_kernel_ms": sim_ms, "pctl_kernel_ms": pct_ms,
+                   "first_launch_sim_kernel_ms": first_ms,
                    "wall_s": wall, "lds_list_cap": tas.tas_list_cap(sim.ctx),
                    "overflowed_instances": overflowed},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
@@ -265,19 +304,34 @@ def main():
                     "p99": float(np.mean([np.percentile(lat[i][m[i]], 99, method="inverted_cdf")
                                           for i in range(s, w.n_inst, S)]))}
                 for s in range(S)}
-    sim.close()
+    timed = None
     if not args.no_cpu and not args.cluster:
+        # the CPU sample's outputs of the last timed launch, kept for the parity check
+        _, sel = cpu_sample(w)
+        lat = [torch.empty((w.n_inst, w.n_req), dtype=torch.int32, device=dev) for _ in range(3)]
+        tas.tas_latencies(sim.ctx, *lat, stream=stream)
+        ix = torch.as_tensor(sel, device=dev)
+        timed = {k: t.index_select(0, ix).cpu().numpy().view(np.uint32)
+                 for k, t in zip(("ttft", "ttlt", "tbtmax"), lat)}
+        del lat
+        for k in ("counters", "pct", "status"):
+            timed[k] = out[k][sel]
+    sim.close()
+    if timed is not None:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        o, sel, cb = cpu_baseline(w, args.cpu_threads)
+        o, sel, cb = cpu_baseline(w, args.cpu_threads or default_cpu_threads())
         res["cpu_baseline"] = cb
-        # the same sample, checked against the GPU results of the timed run
-        sim2 = tas.Simulation(w.subset(sel), device=dev)
-        sim2.step(stream)
-        g = sim2.results()
-        sim2.close()
-        res["sample_parity"] = bool(all(np.array_equal(g[k], o[k]) for k in
-                                        ("ttft", "ttlt", "tbtmax", "counters", "pct")))
+        # the sample, checked element by element against the timed launch's outputs
+        bad = [k for k in ("ttft", "ttlt", "tbtmax", "counters", "pct", "status")
+               if not np.array_equal(timed[k], o[k])]
+        res["sample_parity"] = not bad
+        if bad:
+            res["sample_parity_mismatch"] = bad
     print(json.dumps(res))
+    if res.get("sample_parity") is False:
+        print(f"[bench] the timed launch differs from the oracle: {res['sample_parity_mismatch']}",
+              file=sys.stderr)
+        sys.exit(1)
 
 
 if __name__ == "__main__":

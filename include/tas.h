@@ -35,6 +35,15 @@
  *                  it, in the decode queue, key t_first - 2^42, so the decode
  *                  queue in order of entry fills the batch first and prefill
  *                  chunks fill the rest
+ *       TAS_LTR    SJF (LTR+; the evaluation's baselines, item 2, and Table 1's
+ *                  LTR row): the SJF key D_i plus starvation control by
+ *                  quantum promotion. After every iteration a candidate that
+ *                  did not run adds one to its starvation count and one that
+ *                  ran resets it; at ltr_starve the request is promoted: key
+ *                  j - 2^42 for a promotion at the end of iteration j (ahead
+ *                  of every unpromoted request, promoted ones in order of
+ *                  promotion), for ltr_quantum iterations in which it runs,
+ *                  after which it returns to key D_i with a count of zero
  *       TAS_SARATHI decode-prioritized continuous batching with round-robin
  *                  decodes and piggy-backed prefill chunks (the evaluation's
  *                  baselines, Sarathi): key a_i before the first token, then
@@ -107,7 +116,7 @@ enum {
 };
 
 enum { TAS_FCFS = 0, TAS_SRPT = 1, TAS_BOOST = 2, TAS_SPF = 3, TAS_SJF = 4, TAS_LAS = 5,
-       TAS_TRAIL = 6, TAS_DIST = 7, TAS_SARATHI = 8 };
+       TAS_TRAIL = 6, TAS_DIST = 7, TAS_SARATHI = 8, TAS_LTR = 9 };
 
 #define TAS_LEVELS 24
 
@@ -127,7 +136,7 @@ typedef struct {
 /* One instance: a trace and a policy setting. */
 typedef struct {
     int32_t trace;    /* index into the traces                                 */
-    int32_t policy;   /* one of the TAS_FCFS .. TAS_SARATHI policies above     */
+    int32_t policy;   /* one of the TAS_FCFS .. TAS_LTR policies above         */
     int32_t k;        /* MemGuard granularity in tokens (BOOST, DIST), >= 1    */
     int32_t memguard; /* 1: a dispatched request is non-evictable until its
                          level passes the level it was dispatched at (BOOST)  */
@@ -153,6 +162,11 @@ typedef struct {
                               Algorithm 2 (P in prefill, dec in decode); 2 =
                               P - h + dec with h from tas_traces.cached; 0
                               for every other policy                          */
+    /* SJF (LTR+), see TAS_LTR above; both 0 for every other policy */
+    int32_t ltr_starve;    /* iterations without service that promote, in
+                              [1, 32767]                                       */
+    int32_t ltr_quantum;   /* iterations of service a promotion grants, in
+                              [1, 32767]                                       */
 } tas_setting;
 
 #define TAS_ADA_WINDOW_MAX 2048
@@ -206,6 +220,11 @@ size_t tas_workspace_bytes(const tas_traces *traces, const tas_params *params);
 
 /* Validate the inputs, build every boost table, lay out the workspace and
  * copy the traces and settings into it (synchronous host-to-device copies).
+ * The inputs are the paper's problem statement (section "Formulation",
+ * Notation: requests (a_i, P_i, D_i) arriving online) plus the policy
+ * settings (Eq. boost_function for the tables; Phase 3 k and MemGuard; Phase
+ * 2 hysteresis delta) and the engine limits of Algorithm 1 (batch size, token
+ * budget, KV blocks).
  * d_ws: DEVICE buffer of ws_bytes >= tas_workspace_bytes(...), 256-byte
  * aligned, owned by the caller. *out receives a new context.
  * Returns TAS_EINVAL if: n_req < 1 or >= 2^20; an arrival is negative,
@@ -228,6 +247,10 @@ int tas_create(const tas_traces *traces, const tas_params *params, void *d_ws, s
 
 /* Enqueue the simulation of every instance on `stream` (one workgroup per
  * instance), followed by the retry pass for instances that outgrew list_cap.
+ * Each instance runs Algorithm 1's loop (arrivals, keys, the greedy batch with
+ * KVNeed / SelectVictim / SwapOut, ExecuteOneStep as the integer cost model,
+ * UpdateStats; with ada = 1 also UpdateGamma of Algorithm 2) until its last
+ * request completes.
  * Per-request latencies, counters and errors land in the workspace. From the
  * second call on (up to 16384 instances, without replicas) the workgroups
  * take the instances longest first, by the durations the previous call
@@ -251,13 +274,17 @@ int tas_percentiles(tas_ctx *ctx, uint32_t *d_out, void *stream);
 int tas_percentiles_grouped(tas_ctx *ctx, int32_t group, uint32_t *d_out, void *stream);
 
 /* Enqueue device-to-device copies of the per-request latencies, DEVICE
- * uint32 [n_inst][n_req] each, microseconds relative to arrival; any pointer
- * may be NULL to skip that array. */
+ * uint32 [n_inst][n_req] each, microseconds relative to arrival: TTFT, TTLT
+ * (T_i = C_i - a_i of section "Formulation") and the largest gap between two
+ * consecutive tokens (the TBT of Table 2, per request its maximum); any
+ * pointer may be NULL to skip that array. */
 int tas_latencies(tas_ctx *ctx, uint32_t *d_ttft, uint32_t *d_ttlt, uint32_t *d_tbtmax,
                   void *stream);
 
-/* Enqueue a copy of the per-instance counters, DEVICE int64 [n_inst][8]:
- * iterations, request-iterations (sum of batch sizes), computed tokens,
+/* Enqueue a copy of the per-instance counters, DEVICE int64 [n_inst][8]
+ * (Algorithm 1's loop as run: its iterations and batches, the SwapOut
+ * evictions, the KV blocks of KVNeed): iterations, request-iterations (sum of
+ * batch sizes), computed tokens,
  * voluntary evictions, forced evictions, final clock us, peak KV blocks,
  * idle us. For a cluster (jsq_replicas > 1): sums over its replicas, except
  * the final clock and the peak KV blocks, which are the largest. */

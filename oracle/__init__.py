@@ -50,11 +50,11 @@ def lib():
         L.tas_oracle_boost_table.argtypes = [f64, i32, f64, P]
         L.tas_oracle_boost_table.restype = ctypes.c_int
         L.tas_oracle_run.argtypes = [i32, i32, P, P, P, P, i32, P, P, P, P, P, P, P, i64,
-                                     P, P, P, P, P, P, P, P, P, P, i32]
+                                     P, P, P, P, P, P, P, P, P, P, P, i32]
         L.tas_oracle_run.restype = ctypes.c_int
-        L.tas_oracle_log.argtypes = [i32, P, P, P, P, i32, i32, i32, i64, P, P, i32, P, i64, P,
-                                     P, P, P, P, i64, P, i64, P, i64, P, P, P]
-        L.tas_oracle_jsq.argtypes = [i32, P, P, P, P, i32, i32, i32, i32, i64, P, P, i32, P,
+        L.tas_oracle_log.argtypes = [i32, P, P, P, P, i32, i32, i32, i64, P, P, i32, P, P, i64,
+                                     P, P, P, P, P, i64, P, i64, P, i64, P, P, P]
+        L.tas_oracle_jsq.argtypes = [i32, P, P, P, P, i32, i32, i32, i32, i64, P, P, i32, P, P,
                                      i64, P, P, P, P, P, P, P]
         L.tas_oracle_jsq.restype = ctypes.c_int
         L.tas_oracle_ada_grid.argtypes = [P, i32, P, P, P]
@@ -156,6 +156,8 @@ def run(w, n_threads: int | None = None, max_iters: int | None = None):
     ada = np.ascontiguousarray(np.stack([ada_params(x, w.engine.tau_us) for x in s])
                                if n_inst else np.zeros((0, 10)), np.float64)
     sg = np.ascontiguousarray(s["signal"], np.int32)
+    lt = np.ascontiguousarray(np.stack([s["ltr_starve"], s["ltr_quantum"]], axis=1)
+                              if n_inst else np.zeros((0, 2)), np.int32)
     out = dict(
         ttft=np.zeros((n_inst, n_req), np.uint32),
         ttlt=np.zeros((n_inst, n_req), np.uint32),
@@ -173,17 +175,18 @@ def run(w, n_threads: int | None = None, max_iters: int | None = None):
                               _p(po), _p(kk), _p(mg), _p(dl), _p(tb), _p(_eng(w.engine)),
                               int(mi), _p(out["ttft"]), _p(out["ttlt"]), _p(out["tbtmax"]),
                               _p(out["counters"]), _p(out["pct"]), _p(out["status"]), _p(ada),
-                              _p(sg), _p(out["gamma"]), _p(out["switches"]), int(nt))
+                              _p(sg), _p(lt), _p(out["gamma"]), _p(out["switches"]), int(nt))
     out["rc"] = rc
     return out
 
 
 def log(arrival, prompt, decode, engine, policy, k=1, memguard=0, delta_us=0, table=None,
         gamma=None, ada=None, signal=0, cached=None, max_iters=None, cap_iter=1 << 20,
-        cap_batch=1 << 22, cap_evict=1 << 20):
+        cap_batch=1 << 22, cap_evict=1 << 20, ltr=None):
     """Run one instance and return its schedule log (see tas_oracle.h). ``ada``:
     adaptive-gamma parameters as in workloads.ADA (gamma is the start);
-    ``cached``: expected prefix-cache hit tokens per request (signal 2)."""
+    ``cached``: expected prefix-cache hit tokens per request (signal 2);
+    ``ltr``: (starvation threshold, quantum) of an LTR instance."""
     arrival = np.ascontiguousarray(arrival, np.int64)
     prompt = np.ascontiguousarray(prompt, np.int32)
     decode = np.ascontiguousarray(decode, np.int32)
@@ -205,10 +208,11 @@ def log(arrival, prompt, decode, engine, policy, k=1, memguard=0, delta_us=0, ta
     ev = np.zeros((cap_evict, 4), np.int64)
     ni, nb, ne = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     mi = engine.max_iters if max_iters is None else max_iters
+    lt = None if ltr is None else np.ascontiguousarray(ltr, np.int32)
     rc = lib().tas_oracle_log(n, _p(arrival), _p(prompt), _p(decode),
                               None if ch is None else _p(ch), policy, k, memguard,
                               int(delta_us), _p(table), _p(prm), int(signal),
-                              _p(_eng(engine)), int(mi),
+                              None if lt is None else _p(lt), _p(_eng(engine)), int(mi),
                               _p(o["ttft"]), _p(o["ttlt"]), _p(o["tbtmax"]), _p(o["counters"]),
                               _p(it), cap_iter, _p(bt), cap_batch, _p(ev), cap_evict,
                               ctypes.byref(ni), ctypes.byref(nb), ctypes.byref(ne))
@@ -270,13 +274,14 @@ def jsq(w, replicas: int, n_threads: int | None = None, max_iters: int | None = 
         de = np.ascontiguousarray(w.decode[t], np.int32)
         ch = None if w.cached is None else np.ascontiguousarray(w.cached[t], np.int32)
         prm = np.ascontiguousarray(ada_params(s[i], w.engine.tau_us), np.float64)
+        lt = np.array([s[i]["ltr_starve"], s[i]["ltr_quantum"]], np.int32)
         bufs = [np.zeros(n_req, np.uint32) for _ in range(3)] + [np.zeros(n_req, np.int32),
                                                                   np.zeros((R, 8), np.int64),
                                                                   np.zeros(R), np.zeros(R, np.int64)]
         rc = lib().tas_oracle_jsq(n_req, _p(arr), _p(pr), _p(de), None if ch is None else _p(ch),
                                   R, int(s[i]["policy"]), int(s[i]["k"]), int(s[i]["memguard"]),
                                   int(s[i]["delta_us"]), _p(tb[i]), _p(prm), int(s[i]["signal"]),
-                                  _p(eng), int(mi), *[_p(b) for b in bufs])
+                                  _p(lt), _p(eng), int(mi), *[_p(b) for b in bufs])
         out["status"][i] = rc
         if rc == 0:
             for key, b in zip(("ttft", "ttlt", "tbtmax", "assign", "counters", "gamma",

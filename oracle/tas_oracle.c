@@ -44,8 +44,17 @@
  * Comparison policies (paper: Table 1 and the baselines of the evaluation):
  *   SPF   shortest prompt first: key = P (static)
  *   SJF   shortest job first with perfect knowledge of the output length (the
- *         ranking LTR learns): key = D (static); the starvation quantum of
- *         LTR+ is not modelled
+ *         ranking LTR learns): key = D (static)
+ *   LTR   SJF (LTR+): the SJF key plus LTR's starvation control by quantum
+ *         promotion (baselines of the evaluation, item 2; Table 1, the LTR
+ *         row). After every iteration each request that was a candidate and
+ *         did not run adds one to its starvation count; one that ran resets
+ *         it. At the threshold S (a setting) the request is promoted: it
+ *         ranks before every unpromoted request, promoted requests in order
+ *         of promotion (key = j - 2^42 for a promotion at the end of
+ *         iteration j, ties by index), for a quantum of Q iterations in which
+ *         it runs (Q a setting); then it returns to its SJF key with a count
+ *         of zero. No MemGuard, no hysteresis.
  *   LAS   least attained service: key = P + dec, the same signal as the boost
  *         (grows with every emitted token)
  *   TRAIL SRPT with perfect knowledge plus the swap-prevention threshold: a
@@ -102,8 +111,10 @@
 
 enum { PENDING = 0, WAITING = 1, RESIDENT = 2, DONE = 3 };
 enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2, P_SPF = 3, P_SJF = 4, P_LAS = 5, P_TRAIL = 6,
-       P_DIST = 7, P_SARATHI = 8 };
+       P_DIST = 7, P_SARATHI = 8, P_LTR = 9 };
+#define P_LAST P_LTR
 #define DECODE_QUEUE_OFFSET ((int64_t)1 << 42) /* decode-queue keys lie below every prefill key */
+#define PROMOTED_OFFSET ((int64_t)1 << 42)     /* LTR+: promoted keys lie below every SJF key */
 
 #define ADA_GRID_MAX 64
 #define ADA_WINDOW_MAX 2048
@@ -129,6 +140,7 @@ typedef struct {
     int32_t signal;   /* BOOST: 0 = P + dec, 1 = Algorithm 2's phase-aware signal,
                          2 = P - h + dec (expected prefix-cache hits h) */
     const int32_t *H; /* expected cached prompt tokens per request, or NULL */
+    int32_t ltr_s, ltr_q; /* LTR+: starvation threshold and quantum, iterations */
 } inst_t;
 
 typedef struct {
@@ -140,6 +152,9 @@ typedef struct {
     int64_t key;   /* priority key, frozen at iteration start */
     int64_t t_first, t_last, tbt_max;
     int64_t evicted_at; /* iteration in which it was last evicted, or -1 */
+    int32_t starve;     /* LTR+: iterations not served (unpromoted), or quantum left */
+    int8_t promoted;    /* LTR+ */
+    int64_t promo_key;  /* LTR+: the key while promoted */
 } req_t;
 
 typedef struct {
@@ -218,6 +233,8 @@ static int64_t key_of(const inst_t *I, int32_t r, const req_t *q) {
     case P_SARATHI:
         if (q->dec > 0) return q->t_last - DECODE_QUEUE_OFFSET; /* round robin */
         return I->a[r];                                         /* arrival order */
+    case P_LTR:
+        return q->promoted ? q->promo_key : I->D[r];
     default:
         return I->a[r] - I->bt[level_of(signal_of(I, r, q), I->k)];
     }
@@ -296,6 +313,7 @@ static int simulate(const inst_t *I0, uint32_t *ttft, uint32_t *ttlt, uint32_t *
     const ada_t *A = I->ada && I->ada->on ? I->ada : NULL;
     const int32_t N = I->N;
     if (I->signal == 2 && !I->H) return TOR_EINVAL;
+    if (I->policy == P_LTR && (I->ltr_s < 1 || I->ltr_q < 1)) return TOR_EINVAL;
     for (int32_t i = 0; i < N; i++) {
         if (I->P[i] < 1 || I->D[i] < 1 || I->a[i] < 0 || (i && I->a[i] < I->a[i - 1]))
             return TOR_EINVAL;
@@ -484,6 +502,27 @@ static int simulate(const inst_t *I0, uint32_t *ttft, uint32_t *ttlt, uint32_t *
             }
         }
 
+        /* LTR+ starvation control: every candidate of this iteration that did
+         * not run counts one more iteration of starvation and is promoted at
+         * the threshold; one that ran resets its count, or spends one
+         * iteration of its quantum. Effective from the next iteration's keys. */
+        if (I->policy == P_LTR) {
+            for (int32_t j = 0; j < nact; j++) {
+                req_t *q = &R[act[j]];
+                if (q->in_batch) {
+                    if (!q->promoted) {
+                        q->starve = 0;
+                    } else if (--q->starve == 0) {
+                        q->promoted = 0; /* the quantum is spent */
+                    }
+                } else if (!q->promoted && ++q->starve >= I->ltr_s) {
+                    q->promoted = 1;
+                    q->starve = I->ltr_q;
+                    q->promo_key = (iters + 1) - PROMOTED_OFFSET;
+                }
+            }
+        }
+
         /* O9 execute: advance KV, emit tokens, record latencies, complete. */
         for (int32_t b = 0; b < nb; b++) {
             int32_t r = bidx[b];
@@ -585,6 +624,7 @@ typedef struct {
     int32_t *status;
     const double *ada; /* [n_inst*10] or NULL */
     const int32_t *signal; /* [n_inst] or NULL */
+    const int32_t *ltr;    /* [n_inst*2] or NULL */
     double *gamma_out;
     int64_t *switch_out;
     int32_t next; /* work counter */
@@ -601,6 +641,7 @@ static void fill_inst(inst_t *I, const int32_t *eng, int32_t n_req, const int64_
     I->ada = NULL;
     I->signal = 0;
     I->H = NULL;
+    I->ltr_s = I->ltr_q = 0;
 }
 
 static void run_one(job_t *J, int32_t i) {
@@ -615,6 +656,7 @@ static void run_one(job_t *J, int32_t i) {
     int st = 0;
     if (J->signal) I.signal = J->signal[i];
     if (J->cached) I.H = J->cached + off;
+    if (J->ltr) I.ltr_s = J->ltr[2 * (size_t)i], I.ltr_q = J->ltr[2 * (size_t)i + 1];
     if (J->ada && J->ada[(size_t)i * 10] != 0.0) {
         A = (ada_t *)malloc(sizeof *A);
         st = A ? ada_setup(A, J->ada + (size_t)i * 10, J->policy[i], J->k[i]) : TOR_EINVAL;
@@ -652,11 +694,14 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
                    const int32_t *memguard, const int64_t *delta, const int64_t *table,
                    const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
                    uint32_t *tbtmax, int64_t *counters, uint32_t *pct, int32_t *status,
-                   const double *ada, const int32_t *signal, double *gamma_out,
-                   int64_t *switch_out, int32_t n_threads) {
+                   const double *ada, const int32_t *signal, const int32_t *ltr,
+                   double *gamma_out, int64_t *switch_out, int32_t n_threads) {
     if (n_traces < 1 || n_req < 1 || n_inst < 0) return TOR_EINVAL;
     for (int32_t i = 0; i < n_inst; i++) {
-        if (trace[i] < 0 || trace[i] >= n_traces || policy[i] < 0 || policy[i] > 8 || k[i] < 1)
+        if (trace[i] < 0 || trace[i] >= n_traces || policy[i] < 0 || policy[i] > P_LAST ||
+            k[i] < 1)
+            return TOR_EINVAL;
+        if (policy[i] == P_LTR && (!ltr || ltr[2 * i] < 1 || ltr[2 * i + 1] < 1))
             return TOR_EINVAL;
         if (signal && signal[i] != 0 &&
             (signal[i] < 1 || signal[i] > 2 || policy[i] != P_BOOST || (signal[i] == 2 && !cached)))
@@ -670,7 +715,8 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
                .memguard = memguard, .delta = delta, .table = table, .eng = eng,
                .max_iters = max_iters, .ttft = ttft, .ttlt = ttlt, .tbtmax = tbtmax,
                .pct = pct, .counters = counters, .status = status, .ada = ada,
-               .signal = signal, .gamma_out = gamma_out, .switch_out = switch_out, .next = 0};
+               .signal = signal, .ltr = ltr, .gamma_out = gamma_out, .switch_out = switch_out,
+               .next = 0};
     if (n_threads < 1) n_threads = 1;
     if (n_threads > n_inst) n_threads = n_inst > 0 ? n_inst : 1;
     pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)n_threads);
@@ -690,11 +736,11 @@ int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
                    const int32_t *decode, const int32_t *cached, int32_t policy, int32_t k,
                    int32_t memguard,
                    int64_t delta, const int64_t *table, const double *ada, int32_t signal,
-                   const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
-                   uint32_t *tbtmax, int64_t *counters, int64_t *log_iter, int64_t iter_cap,
-                   int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
+                   const int32_t *ltr, const int32_t *eng, int64_t max_iters, uint32_t *ttft,
+                   uint32_t *ttlt, uint32_t *tbtmax, int64_t *counters, int64_t *log_iter,
+                   int64_t iter_cap, int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
                    int64_t evict_cap, int64_t *n_iter, int64_t *n_batch, int64_t *n_evict) {
-    if (policy < 0 || policy > 8 ||
+    if (policy < 0 || policy > P_LAST ||
         (signal != 0 && (signal < 1 || signal > 2 || policy != P_BOOST || (signal == 2 && !cached))))
         return TOR_EINVAL;
     inst_t I;
@@ -702,6 +748,7 @@ int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
               max_iters);
     I.signal = signal;
     I.H = cached;
+    if (ltr) I.ltr_s = ltr[0], I.ltr_q = ltr[1];
     ada_t *A = NULL;
     if (ada && ada[0] != 0.0) {
         A = (ada_t *)malloc(sizeof *A);
@@ -737,10 +784,11 @@ int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
 int tas_oracle_jsq(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
                    const int32_t *decode, const int32_t *cached, int32_t replicas,
                    int32_t policy, int32_t k, int32_t memguard, int64_t delta,
-                   const int64_t *table, const double *ada, int32_t signal, const int32_t *eng,
-                   int64_t max_iters, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
-                   int32_t *assign, int64_t *counters, double *gamma_out, int64_t *switch_out) {
-    if (n_req < 1 || replicas < 1 || policy < 0 || policy > 8 || k < 1 ||
+                   const int64_t *table, const double *ada, int32_t signal, const int32_t *ltr,
+                   const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
+                   uint32_t *tbtmax, int32_t *assign, int64_t *counters, double *gamma_out,
+                   int64_t *switch_out) {
+    if (n_req < 1 || replicas < 1 || policy < 0 || policy > P_LAST || k < 1 ||
         (signal != 0 && (signal < 1 || signal > 2 || policy != P_BOOST || (signal == 2 && !cached))))
         return TOR_EINVAL;
     for (int32_t j = 1; j < n_req; j++)
@@ -810,6 +858,7 @@ int tas_oracle_jsq(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
             I.signal = signal;
             I.H = cached ? P + 2 * n : NULL;
             I.ada = A;
+            if (ltr) I.ltr_s = ltr[0], I.ltr_q = ltr[1];
             int64_t c8[8];
             double g = 0.0;
             int64_t sw = 0;

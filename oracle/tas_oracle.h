@@ -18,7 +18,7 @@
  *   cached [n_traces*n_req] int32 expected prefix-cache hit tokens, 0 <= h < P,
  *   or NULL (needed only by signal 2)
  *   per instance i: trace[i], policy[i] (0 FCFS, 1 SRPT, 2 BOOST, 3 SPF,
- *   4 SJF, 5 LAS, 6 TRAIL, 7 DIST, 8 SARATHI), k[i] >= 1,
+ *   4 SJF, 5 LAS, 6 TRAIL, 7 DIST, 8 SARATHI, 9 LTR), k[i] >= 1,
  *   memguard[i] in {0,1}, delta[i] >= 0 us, table[i*24 .. i*24+23] int64 us
  *   eng[8] = {max_seqs, max_tokens, chunk, kv_blocks, block_tokens,
  *             iter_base_us, iter_tok_us, iter_ctx_div}
@@ -38,6 +38,12 @@
  * to the current gamma (see tas_oracle.c). Outputs gamma_out [n_inst] (final
  * gamma, 0 when not adaptive) and switch_out [n_inst] (grid-cell changes) may
  * be NULL.
+ *
+ * ltr [n_inst*2] (NULL: no LTR instance): for an LTR instance (SJF (LTR+),
+ * the evaluation's baselines) ltr[2i] = the starvation threshold S >= 1 and
+ * ltr[2i+1] = the promotion quantum Q >= 1, both in iterations (see
+ * tas_oracle.c); ignored for the other policies. tas_oracle_log and
+ * tas_oracle_jsq take the pair of their one setting (or NULL).
  *
  * signal [n_inst] (NULL: all 0): the boost signal of a BOOST instance, 0 =
  * prompt plus emitted tokens, 1 = Algorithm 2's phase-aware signal (prompt
@@ -73,8 +79,8 @@ int tas_oracle_run(int32_t n_traces, int32_t n_req, const int64_t *arrival,
                    const int32_t *memguard, const int64_t *delta, const int64_t *table,
                    const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
                    uint32_t *tbtmax, int64_t *counters, uint32_t *pct, int32_t *status,
-                   const double *ada, const int32_t *signal, double *gamma_out,
-                   int64_t *switch_out, int32_t n_threads);
+                   const double *ada, const int32_t *signal, const int32_t *ltr,
+                   double *gamma_out, int64_t *switch_out, int32_t n_threads);
 
 /* Run ONE instance and record its schedule, for invariant checks.
  * log_iter[it*8 + {0..7}] = {t_start, dt, batch size, KV blocks in use
@@ -90,9 +96,9 @@ int tas_oracle_log(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
                    const int32_t *decode, const int32_t *cached, int32_t policy, int32_t k,
                    int32_t memguard,
                    int64_t delta, const int64_t *table, const double *ada, int32_t signal,
-                   const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
-                   uint32_t *tbtmax, int64_t *counters, int64_t *log_iter, int64_t iter_cap,
-                   int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
+                   const int32_t *ltr, const int32_t *eng, int64_t max_iters, uint32_t *ttft,
+                   uint32_t *ttlt, uint32_t *tbtmax, int64_t *counters, int64_t *log_iter,
+                   int64_t iter_cap, int32_t *log_batch, int64_t batch_cap, int64_t *log_evict,
                    int64_t evict_cap, int64_t *n_iter, int64_t *n_batch, int64_t *n_evict);
 
 /* The adaptive-gamma grid of prm[10] (layout as above, on = 1): grid[G],
@@ -119,9 +125,10 @@ uint32_t tas_oracle_percentile(const uint32_t *v, int32_t n, int32_t q);
 int tas_oracle_jsq(int32_t n_req, const int64_t *arrival, const int32_t *prompt,
                    const int32_t *decode, const int32_t *cached, int32_t replicas,
                    int32_t policy, int32_t k, int32_t memguard, int64_t delta,
-                   const int64_t *table, const double *ada, int32_t signal, const int32_t *eng,
-                   int64_t max_iters, uint32_t *ttft, uint32_t *ttlt, uint32_t *tbtmax,
-                   int32_t *assign, int64_t *counters, double *gamma_out, int64_t *switch_out);
+                   const int64_t *table, const double *ada, int32_t signal, const int32_t *ltr,
+                   const int32_t *eng, int64_t max_iters, uint32_t *ttft, uint32_t *ttlt,
+                   uint32_t *tbtmax, int32_t *assign, int64_t *counters, double *gamma_out,
+                   int64_t *switch_out);
 
 #ifdef __cplusplus
 }

@@ -31,6 +31,7 @@ constexpr int64_t kMaxLds = 160 * 1024;  // gfx950 LDS per workgroup
 constexpr int64_t kTwo41 = int64_t(1) << 41;
 constexpr int64_t kTwo42 = int64_t(1) << 42;
 constexpr int64_t kTwo40 = int64_t(1) << 40;  // DistBoost tables: decode keys stay below
+constexpr int32_t kLtrMax = (1 << 15) - 1;    // LTR+ counts live in 15 bits of the flag word
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -56,6 +57,8 @@ int64_t launch_lds(int32_t list_cap, int32_t wmax, int32_t replicas, bool compac
 // P + D <= 65535 and D <= 32768, and the instance is a single server.
 bool compact_ok(const tas_traces *t, const tas_params *p) {
     if (replicas_of(p) > 1) return false;
+    for (int32_t i = 0; i < p->n_inst; i++)  // LTR+ keeps its counts in those bits
+        if (p->inst[i].policy == TAS_LTR) return false;
     const size_t tn = (size_t)t->n_traces * (size_t)t->n_req;
     for (size_t i = 0; i < tn; i++) {
         const int64_t P = t->prompt[i], D = t->decode[i];
@@ -202,8 +205,15 @@ int check_setting(const tas_setting &s, int32_t n_traces, double tau_us, bool ha
     if (s.ada != 0 && (s.ada != 1 || !ada_ok(s))) return TAS_EINVAL;
     if (s.signal != 0 && (s.signal < 1 || s.signal > 2 || s.policy != TAS_BOOST)) return TAS_EINVAL;
     if (s.signal == 2 && !has_cached) return TAS_EINVAL;
-    if (s.policy < TAS_FCFS || s.policy > TAS_SARATHI) return TAS_EINVAL;
+    if (s.policy < TAS_FCFS || s.policy > TAS_LTR) return TAS_EINVAL;
     if (s.delta_us < 0) return TAS_EINVAL;
+    if (s.policy == TAS_LTR) {
+        if (s.ltr_starve < 1 || s.ltr_starve > kLtrMax || s.ltr_quantum < 1 ||
+            s.ltr_quantum > kLtrMax)
+            return TAS_EINVAL;
+    } else if (s.ltr_starve != 0 || s.ltr_quantum != 0) {
+        return TAS_EINVAL;
+    }
     const bool boosted = s.policy == TAS_BOOST || s.policy == TAS_DIST;
     if (s.policy != TAS_BOOST) {
         if (s.memguard != 0 || s.delta_us != 0) return TAS_EINVAL;
@@ -329,7 +339,9 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
         d.delta = s.policy == TAS_BOOST ? s.delta_us : 0;
         d.ada = -1;
         d.signal = s.signal;
-        if (s.signal || s.policy == TAS_DIST || s.policy == TAS_SARATHI) ext = true;
+        d.ltr_s = s.ltr_starve, d.ltr_q = s.ltr_quantum;
+        if (s.signal || s.policy == TAS_DIST || s.policy == TAS_SARATHI || s.policy == TAS_LTR)
+            ext = true;
         if (boosted) {
             if (s.table_given) std::memcpy(d.bt, s.boost_us, sizeof d.bt);
             else tas_boost_table(s.gamma, s.k, p->tau_us, d.bt);

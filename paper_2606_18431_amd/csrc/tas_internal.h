@@ -26,6 +26,8 @@ struct DevSetting {
     int32_t ada;          // index into SimArgs::ada, or -1
     int32_t signal;       // BOOST: 1 = Algorithm 2's phase-aware signal,
                           // 2 = P - h + dec (expected prefix-cache hits h)
+    int32_t ltr_s, ltr_q; // LTR+: starvation threshold and quantum (iterations)
+    int32_t pad_;
 };
 
 // Adaptive gamma of one instance (host-built): the update constants, the

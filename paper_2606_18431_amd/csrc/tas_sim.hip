@@ -55,6 +55,11 @@ constexpr int G_LVL_SHIFT = 12;          // current MemGuard level (5 bits)
 constexpr uint32_t G_LVL = 0x1fu << G_LVL_SHIFT;
 constexpr uint32_t G_FLAGS = 0x1ffffu;   // the flags and levels: bits 0..16
 constexpr int kLeftShift = 17;           // compact slots: left - 1 in bits 17..31
+// LTR+ (which has no MemGuard level, and never uses compact slots): the
+// level's lowest bit marks a promoted request, bits 17..31 hold its
+// starvation count, or while promoted the quantum left
+constexpr uint32_t G_PROMO = 1u << G_LVL_SHIFT;
+constexpr int kLtrShift = 17;
 constexpr int kHoleLimit = 16;           // compact once this many holes accumulate
 
 enum { S_OK = 0, S_EOVERFLOW = -5, S_ELIVELOCK = -6, S_ESTATE = -7, S_ECAPACITY = -8 };
@@ -65,7 +70,10 @@ enum { S_OK = 0, S_EOVERFLOW = -5, S_ELIVELOCK = -6, S_ESTATE = -7, S_ECAPACITY 
 // SRPT with TRAIL's swap-prevention threshold (TRAIL); and the Phase 1
 // strawman DistBoost (DIST).
 enum { P_FCFS = 0, P_SRPT = 1, P_BOOST = 2, P_SPF = 3, P_SJF = 4, P_LAS = 5, P_TRAIL = 6,
-       P_DIST = 7, P_SARATHI = 8 };
+       P_DIST = 7, P_SARATHI = 8, P_LTR = 9 };
+// LTR+ ranks a promoted request ahead of every unpromoted one (SJF keys are
+// D >= 1): key j - 2^42 for a promotion at the end of iteration j.
+constexpr int64_t kPromotedOff = int64_t(1) << 42;
 // DistBoost ranks its decode queue (key: the time a request entered it, its
 // first-token time) ahead of its prefill queue: decode keys are shifted down
 // by 2^42, below every prefill key a - bt (boost tables are capped at 2^40).
@@ -280,6 +288,7 @@ struct Sim {
     Lds S;
     // instance constants (memguard and delta are zero unless pol is BOOST)
     int inst, N, M, T, c, Kb, bs, base, tok, div, pol, k, lk, memguard, lcap, scap;
+    int ltr_s, ltr_q;  // LTR+: starvation threshold and quantum (iterations)
     int64_t delta, max_iters;
     uint64_t div_magic;  // ceil(2^64 / div) for div >= 2
     const int64_t *arr;
@@ -335,6 +344,7 @@ struct Sim {
         k = st.k > 0 ? st.k : 1;
         lk = 31 - __clz(k);
         pol = st.policy;
+        ltr_s = st.ltr_s, ltr_q = st.ltr_q;
         memguard = st.memguard;
         delta = st.delta;
         max_iters = a.max_iters;
@@ -458,6 +468,7 @@ struct Sim {
     // and a list padded with waiting entries costs every pass over it.
     DEV int cap_now() const {
         if constexpr (EXT) {
+            if (pol == P_LTR) return lcap;  // LTR+ keeps every request on chip
             return min(lcap, max(M, nR) + 128);
         } else {
             return lcap;
@@ -511,8 +522,8 @@ struct Sim {
             key = (int64_t)P + D - 1;  // remaining computed tokens
         } else if (pol == P_SPF || pol == P_LAS) {
             key = P;  // prompt length; the attained service P + dec at dec = 0
-        } else if (pol == P_SJF) {
-            key = D;  // output length
+        } else if (pol == P_SJF || (EXT && pol == P_LTR)) {
+            key = D;  // output length (LTR+: until a promotion)
         } else {
             int sig = P;  // the signal before the first token
             if constexpr (EXT) {
@@ -638,6 +649,13 @@ struct Sim {
         drop_holes();
         const int E = L - cap;
         if (E <= 0) return;
+        if (EXT && pol == P_LTR) {
+            // a spilled request's starvation count would have to advance in
+            // HBM every iteration: an LTR+ instance keeps every request on
+            // chip, and one that outgrows the list reruns with a larger one
+            fail(S_ECAPACITY);
+            return;
+        }
         if (spill_n + E > scap) {
             fail(S_ECAPACITY);
             return;
@@ -964,7 +982,13 @@ struct Sim {
         const int lim = lcap + kStage;
         uint4 nx = make_uint4(0u, 0u, 0u, 0u);
         bool have_nx = false;
-        for (int guard = 0; guard < (1 << 22); guard++) {
+        // every pass advances p or refills from the spill, so the walk ends
+        // within L + spill_cap passes; a walk that does not is a broken state
+        for (int pass = 0;; pass++) {
+            if (UNLIKELY(pass > lcap + kStage + scap + 2)) {
+                fail(S_ESTATE);
+                return;
+            }
             if (cnt >= M || used >= T || (closed && r_ahead <= 0)) break;
             if (UNLIKELY(!closed && p >= bstar)) {  // bstar <= L: spilled entries come next
                 mid_refill(p);
@@ -1070,7 +1094,9 @@ struct Sim {
         int dnext = 0;        // members whose next token opens a KV block
         const uint32_t t32 = (uint32_t)t_end;
         const int nch = (L + kWave - 1) >> 6;
-        uint64_t todo = emit_all ? (nch >= 64 ? ~0ull : ((1ull << nch) - 1ull)) : emit_chunks;
+        // LTR+ updates every candidate's starvation count: visit every chunk
+        const bool all = emit_all || (EXT && pol == P_LTR);
+        uint64_t todo = all ? (nch >= 64 ? ~0ull : ((1ull << nch) - 1ull)) : emit_chunks;
         if (!todo) return INT32_MAX;
         // chunks are visited in ascending order, the next one's records loaded
         // while this one is processed (a chunk's edits stay inside it)
@@ -1155,6 +1181,19 @@ struct Sim {
                     pk = pack((int64_t)w + left - 1 - kv, idx);
                     chg = true;
                 }
+                if constexpr (EXT) {
+                    if (pol == P_LTR && !fin) {  // it ran: the count resets, or
+                        if (!(gs & G_PROMO)) {   // a promotion spends its quantum
+                            gs &= G_FLAGS;
+                        } else if ((gs >> kLtrShift) <= 1u) {
+                            gs = (gs & G_FLAGS & ~G_PROMO) | G_DIRTY;  // back to key D
+                            pk = pack((int64_t)(w - Pp[idx]) + left, idx);
+                            chg = true;
+                        } else {
+                            gs -= 1u << kLtrShift;
+                        }
+                    }
+                }
                 mute = !emit;
                 opens = emit && !fin && blocks(kv + 1) != blocks(kv);
                 stq(r, gs, w, kv, left);
@@ -1166,6 +1205,22 @@ struct Sim {
                     chg = true;
                 }
                 stx(r, g & ~G_EVI);
+            }
+            if constexpr (EXT) {
+                // LTR+: a candidate that did not run starves one more
+                // iteration; at the threshold it is promoted for a quantum
+                if (pol == P_LTR && !(g & mem) && r < L && !(g & (G_DONE | G_PROMO))) {
+                    const uint32_t cnt = (g >> kLtrShift) + 1u;
+                    uint32_t gx = (g & G_FLAGS & ~G_EVI) | (cnt << kLtrShift);
+                    if ((int)cnt >= ltr_s) {
+                        gx = (g & G_FLAGS & ~G_EVI) | G_PROMO | G_DIRTY |
+                             ((uint32_t)ltr_q << kLtrShift);
+                        pk = pack(iters + 1 - kPromotedOff, idx_of(pk));
+                        S.k[r] = pk;
+                        chg = true;
+                    }
+                    stx(r, gx);
+                }
             }
             const uint64_t cm = ballot(chg), fm = ballot(fin);
             noemit |= ballot(mute);

@@ -23,6 +23,7 @@ LEVELS = 24
 
 TAS_OK, TAS_EINVAL, TAS_EINFEASIBLE, TAS_ENOMEM, TAS_EHIP = 0, -1, -2, -3, -4
 TAS_EOVERFLOW, TAS_ELIVELOCK, TAS_ESTATE, TAS_ECAPACITY = -5, -6, -7, -8
+TAS_LTR = 9
 
 
 class TasError(RuntimeError):
@@ -45,7 +46,8 @@ class tas_setting(ctypes.Structure):
                 ("ada_beta", ctypes.c_double), ("ada_gamma_min", ctypes.c_double),
                 ("ada_gamma_max", ctypes.c_double), ("ada_eps_us", ctypes.c_double),
                 ("ada_window", ctypes.c_int32), ("ada_min_samples", ctypes.c_int32),
-                ("ada_grid", ctypes.c_int32), ("signal", ctypes.c_int32)]
+                ("ada_grid", ctypes.c_int32), ("signal", ctypes.c_int32),
+                ("ltr_starve", ctypes.c_int32), ("ltr_quantum", ctypes.c_int32)]
 
 
 class tas_params(ctypes.Structure):
@@ -59,7 +61,7 @@ class tas_params(ctypes.Structure):
                 ("inst", ctypes.c_void_p), ("jsq_replicas", ctypes.c_int32)]
 
 
-assert ctypes.sizeof(tas_setting) == W.SETTING_DTYPE.itemsize == 280
+assert ctypes.sizeof(tas_setting) == W.SETTING_DTYPE.itemsize == 288
 
 EXPORTS = ["tas_workspace_bytes", "tas_create", "tas_run", "tas_percentiles",
            "tas_percentiles_grouped", "tas_latencies",
@@ -265,6 +267,16 @@ def tas_list_cap(ctx) -> int:
     return int(lib().tas_list_cap(ctx))
 
 
+def _host(t, stream):
+    """Copy a device tensor to a host numpy array once the work enqueued on
+    `stream` has finished (the whole device is synchronised, so any stream,
+    torch's or a raw handle, is covered)."""
+    import torch
+
+    torch.cuda.synchronize(t.device)
+    return t.cpu().numpy()
+
+
 class Simulation:
     """One workload on one GPU: workspace, outputs and the C-ABI calls."""
 
@@ -291,11 +303,16 @@ class Simulation:
         self.switch_buf = torch.zeros(n, dtype=torch.int64, device=device)
         self.status_buf = torch.zeros(n, dtype=torch.int32, device=device)
         self.m = m
+        # the stream of the latest run: copies and status calls follow it
+        # (every call on one context is ordered on one stream)
+        self.stream = None
 
     def run(self, stream=None):
+        self.stream = stream
         tas_run(self.ctx, stream)
 
     def percentiles(self, stream=None):
+        self.stream = stream
         tas_percentiles(self.ctx, self.pct, stream)
 
     def step(self, stream=None):
@@ -304,45 +321,48 @@ class Simulation:
         self.percentiles(stream)
 
     def results(self, latencies: bool = True):
-        """Synchronise and copy everything to host numpy arrays."""
+        """Synchronise and copy everything to host numpy arrays (on the
+        stream of the latest run)."""
         torch = self.torch
         n = self.w.n_inst
+        st = self.stream
         out = {}
         if latencies:
             lat = [torch.empty((n, self.m), dtype=torch.int32, device=self.pct.device)
                    for _ in range(3)]
-            tas_latencies(self.ctx, *lat)
+            tas_latencies(self.ctx, *lat, stream=st)
             for key, t in zip(("ttft", "ttlt", "tbtmax"), lat):
-                out[key] = t.cpu().numpy().view(np.uint32)
-        tas_counters(self.ctx, self.counters)
-        tas_gamma(self.ctx, self.gamma_buf, self.switch_buf)
-        tas_instance_status(self.ctx, self.status_buf)
+                out[key] = _host(t, st).view(np.uint32)
+        tas_counters(self.ctx, self.counters, st)
+        tas_gamma(self.ctx, self.gamma_buf, self.switch_buf, st)
+        tas_instance_status(self.ctx, self.status_buf, st)
         out["rc"] = tas_status(self.ctx)
-        out["counters"] = self.counters.cpu().numpy()
-        out["gamma"] = self.gamma_buf.cpu().numpy()
-        out["switches"] = self.switch_buf.cpu().numpy()
-        out["status"] = self.status_buf.cpu().numpy()
-        out["pct"] = self.pct.cpu().numpy().view(np.uint32)
+        out["counters"] = _host(self.counters, st)
+        out["gamma"] = _host(self.gamma_buf, st)
+        out["switches"] = _host(self.switch_buf, st)
+        out["status"] = _host(self.status_buf, st)
+        out["pct"] = _host(self.pct, st).view(np.uint32)
         if self.replicas > 1:  # the router's assignment and the replicas' counters
             asg = torch.empty((n, self.m), dtype=torch.int32, device=self.pct.device)
             rc = torch.empty((n, self.replicas, 8), dtype=torch.int64, device=self.pct.device)
             rg = torch.empty((n, self.replicas), dtype=torch.float64, device=self.pct.device)
             rs = torch.empty((n, self.replicas), dtype=torch.int64, device=self.pct.device)
-            tas_replicas(self.ctx, asg, rc, rg, rs)
-            out["assign"] = asg.cpu().numpy()
-            out["rcounters"] = rc.cpu().numpy()
-            out["rgamma"] = rg.cpu().numpy()
-            out["rswitches"] = rs.cpu().numpy()
+            tas_replicas(self.ctx, asg, rc, rg, rs, stream=st)
+            out["assign"] = _host(asg, st)
+            out["rcounters"] = _host(rc, st)
+            out["rgamma"] = _host(rg, st)
+            out["rswitches"] = _host(rs, st)
         return out
 
     def group_percentiles(self, group: int, stream=None) -> np.ndarray:
         """Percentiles pooled over groups of `group` adjacent instances
         [n_inst/group, 3, 3] (synchronises)."""
         torch = self.torch
-        out = torch.zeros((self.w.n_inst // group, 3, 3), dtype=torch.int32,
+        st = self.stream if stream is None else stream
+        out = torch.empty((self.w.n_inst // group, 3, 3), dtype=torch.int32,
                           device=self.pct.device)
-        tas_percentiles_grouped(self.ctx, group, out, stream)
-        return out.cpu().numpy().view(np.uint32)
+        tas_percentiles_grouped(self.ctx, group, out, st)
+        return _host(out, st).view(np.uint32)
 
     def table(self, inst: int) -> np.ndarray:
         return tas_instance_table(self.ctx, inst)

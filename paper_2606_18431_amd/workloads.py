@@ -36,9 +36,9 @@ import math
 
 import numpy as np
 
-FCFS, SRPT, BOOST, SPF, SJF, LAS, TRAIL, DIST, SARATHI = 0, 1, 2, 3, 4, 5, 6, 7, 8
+FCFS, SRPT, BOOST, SPF, SJF, LAS, TRAIL, DIST, SARATHI, LTR = 0, 1, 2, 3, 4, 5, 6, 7, 8, 9
 POLICY_NAMES = {FCFS: "fcfs", SRPT: "srpt", BOOST: "boost", SPF: "spf", SJF: "sjf", LAS: "las",
-                TRAIL: "trail", DIST: "distboost", SARATHI: "sarathi"}
+                TRAIL: "trail", DIST: "distboost", SARATHI: "sarathi", LTR: "ltr"}
 LEVELS = 24
 
 # One numpy record per instance; field order mirrors the C struct tas_setting.
@@ -61,6 +61,8 @@ SETTING_DTYPE = np.dtype(
         ("ada_min_samples", np.int32),
         ("ada_grid", np.int32),
         ("signal", np.int32),
+        ("ltr_starve", np.int32),
+        ("ltr_quantum", np.int32),
     ]
 )
 
@@ -119,14 +121,18 @@ class Workload:
 
 
 def setting(trace, policy, k=1, memguard=0, delta_us=0, gamma=0.0, table=None, ada=None,
-            signal=0):
+            signal=0, ltr=None):
     """One instance record. ``ada``: adaptive-gamma parameters (keys of ADA
     without the ``ada_`` prefix, e.g. ``dict(ADA)``), gamma being the start.
     ``signal`` 1: Algorithm 2's phase-aware boost signal (BOOST); 2: the
-    cache-aware signal P - h + dec (BOOST; needs the workload's ``cached``)."""
+    cache-aware signal P - h + dec (BOOST; needs the workload's ``cached``).
+    ``ltr``: (starvation threshold, quantum) in iterations of an LTR setting
+    (default LTR_CONTROL)."""
     s = np.zeros((), dtype=SETTING_DTYPE)
     s["trace"], s["policy"], s["k"], s["memguard"] = trace, policy, k, memguard
     s["delta_us"], s["gamma"], s["signal"] = delta_us, gamma, signal
+    if policy == LTR:
+        s["ltr_starve"], s["ltr_quantum"] = LTR_CONTROL if ltr is None else ltr
     if ada is not None:
         s["ada"] = 1
         for key, v in ada.items():
@@ -140,6 +146,10 @@ def setting(trace, policy, k=1, memguard=0, delta_us=0, gamma=0.0, table=None, a
 
 
 UNIBOOST = dict(k=256, memguard=1, delta_us=100_000)  # defaults k=256, delta=0.1 s
+# SJF (LTR+): a request not served for 512 iterations in a row (about 2.5-5 s
+# at the workloads' 5-10 ms steps) is promoted for 64 iterations of service;
+# the paper states the mechanism, not its parameters
+LTR_CONTROL = (512, 64)
 VANILLA = dict(k=1, memguard=0, delta_us=0)
 # Adaptive gamma: EMA weight per iteration, clip bounds = grid ends (10 grid
 # points per decade), floor of the tail band in us, window of completed
@@ -169,11 +179,12 @@ def settings_grid(n_traces: int, n_settings: int) -> np.ndarray:
 
 
 def comparator_settings(n_traces: int, gamma: float = 1e-3) -> np.ndarray:
-    """Per trace, 9 settings: FCFS, SRPT, SPF, SJF, LAS, TRAIL, then UniBoost and
-    vanilla boost at one gamma, then Sarathi. Instance id = trace * 9 + s."""
+    """Per trace, 10 settings: FCFS, SRPT, SPF, SJF, LAS, TRAIL, then UniBoost and
+    vanilla boost at one gamma, then Sarathi and SJF (LTR+). Instance id =
+    trace * 10 + s."""
     per = [dict(policy=FCFS), dict(policy=SRPT), dict(policy=SPF), dict(policy=SJF),
            dict(policy=LAS), dict(policy=TRAIL), dict(policy=BOOST, gamma=gamma, **UNIBOOST),
-           dict(policy=BOOST, gamma=gamma, **VANILLA), dict(policy=SARATHI)]
+           dict(policy=BOOST, gamma=gamma, **VANILLA), dict(policy=SARATHI), dict(policy=LTR)]
     out = np.zeros(n_traces * len(per), dtype=SETTING_DTYPE)
     for t in range(n_traces):
         for s, kw in enumerate(per):
@@ -457,7 +468,7 @@ def make(cfg: int, n_traces: int | None = None, n_settings: int | None = None,
         arr[t], pr[t], de[t] = _trace(cfg, t, N, eng)
     if grid == "comparators":
         sets = comparator_settings(T)
-        S = 9
+        S = len(sets) // T
     elif grid == "ada":
         sets = ada_settings(T)
         S = 8

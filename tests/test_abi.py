@@ -290,3 +290,21 @@ def test_bench_refuses_more_than_one_gpu():
     r = subprocess.run([os.environ.get("PYTHON", "python3"), os.path.join(ROOT, "bench.py"),
                         "--gpus", "2"], capture_output=True, text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_ltr_control_validation():
+    """SJF (LTR+) needs a starvation threshold and a quantum in [1, 32767]; the
+    other policies must leave both at zero."""
+    w = small()
+    for bad in ((0, 4), (4, 0), (32768, 4), (4, 32768), (-1, 4)):
+        s = w.settings.copy()
+        s[0] = W.setting(int(s[0]["trace"]), W.LTR, ltr=bad)
+        assert create_rc(w, settings=s)[0] == tas.TAS_EINVAL, bad
+    s = w.settings.copy()
+    s[0]["ltr_starve"] = 8  # FCFS with an LTR field
+    assert create_rc(w, settings=s)[0] == tas.TAS_EINVAL
+    s = w.settings.copy()
+    s[0] = W.setting(int(s[0]["trace"]), W.LTR, ltr=(32767, 32767))
+    assert create_rc(w, settings=s)[0] != tas.TAS_EINVAL  # valid (the copy needs a GPU)
+    s[0]["policy"] = 10  # beyond the last policy
+    assert create_rc(w, settings=s)[0] == tas.TAS_EINVAL

@@ -69,7 +69,7 @@ def test_hand_worked_on_gpu(torch, case):
     tb = case.get("table")
     s = W.setting(0, case["policy"], k=case.get("k", 1), memguard=case.get("memguard", 0),
                   delta_us=case.get("delta_us", 0), table=tb if tb is not None else None,
-                  signal=case.get("signal", 0))
+                  signal=case.get("signal", 0), ltr=case.get("ltr"))
     w = W.Workload(case["name"], np.array([case["arrival"]], np.int64),
                    np.array([case["prompt"]], np.int32), np.array([case["decode"]], np.int32),
                    e, np.stack([s]),
@@ -384,3 +384,33 @@ def test_launch_order_permutation_at_size(torch, n):
         for key in ("ttft", "ttlt", "tbtmax"):
             assert np.array_equal(g[key][i], o[key][j]), (i, key)
         assert np.array_equal(g["counters"][i], o["counters"][j]), i
+
+
+@pytest.mark.parametrize("cfg,n_traces,n_req,ltr", [
+    (1, 2, 3000, (8, 4)),
+    (2, 2, 3000, (8, 4)),      # KV pressure: promoted requests evict residents
+    (2, 1, 3000, (40, 16)),
+    (3, 1, 5000, (24, 2)),
+    (4, 1, 12000, (64, 32)),   # 256 sequences: queues form after the first 6000 requests
+])
+def test_parity_ltr(torch, cfg, n_traces, n_req, ltr):
+    """SJF (LTR+) with thresholds low enough that promotions, quantum expiries
+    and demotions happen all along; with max_seqs 64 the first-pass list holds
+    192 entries, so instances whose queue outgrows it rerun with the large
+    list (LTR+ keeps every request on chip)."""
+    import dataclasses
+
+    w = W.make(cfg, n_traces=n_traces, n_settings=4, n_req=n_req)
+    s = np.stack([W.setting(t, W.LTR, ltr=ltr) for t in range(n_traces)] +
+                 [W.setting(t, W.SJF) for t in range(n_traces)])
+    w = dataclasses.replace(w, settings=s)
+    o = oracle.run(w)
+    g = gpu_run(w)
+    assert (o["status"] == g["status"]).all(), (o["status"], g["status"])
+    ok = o["status"] == 0
+    assert ok.any()
+    for key in ("ttft", "ttlt", "tbtmax", "counters", "pct"):
+        assert np.array_equal(g[key][ok], o[key][ok]), key
+    # the control changed the schedule somewhere
+    n = n_traces
+    assert any(not np.array_equal(o["ttlt"][i], o["ttlt"][n + i]) for i in range(n) if ok[i])

@@ -205,3 +205,23 @@ def test_ada_rejects_bad_parameters():
     assert lg["rc"] == oracle.EINVAL
     lg = oracle.log(a, p, d, e, W.FCFS, gamma=1e-3, ada=good)  # adaptive gamma is BOOST only
     assert lg["rc"] == oracle.EINVAL
+
+
+def test_golden_values_follow_closed_forms():
+    """The stored adaptive-gamma cases agree with their closed-form derivation
+    (tests/golden/ada_hand_calc.py: isolated-request latencies, the tail-band
+    estimator, the EMA and the clip), independently of the oracle."""
+    import json
+    import sys
+
+    sys.path.insert(0, os.path.join(os.path.dirname(__file__), "golden"))
+    import ada_hand_calc as C
+
+    cases = {c["name"]: c for c in json.load(open(os.path.join(
+        os.path.dirname(__file__), "golden", "ada_hand.json")))["cases"]}
+    exp = C.expected()
+    assert set(exp) <= set(cases)
+    for name, e in exp.items():
+        assert cases[name]["gamma_final"] == pytest.approx(e["gamma_final"], rel=1e-12), name
+    assert cases["ada_estimator"]["ttlt"][:20] == exp["ada_estimator"]["ttlt_alone"]
+    assert cases["ada_eps_floor"]["ttlt"] == [C.alone(100, 5)] * 21

@@ -180,3 +180,71 @@ def test_sarathi_is_distboost_without_contention(seed):
     f2 = oracle.log(a, p, d, e2, FCFS)
     assert not np.array_equal(s2["ttlt"], t2["ttlt"])
     assert not np.array_equal(s2["ttlt"], f2["ttlt"])
+
+
+# ------------------------------------------------------------ SJF (LTR+)
+
+
+def test_ltr_without_reachable_threshold_is_sjf():
+    """SJF (LTR+) whose starvation threshold no wait reaches is plain SJF, bit
+    for bit (the promotion is the only difference)."""
+    import dataclasses
+
+    w = W.make(2, n_traces=1, n_settings=4, n_req=800)
+    sjf = w.settings.copy()
+    sjf["policy"], sjf["k"], sjf["memguard"], sjf["delta_us"] = W.SJF, 1, 0, 0
+    ltr = sjf.copy()
+    ltr["policy"], ltr["ltr_starve"], ltr["ltr_quantum"] = W.LTR, 1 << 30, 7
+    a = oracle.run(dataclasses.replace(w, settings=sjf))
+    b = oracle.run(dataclasses.replace(w, settings=ltr))
+    assert a["rc"] == 0 and b["rc"] == 0
+    for key in ("ttft", "ttlt", "tbtmax", "counters", "pct"):
+        assert np.array_equal(a[key], b[key]), key
+
+
+@pytest.mark.parametrize("S,Q", [(3, 1), (6, 4), (20, 10)])
+def test_ltr_bounds_unserved_streaks(S, Q):
+    """Under LTR+ an unpromoted request is promoted after S iterations without
+    service, and a promoted one ranks ahead of every unpromoted request: at
+    most M - 1 promoted requests (the batch) ahead of it can keep it waiting
+    each iteration. So, with a batch of one, a request never waits more than
+    S + (promoted requests ahead) * Q iterations in a row; the replay of the
+    schedule finds the streaks, and SJF exceeds the bound on the same trace."""
+    a, p, d = W.small_random(5, 200, rate_per_s=80.0, p_max=300, d_max=120)
+    e = W.Engine(max_seqs=1, max_tokens=1024, chunk=512, kv_blocks=4096)
+
+    def longest_wait(o):
+        N = len(a)
+        t0s = o["iters"][:, 0]
+        rows = np.cumsum(np.r_[0, o["iters"][:, 2]])
+        served = [set(o["batch"][rows[i]:rows[i + 1], 0].tolist()) for i in range(len(t0s))]
+        done_at = {}
+        for i in range(len(t0s)):
+            for r in served[i]:
+                done_at[r] = i
+        worst = 0
+        for r in range(N):
+            run = 0
+            for i in range(len(t0s)):
+                if t0s[i] < a[r] or i > done_at[r]:
+                    continue
+                run = 0 if r in served[i] else run + 1
+                worst = max(worst, run)
+        return worst
+
+    o = oracle.log(a, p, d, e, W.LTR, ltr=(S, Q))
+    s = oracle.log(a, p, d, e, W.SJF)
+    assert o["rc"] == 0 and s["rc"] == 0
+    bound = S + len(a) * Q  # loose: promoted requests ahead, each served Q times
+    assert longest_wait(o) <= bound
+    assert longest_wait(o) < longest_wait(s)
+    assert not np.array_equal(o["ttlt"], s["ttlt"])
+
+
+def test_ltr_rejects_bad_control():
+    e = W.Engine()
+    for bad in ((0, 4), (4, 0), (-1, 1)):
+        o = oracle.log([0, 0], [16, 16], [2, 2], e, W.LTR, ltr=bad)
+        assert o["rc"] == oracle.EINVAL, bad
+    o = oracle.log([0, 0], [16, 16], [2, 2], e, W.LTR)  # no control given
+    assert o["rc"] == oracle.EINVAL

@@ -32,8 +32,9 @@ def sig_of(r, p, dec, signal, h=None):
 
 
 def key_of(policy, r, a, p, d, kv, dec, k, table, signal=0, t_first=None, h=None,
-           t_last=None):
-    """Iteration-start priority key of request r (lower is served first)."""
+           t_last=None, promo=None):
+    """Iteration-start priority key of request r (lower is served first).
+    ``promo``: SJF (LTR+), the promotion iteration of each request or -1."""
     if policy == 0:
         return int(a[r])  # FCFS: arrival
     if policy in (1, 6):
@@ -51,12 +52,20 @@ def key_of(policy, r, a, p, d, kv, dec, k, table, signal=0, t_first=None, h=None
         return (1, int(a[r]) - int(table[lvl]))
     if policy == 8:  # Sarathi: decodes by their latest token time, then prefills by arrival
         return (0, int(t_last[r])) if dec[r] > 0 else (1, int(a[r]))
+    if policy == 9:  # LTR+: promoted requests first, by promotion iteration; then SJF
+        return (0, int(promo[r])) if promo[r] >= 0 else (1, int(d[r]))
     lvl = min(23, (max(sig_of(r, p, dec, signal, h), k) // k).bit_length() - 1)
     return int(a[r]) - int(table[lvl])  # boost: a - b(quantized signal)
 
 
-def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_us=0, h=None):
+def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_us=0, h=None,
+           ltr=None):
     N = len(a)
+    # LTR+ state, rebuilt from the batches: the iteration of the current
+    # promotion (-1: none), the iterations not served in a row, the quantum left
+    promo = np.full(N, -1, np.int64)
+    starve = np.zeros(N, np.int64)
+    quantum = np.zeros(N, np.int64)
     bs = e.block_tokens
     kv = np.zeros(N, np.int64)
     dec = np.zeros(N, np.int64)
@@ -86,7 +95,7 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_u
         row += nb
         # iteration-start keys of every active request
         active = [r for r in range(N) if a[r] <= t0 and not done[r]]
-        key0 = {r: key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first, h, t_last)
+        key0 = {r: key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first, h, t_last, promo)
                 for r in active}
 
         def eligible(x):  # may be a voluntary victim (MemGuard, TRAIL threshold)
@@ -138,7 +147,7 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_u
         # formation takes candidates in ascending (key, idx) order of the
         # iteration-start keys (batch members were not evicted, so their kv is
         # still the iteration-start value)
-        keys = [(key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first, h, t_last), r)
+        keys = [(key_of(policy, r, a, p, d, kv, dec, k, table, signal, t_first, h, t_last, promo), r)
                 for r in members]
         assert keys == sorted(keys)
         assert not (set(members) & evicted)
@@ -168,13 +177,31 @@ def replay(a, p, d, e, o, policy, k=1, memguard=0, table=None, signal=0, delta_u
                         return False
                     return not (policy == 6 and 5 * dec[v] >= 3 * d[v])
                 for w in waiting:
-                    kw = key_of(policy, w, a, p, d, kv, dec, k, table, signal, t_first, h, t_last)
+                    kw = key_of(policy, w, a, p, d, kv, dec, k, table, signal, t_first, h, t_last, promo)
                     for v in outside:
                         kvv = key_of(policy, v, a, p, d, kv, dec, k, table, signal, t_first, h,
-                                     t_last)
+                                     t_last, promo)
                         worse = ((kvv, v) > (kw, w)) if isinstance(kvv, tuple) else \
                             ((kvv - delta_us, v) > (kw, w))
                         assert not (worse and eligible(v)), (i, w, v)
+        # LTR+: candidates left out starve one more iteration (promoted at the
+        # threshold), members reset or spend one iteration of their quantum
+        if policy == 9:
+            S_, Q_ = ltr
+            for r in active:
+                if r in members:
+                    if promo[r] < 0:
+                        starve[r] = 0
+                    else:
+                        quantum[r] -= 1
+                        if quantum[r] == 0:
+                            promo[r] = -1
+                            starve[r] = 0
+                elif promo[r] < 0:
+                    starve[r] += 1
+                    if starve[r] >= S_:
+                        promo[r] = i + 1
+                        quantum[r] = Q_
         # cost model and I1
         ctx = sum(int(kv[r] + n) for r, n in zip(members, ns))
         assert dt == e.iter_base_us + e.iter_tok_us * int(ns.sum()) + ctx // e.iter_ctx_div
@@ -245,6 +272,8 @@ POLICIES = [
     dict(policy=2, k=16, memguard=1, delta_us=20000, gamma=1e-3, signal=2),  # cache-aware signal
     dict(policy=2, k=1, memguard=0, delta_us=0, gamma=3e-2, signal=2),
     dict(policy=8),  # Sarathi
+    dict(policy=9, ltr=(4, 3)),  # SJF (LTR+), promotions within a few iterations
+    dict(policy=9, ltr=(12, 1)),
 ]
 
 
@@ -259,12 +288,13 @@ def test_replay_invariants(seed, ei, pi):
         else None
     o = oracle.log(a, p, d, e, pol["policy"], k=pol.get("k", 1), memguard=pol.get("memguard", 0),
                    delta_us=pol.get("delta_us", 0), gamma=pol.get("gamma"),
-                   signal=pol.get("signal", 0), cached=h)
+                   signal=pol.get("signal", 0), cached=h, ltr=pol.get("ltr"))
     assert o["rc"] == 0
     table = (oracle.boost_table(pol["gamma"], pol.get("k", 1), e.tau_us)
              if pol["policy"] in (2, 7) else None)
     replay(a, p, d, e, o, pol["policy"], k=pol.get("k", 1), memguard=pol.get("memguard", 0),
-           table=table, signal=pol.get("signal", 0), delta_us=pol.get("delta_us", 0), h=h)
+           table=table, signal=pol.get("signal", 0), delta_us=pol.get("delta_us", 0), h=h,
+           ltr=pol.get("ltr"))
 
 
 def test_replay_sees_evictions():

@@ -45,7 +45,7 @@ def test_hand_worked_schedules(case):
     o = oracle.log(case["arrival"], case["prompt"], case["decode"], e, case["policy"],
                    k=case.get("k", 1), memguard=case.get("memguard", 0),
                    delta_us=case.get("delta_us", 0), table=tb, signal=case.get("signal", 0),
-                   cached=case.get("cached"))
+                   cached=case.get("cached"), ltr=case.get("ltr"))
     assert o["rc"] == 0
     assert o["ttft"].tolist() == case["ttft"]
     assert o["ttlt"].tolist() == case["ttlt"]
