@@ -245,6 +245,20 @@ size_t tas_workspace_bytes(const tas_traces *traces, const tas_params *params);
 int tas_create(const tas_traces *traces, const tas_params *params, void *d_ws, size_t ws_bytes,
                tas_ctx **out);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): tas_create with
+ * the workspace in a static device array of TAS_STATIC_WORKSPACE_BYTES that
+ * the library holds on each GPU it runs on until the process ends. No device
+ * memory is allocated. Returns TAS_ENOMEM when tas_workspace_bytes exceeds
+ * TAS_STATIC_WORKSPACE_BYTES, TAS_EHIP when the array's address cannot be
+ * obtained, otherwise as tas_create. All contexts created this way on one
+ * GPU share its array: creating one overwrites the workspace of the previous
+ * one, which must no longer be used, and calls on two such contexts that
+ * overlap on one GPU race. The array keeps the last call's contents; what
+ * must start at zero is cleared by this call, as by tas_create. */
+#define TAS_STATIC_WORKSPACE_BYTES ((size_t)64 << 20)
+int tas_create_static(const tas_traces *traces, const tas_params *params, tas_ctx **out);
+
 /* Enqueue the simulation of every instance on `stream` (one workgroup per
  * instance), followed by the retry pass for instances that outgrew list_cap.
  * Each instance runs Algorithm 1's loop (arrivals, keys, the greedy batch with

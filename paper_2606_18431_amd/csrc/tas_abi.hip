@@ -8,6 +8,7 @@
 
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -245,6 +246,35 @@ int launch(const tas::SimArgs &a, int64_t lds_bytes, void *stream) {
 
 }  // namespace
 
+// Device workspace for callers that cannot allocate (tas_create_static): a
+// file-scope array of TAS_STATIC_WORKSPACE_BYTES on every GPU the library
+// runs on, held until the process ends. Host code never passes the array's
+// name to a kernel or a copy: it uses the address hipGetSymbolAddress gives
+// on each device.
+static __device__ __align__(256) unsigned char scratch[TAS_STATIC_WORKSPACE_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void *scratch_addr[kMaxDevices];  // per device, looked up on its first use
+
+// The device address of `scratch` on the current device.
+int scratch_ptr(void **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TAS_EHIP;
+    std::lock_guard<std::mutex> g(scratch_mu);
+    if (!scratch_addr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return TAS_EHIP;
+        scratch_addr[dev] = p;
+    }
+    *out = scratch_addr[dev];
+    return TAS_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int tas_boost_table(double gamma, int32_t k, double tau_us, int64_t *out) {
@@ -282,6 +312,19 @@ size_t tas_workspace_bytes(const tas_traces *t, const tas_params *p) {
     Layout L;
     layout(t, p, rc, sc, &L);
     return L.total;
+}
+
+int tas_create_static(const tas_traces *t, const tas_params *p, tas_ctx **out) {
+    if (!out) return TAS_EINVAL;
+    *out = nullptr;
+    const size_t need = tas_workspace_bytes(t, p);
+    if (need > TAS_STATIC_WORKSPACE_BYTES) return TAS_ENOMEM;
+    void *ws = nullptr;
+    if (need > 0) {  // (invalid inputs: tas_create names the error)
+        const int rc = scratch_ptr(&ws);
+        if (rc) return rc;
+    }
+    return tas_create(t, p, ws, TAS_STATIC_WORKSPACE_BYTES, out);
 }
 
 int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_bytes,

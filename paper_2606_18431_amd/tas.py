@@ -67,7 +67,8 @@ EXPORTS = ["tas_workspace_bytes", "tas_create", "tas_run", "tas_percentiles",
            "tas_percentiles_grouped", "tas_latencies",
            "tas_counters", "tas_gamma", "tas_status", "tas_instance_status", "tas_destroy",
            "tas_strerror", "tas_boost_table", "tas_ada_grid", "tas_instance_table",
-           "tas_list_cap", "tas_replicas", "tas_schedule"]
+           "tas_list_cap", "tas_replicas", "tas_schedule", "tas_create_static"]
+STATIC_WORKSPACE_BYTES = 64 << 20
 
 _lib = None
 
@@ -84,6 +85,8 @@ def lib():
         L.tas_workspace_bytes.argtypes = [P, P]
         L.tas_workspace_bytes.restype = ctypes.c_size_t
         L.tas_create.argtypes = [P, P, P, ctypes.c_size_t, ctypes.POINTER(P)]
+        L.tas_create_static.argtypes = [P, P, ctypes.POINTER(P)]
+        L.tas_create_static.restype = ctypes.c_int
         for name in ("tas_create", "tas_run", "tas_percentiles", "tas_percentiles_grouped",
                      "tas_latencies", "tas_counters",
                      "tas_gamma", "tas_status", "tas_instance_status", "tas_boost_table",
@@ -186,6 +189,15 @@ def tas_create(traces: tas_traces, params: tas_params, ws, ws_bytes: int | None 
     rc = lib().tas_create(ctypes.byref(traces), ctypes.byref(params), addr, nbytes,
                           ctypes.byref(ctx))
     _check(rc, "tas_create")
+    return ctx.value
+
+
+def tas_create_static(traces: tas_traces, params: tas_params):
+    """tas_create with the library's static device workspace (no device
+    memory is allocated). Returns a context handle (int)."""
+    ctx = ctypes.c_void_p()
+    rc = lib().tas_create_static(ctypes.byref(traces), ctypes.byref(params), ctypes.byref(ctx))
+    _check(rc, "tas_create_static")
     return ctx.value
 
 
