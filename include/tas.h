@@ -265,11 +265,14 @@ int tas_create_static(const tas_traces *traces, const tas_params *params, tas_ct
  * KVNeed / SelectVictim / SwapOut, ExecuteOneStep as the integer cost model,
  * UpdateStats; with ada = 1 also UpdateGamma of Algorithm 2) until its last
  * request completes.
- * Per-request latencies, counters and errors land in the workspace. From the
- * second call on (up to 16384 instances, without replicas) the workgroups
- * take the instances longest first, by the durations the previous call
- * recorded: a launch lasts until its last instance ends. The results do not
- * depend on the order. Calls on one context share its workspace: a call on
+ * Per-request latencies, counters and errors land in the workspace. The
+ * workgroups (up to 16384 instances, without replicas) take the instances
+ * longest first: a launch lasts until its last instance ends. The first call
+ * ranks them by an estimate of their work from the inputs (the sum over the
+ * trace of D + ceil(P / chunk), times 5/4 for SRPT, TRAIL, LAS and Sarathi),
+ * later calls by the durations the previous call recorded. Consecutive
+ * workgroups go to different XCDs, so the sorted order also spreads each
+ * kind of instance over them. The results do not depend on the order. Calls on one context share its workspace: a call on
  * another stream must be ordered after the previous one by the caller. */
 int tas_run(tas_ctx *ctx, void *stream);
 
@@ -326,9 +329,10 @@ int tas_replicas(tas_ctx *ctx, int32_t *d_assign, int64_t *d_counters, double *d
 int tas_status(tas_ctx *ctx);
 
 /* The schedule of the latest tas_run: d_dur DEVICE int64 [n_inst], each
- * instance's wall-clock time on the GPU in 100 MHz ticks (0 before the first
- * run), and d_order DEVICE int32 [n_inst], the instance each workgroup took
- * (a permutation; the index order on the first run). Either pointer may be
+ * instance's wall-clock time on the GPU in 100 MHz ticks (before the first
+ * run: the work estimates that order it), and d_order DEVICE int32 [n_inst],
+ * the instance each workgroup took (a permutation; the index order before
+ * the first run). Either pointer may be
  * NULL. TAS_EINVAL where no order is kept (replicas, or more than 16384
  * instances). */
 int tas_schedule(tas_ctx *ctx, int64_t *d_dur, int32_t *d_order, void *stream);

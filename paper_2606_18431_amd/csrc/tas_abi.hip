@@ -18,7 +18,7 @@
 struct tas_ctx {
     int32_t n_traces = 0, n_req = 0, n_inst = 0, list_cap = 0, spill_cap = 0, retry_cap = 0;
     int32_t replicas = 1;  // > 1: replicas behind a join-shortest-queue router
-    bool ordered = false;  // a run has recorded durations: order the next one
+    bool ordered = false;  // order the next launch by `dur` (estimates, then durations)
     int64_t lds_bytes = 0, lds_retry = 0;
     tas::SimArgs args{};
     std::vector<tas::DevSetting> settings;
@@ -418,12 +418,33 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     if (ok && n_ada > 0)
         ok = hipMemcpy(ws + L.ada, c->ada.data(), c->ada.size() * sizeof(tas::DevAda),
                        hipMemcpyHostToDevice) == hipSuccess;
-    if (ok && p->n_inst > 0) {  // the first launch runs the instances in index order
+    if (ok && p->n_inst > 0) {
+        // The first launch's order comes from an estimate of each instance's
+        // work, in place of the durations a launch records for the next one:
+        // the requests' minimum iterations in a batch, sum(D + ceil(P / c))
+        // over the trace, weighted 5/4 for policies that re-key every batch
+        // member at every token (the list is repaired after each iteration).
+        // Sorted longest first, and dealt round robin over the XCDs that take
+        // consecutive workgroups, it keeps any one setting of the sweep from
+        // landing on a single XCD (as index order does).
+        std::vector<int64_t> work((size_t)t->n_traces, 0), est((size_t)p->n_inst);
+        for (int32_t tr = 0; tr < t->n_traces; tr++)
+            for (int32_t j = 0; j < N; j++) {
+                const size_t x = (size_t)tr * (size_t)N + (size_t)j;
+                work[(size_t)tr] += t->decode[x] + (t->prompt[x] + p->chunk - 1) / p->chunk;
+            }
+        for (int32_t i = 0; i < p->n_inst; i++) {
+            const int32_t pol = p->inst[i].policy;
+            const bool rekey = pol == TAS_SRPT || pol == TAS_TRAIL || pol == TAS_LAS ||
+                               pol == TAS_SARATHI;
+            est[(size_t)i] = work[(size_t)p->inst[i].trace] * (rekey ? 5 : 4);
+        }
         std::vector<int32_t> iota((size_t)p->n_inst);
         for (int32_t i = 0; i < p->n_inst; i++) iota[(size_t)i] = i;
         ok = hipMemcpy(ws + L.order, iota.data(), iota.size() * 4, hipMemcpyHostToDevice) ==
                  hipSuccess &&
-             hipMemset(ws + L.dur, 0, (size_t)p->n_inst * 8) == hipSuccess;
+             hipMemcpy(ws + L.dur, est.data(), est.size() * 8, hipMemcpyHostToDevice) ==
+                 hipSuccess;
     }
     // the fixed-gamma kernel build leaves the adaptive outputs alone: zero them
     if (ok && p->n_inst > 0)
@@ -470,6 +491,7 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     const bool orderable = c->replicas == 1 && p->n_inst <= tas::kMaxOrdered;
     a.order = orderable ? (const int32_t *)(ws + L.order) : nullptr;
     a.dur = orderable ? (int64_t *)(ws + L.dur) : nullptr;
+    c->ordered = orderable;  // the first launch is ordered by the work estimate
     *out = c;
     return TAS_OK;
 }

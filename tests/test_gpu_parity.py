@@ -324,10 +324,21 @@ def test_parity_chunk_sizes(torch, chunk):
     assert_parity(w, gpu_run(w), o)
 
 
+def work_estimate(w):
+    """The first launch's ranking: per trace, the sum of D + ceil(P / chunk);
+    times 5 for policies that re-key every batch member at every token, else 4."""
+    c = w.engine.chunk
+    work = [int(sum(int(d) + -(-int(p) // c) for p, d in zip(w.prompt[t], w.decode[t])))
+            for t in range(w.n_traces)]
+    return [work[int(s["trace"])] * (5 if int(s["policy"]) in (W.SRPT, W.TRAIL, W.LAS,
+                                                                  W.SARATHI) else 4)
+            for s in w.settings]
+
+
 def test_launch_order_follows_previous_durations(torch):
-    """From the second run on, the workgroups take the instances longest first
-    by the previous run's durations (a permutation), and every run gives the
-    same results, equal to the oracle."""
+    """The first run takes the instances longest first by the work estimate,
+    later runs by the previous run's durations (each a permutation), and every
+    run gives the same results, equal to the oracle."""
     from paper_2606_18431_amd import tas
 
     w = W.make(2, n_traces=3, n_settings=8, n_req=2000)
@@ -336,7 +347,9 @@ def test_launch_order_follows_previous_durations(torch):
     n = w.n_inst
     dur = torch.zeros(n, dtype=torch.int64, device="cuda")
     order = torch.zeros(n, dtype=torch.int32, device="cuda")
-    prev = None
+    tas.tas_schedule(sim.ctx, dur, order)
+    prev = dur.cpu().numpy()
+    assert prev.tolist() == work_estimate(w)
     for k in range(3):
         print(f"[gpu] launch order, run {k}", flush=True)
         sim.step()
@@ -345,10 +358,8 @@ def test_launch_order_follows_previous_durations(torch):
         tas.tas_schedule(sim.ctx, dur, order)
         d, od = dur.cpu().numpy(), order.cpu().numpy()
         assert np.all(d > 0) and sorted(od.tolist()) == list(range(n))
-        if prev is None:
-            assert od.tolist() == list(range(n))
-        else:  # longest first, ties by index
-            assert od.tolist() == sorted(range(n), key=lambda i: (-int(prev[i]), i))
+        # longest first, ties by index
+        assert od.tolist() == sorted(range(n), key=lambda i: (-int(prev[i]), i))
         prev = d.copy()
     sim.close()
 
@@ -364,15 +375,14 @@ def test_launch_order_permutation_at_size(torch, n):
     sim = tas.Simulation(w)
     dur = torch.zeros(n, dtype=torch.int64, device="cuda")
     order = torch.zeros(n, dtype=torch.int32, device="cuda")
-    prev = None
+    prev = np.asarray(work_estimate(w), np.int64)
     for k in range(2):
         print(f"[gpu] launch order at {n} instances, run {k}", flush=True)
         sim.step()
         tas.tas_schedule(sim.ctx, dur, order)
         d, od = dur.cpu().numpy(), order.cpu().numpy()
         assert np.array_equal(np.sort(od), np.arange(n)) and np.all(d > 0)
-        if prev is not None:
-            assert np.array_equal(od, np.lexsort((np.arange(n), -prev)))
+        assert np.array_equal(od, np.lexsort((np.arange(n), -prev)))
         prev = d.copy()
     g = sim.results()
     sim.close()
