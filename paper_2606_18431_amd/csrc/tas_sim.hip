@@ -320,6 +320,7 @@ struct Sim {
     // and how many new KV blocks the members need for their next token.
     bool rep, all_emit;
     int du_next;
+    int nmoved;  // entries whose key the latest emission moved
     // entries extracted by compact_extract, lanes [0, min(count, kStage));
     // the rest go to the per-instance HBM overflow
     R stage;
@@ -401,6 +402,7 @@ struct Sim {
         emit_all = false;
         rep = all_emit = false;
         du_next = 0;
+        nmoved = 0;
         vm_res = vm_ev = 0;
         vm_ok = false;
         wsync();
@@ -1088,7 +1090,8 @@ struct Sim {
     // batch also G_RES), with `n1` added to their scheduled tokens (1 in a
     // repeated batch, whose entries carry no token count).
     DEV int emission(int64_t t_end, uint32_t mem, int n1) {
-        int lo = INT32_MAX, lohole = INT32_MAX, nd = 0, ufree = 0;
+        int lo = INT32_MAX, lohole = INT32_MAX, nd = 0, ufree = 0, nmv = 0;
+        nmoved = 0;
         bool bad_idx = false;
         uint64_t noemit = 0;  // batch members that emitted no token
         int dnext = 0;        // members whose next token opens a KV block
@@ -1225,7 +1228,10 @@ struct Sim {
             const uint64_t cm = ballot(chg), fm = ballot(fin);
             noemit |= ballot(mute);
             dnext += popc(ballot(opens));
-            if (cm && lo == INT32_MAX) lo = b + ffs0(cm);
+            if (cm) {
+                nmv += popc(cm);
+                if (lo == INT32_MAX) lo = b + ffs0(cm);
+            }
             if (fm) {
                 if (lohole == INT32_MAX) lohole = b + ffs0(fm);
                 nd += popc(fm);
@@ -1248,6 +1254,7 @@ struct Sim {
         wsync();
         if (ballot(bad_idx)) fail(S_ESTATE);
         all_emit = noemit == 0;
+        nmoved = nmv;
         du_next = dnext;
         if (nd) {
             U -= wsum(ufree);
@@ -1337,6 +1344,69 @@ struct Sim {
         return true;
     }
 
+    // The list is in key order except for the resident entry at rank r, whose
+    // key moved: put it at its rank among the others, shifting the entries
+    // in between by one slot (one pass over them, instead of extracting the
+    // tail of the list and merging it back). Holes keep their stale keys,
+    // which are in order, and move with the others.
+    DEV void move_one(int r) {
+        vm_ok = false;
+        R x;
+        ldr(r, x);  // every lane reads the entry (one address)
+        x.gs &= ~G_DIRTY;
+        const uint64_t key = x.pk;
+        // its new rank: the entries other than it with smaller keys. Entries
+        // before r had keys below its old key and after r above it, so only
+        // one side is counted, chunk by chunk, until a chunk lies beyond.
+        int to;
+        const bool right = r + 1 < L && uniu(S.k[r + 1]) < key;
+        if (right) {
+            to = r;
+            for (int b = ((r + 1) >> 6) << 6; b < L; b += kWave) {
+                const int i = b + lane();
+                const bool lt = i > r && i < L && S.k[i] < key;
+                const uint64_t m = ballot(lt);
+                to += popc(m);
+                if (popc(m) < min(L, b + kWave) - max(b, r + 1)) break;
+            }
+        } else {
+            to = r;
+            for (int b = ((r - 1) >> 6) << 6; b >= 0 && r > 0; b -= kWave) {
+                const int i = b + lane();
+                const bool gt = i < r && S.k[i] > key;
+                const uint64_t m = ballot(gt);
+                to -= popc(m);
+                if (popc(m) < min(r, b + kWave) - b) break;
+            }
+        }
+        wsync();
+        if (to > r) {  // entries r+1 .. to move down one slot, in ascending chunks
+            for (int b = ((r + 1) >> 6) << 6; b <= to; b += kWave) {
+                const int i = b + lane();
+                const bool mv = i > r && i <= to;
+                R y;
+                if (mv) ldr(i, y);
+                wsync();
+                if (mv) str(i - 1, y);
+                wsync();
+            }
+            if (lo_hole > r && lo_hole <= to) lo_hole--;
+        } else if (to < r) {  // entries to .. r-1 move up one slot, in descending chunks
+            for (int b = ((r - 1) >> 6) << 6; b >= 0 && b + kWave > to; b -= kWave) {
+                const int i = b + lane();
+                const bool mv = i >= to && i < r;
+                R y;
+                if (mv) ldr(i, y);
+                wsync();
+                if (mv) str(i + 1, y);
+                wsync();
+            }
+            if (lo_hole >= to && lo_hole < r) lo_hole++;
+        }
+        if (lane() == 0) str(to, x);
+        wsync();
+    }
+
     DEV void maintenance(int lo_mod) {
         if constexpr (EXT) {
             // Sarathi moves every decode that emitted to the same, latest key:
@@ -1345,6 +1415,11 @@ struct Sim {
             if (pol == P_SARATHI && lo_mod < L && n_holes < kHoleLimit && L <= cap_now() &&
                 settle_in_place(min(lo_mod, lo_hole)))
                 lo_mod = L;
+        }
+        if (nmoved == 1 && lo_mod < L && n_holes < kHoleLimit && L <= cap_now() &&
+            (ldx(lo_mod) & G_RES)) {
+            move_one(lo_mod);  // one resident re-keyed (a level crossing, say)
+            lo_mod = L;
         }
         if (UNLIKELY(lo_mod < L || n_holes >= kHoleLimit || L > cap_now())) {
             const int nx = compact_extract(min(min(lo_mod, lo_hole), L));
