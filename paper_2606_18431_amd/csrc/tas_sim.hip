@@ -321,6 +321,11 @@ struct Sim {
     bool rep, all_emit;
     int du_next;
     int nmoved;  // entries whose key the latest emission moved
+    // the key of the waiting candidate that closed admissions in the latest
+    // formation (~0: none), the smallest key of the arrivals taken since
+    // (~0: none) and a count of spill_excess calls
+    uint64_t close_pk, arr_min_pk;
+    int n_spilled;
     // entries extracted by compact_extract, lanes [0, min(count, kStage));
     // the rest go to the per-instance HBM overflow
     R stage;
@@ -403,6 +408,8 @@ struct Sim {
         rep = all_emit = false;
         du_next = 0;
         nmoved = 0;
+        close_pk = arr_min_pk = ~0ull;
+        n_spilled = 0;
         vm_res = vm_ev = 0;
         vm_ok = false;
         wsync();
@@ -555,6 +562,8 @@ struct Sim {
             if (LIKELY(n_arr == 0)) return;
             const R x = new_record(CL ? pidx : r, pa, pP, pD);
             const R y = off ? shfl_rec(x, min(off + lane(), kWave - 1)) : x;
+            if constexpr (!CL && !EXT)
+                arr_min_pk = min(arr_min_pk, wminu(lane() < n_arr ? y.pk : ~0ull));
             nW += n_arr;
             next += n_arr;
             add_entries(y, n_arr);
@@ -651,6 +660,7 @@ struct Sim {
         drop_holes();
         const int E = L - cap;
         if (E <= 0) return;
+        n_spilled++;
         if (EXT && pol == P_LTR) {
             // a spilled request's starvation count would have to advance in
             // HBM every iteration: an LTR+ instance keeps every request on
@@ -943,6 +953,7 @@ struct Sim {
                 return;
             }
             closed = true;
+            close_pk = uniu(S.k[q]);
             return;
         }
         fail(S_ESTATE);
@@ -971,6 +982,7 @@ struct Sim {
     }
 
     DEV void formation() {
+        close_pk = ~0ull;
         cnt = 0, used = 0;
         sum_ctx = 0;
         emit_chunks = 0;
@@ -1407,6 +1419,17 @@ struct Sim {
         wsync();
     }
 
+    // emit_chunks := the 64-entry chunks holding residents (in a repeated
+    // batch, every resident is a member)
+    DEV void resident_chunks() {
+        uint64_t m = 0;
+        for (int b = 0; b < L; b += kWave) {
+            const int r = b + lane();
+            if (ballot(r < L && (ldx(r) & G_RES))) m |= 1ull << (b >> 6);
+        }
+        emit_chunks = m;
+    }
+
     DEV void maintenance(int lo_mod) {
         if constexpr (EXT) {
             // Sarathi moves every decode that emitted to the same, latest key:
@@ -1656,9 +1679,19 @@ struct Sim {
             bool nrep = rep_form && all_emit && completed == c0 && lo_mod == INT32_MAX &&
                         L <= cap_now() && U + du_next <= Kb;
             if constexpr (EXT) nrep = nrep && ad == nullptr;
-            const int next0 = next;
+            // Arrivals (merged on chip or sent to the spill) that rank after
+            // the candidate that closed admissions are met after it closes
+            // them again, and skipped: the batch still repeats, as long as
+            // nothing was spilled to make room (the on-chip list keeps every
+            // waiting entry it had). The members' chunks are recounted, as
+            // the merged arrivals may shift them. (Fixed build only: its
+            // registers would cost the extended build occupancy.)
+            const int next0 = next, sp0 = n_spilled;
+            arr_min_pk = ~0ull;
             maintenance(lo_mod);
-            rep = nrep && next == next0;
+            rep = nrep && (next == next0 || (!EXT && arr_min_pk > close_pk && n_spilled == sp0 &&
+                                             close_pk != ~0ull));
+            if (!EXT && rep && next != next0) resident_chunks();
         }
         finish();
     }
