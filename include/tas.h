@@ -270,10 +270,13 @@ int tas_create_static(const tas_traces *traces, const tas_params *params, tas_ct
  * longest first: a launch lasts until its last instance ends. The first call
  * ranks them by an estimate of their work from the inputs (the sum over the
  * trace of D + ceil(P / chunk), times 5/4 for SRPT, TRAIL, LAS and Sarathi),
- * later calls by the durations the previous call recorded. Consecutive
- * workgroups go to different XCDs, so the sorted order also spreads each
- * kind of instance over them. The results do not depend on the order. Calls on one context share its workspace: a call on
- * another stream must be ordered after the previous one by the caller. */
+ * later calls by the tokens each instance computed in the previous call
+ * (counter 2 of tas_counters: a measure of its work that, unlike its
+ * wall-clock time, does not depend on where it ran). Consecutive workgroups
+ * go to different XCDs, so the sorted order also spreads each kind of
+ * instance over them. The results do not depend on the order. Calls on one
+ * context share its workspace: a call on another stream must be ordered
+ * after the previous one by the caller. */
 int tas_run(tas_ctx *ctx, void *stream);
 
 /* Enqueue the nearest-rank percentile reduction: d_out DEVICE uint32
@@ -328,14 +331,14 @@ int tas_replicas(tas_ctx *ctx, int32_t *d_assign, int64_t *d_counters, double *d
  * TAS_EOVERFLOW, TAS_ECAPACITY; TAS_EHIP if the stream reports a failure. */
 int tas_status(tas_ctx *ctx);
 
-/* The schedule of the latest tas_run: d_dur DEVICE int64 [n_inst], each
- * instance's wall-clock time on the GPU in 100 MHz ticks (before the first
- * run: the work estimates that order it), and d_order DEVICE int32 [n_inst],
- * the instance each workgroup took (a permutation; the index order before
- * the first run). Either pointer may be
- * NULL. TAS_EINVAL where no order is kept (replicas, or more than 16384
+/* The schedule of the latest tas_run: d_work DEVICE int64 [n_inst], the key
+ * the next tas_run orders the instances by, largest first (before the first
+ * run: the work estimates; after a run: each instance's computed tokens in
+ * it), and d_order DEVICE int32 [n_inst], the instance each workgroup took
+ * (a permutation; the index order before the first run). Either pointer may
+ * be NULL. TAS_EINVAL where no order is kept (replicas, or more than 16384
  * instances). */
-int tas_schedule(tas_ctx *ctx, int64_t *d_dur, int32_t *d_order, void *stream);
+int tas_schedule(tas_ctx *ctx, int64_t *d_work, int32_t *d_order, void *stream);
 
 /* Per-instance status codes, DEVICE int32 [n_inst] (enqueued copy). */
 int tas_instance_status(tas_ctx *ctx, int32_t *d_out, void *stream);

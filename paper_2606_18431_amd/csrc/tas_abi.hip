@@ -18,7 +18,7 @@
 struct tas_ctx {
     int32_t n_traces = 0, n_req = 0, n_inst = 0, list_cap = 0, spill_cap = 0, retry_cap = 0;
     int32_t replicas = 1;  // > 1: replicas behind a join-shortest-queue router
-    bool ordered = false;  // order the next launch by `dur` (estimates, then durations)
+    bool ordered = false;  // order the next launch by `work` (estimates, then computed tokens)
     int64_t lds_bytes = 0, lds_retry = 0;
     tas::SimArgs args{};
     std::vector<tas::DevSetting> settings;
@@ -39,7 +39,7 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 struct Layout {
     size_t arrival, prompt, decode, cached, settings, ada, tfirst, tlast, ttft, ttlt, tbtmax,
         counters, status, gamma, switches, spill, ovf, jidx, assign, rcounters, rgamma, rswitches,
-        dur, order, total;
+        work, order, total;
 };
 
 // Replicas per instance behind the join-shortest-queue router (1: none).
@@ -183,7 +183,7 @@ bool layout(const tas_traces *t, const tas_params *p, int32_t rc, int32_t sc, La
     L->rcounters = o, o = align256(o + (cl ? slots * 8 * 8 : 0));
     L->rgamma = o, o = align256(o + (cl ? slots * 8 : 0));
     L->rswitches = o, o = align256(o + (cl ? slots * 8 : 0));
-    L->dur = o, o = align256(o + (size_t)p->n_inst * 8);
+    L->work = o, o = align256(o + (size_t)p->n_inst * 8);
     L->order = o, o = align256(o + (size_t)p->n_inst * 4);
     L->total = o;
     return true;
@@ -420,13 +420,13 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
                        hipMemcpyHostToDevice) == hipSuccess;
     if (ok && p->n_inst > 0) {
         // The first launch's order comes from an estimate of each instance's
-        // work, in place of the durations a launch records for the next one:
-        // the requests' minimum iterations in a batch, sum(D + ceil(P / c))
-        // over the trace, weighted 5/4 for policies that re-key every batch
-        // member at every token (the list is repaired after each iteration).
-        // Sorted longest first, and dealt round robin over the XCDs that take
-        // consecutive workgroups, it keeps any one setting of the sweep from
-        // landing on a single XCD (as index order does).
+        // work, in place of the computed tokens a launch records for the next
+        // one: the requests' minimum iterations in a batch, sum(D + ceil(P /
+        // c)) over the trace, weighted 5/4 for policies that re-key every
+        // batch member at every token (the list is repaired after each
+        // iteration). Sorted longest first, and dealt round robin over the
+        // XCDs that take consecutive workgroups, it keeps any one setting of
+        // the sweep from landing on a single XCD (as index order does).
         std::vector<int64_t> work((size_t)t->n_traces, 0), est((size_t)p->n_inst);
         for (int32_t tr = 0; tr < t->n_traces; tr++)
             for (int32_t j = 0; j < N; j++) {
@@ -443,7 +443,7 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
         for (int32_t i = 0; i < p->n_inst; i++) iota[(size_t)i] = i;
         ok = hipMemcpy(ws + L.order, iota.data(), iota.size() * 4, hipMemcpyHostToDevice) ==
                  hipSuccess &&
-             hipMemcpy(ws + L.dur, est.data(), est.size() * 8, hipMemcpyHostToDevice) ==
+             hipMemcpy(ws + L.work, est.data(), est.size() * 8, hipMemcpyHostToDevice) ==
                  hipSuccess;
     }
     // the fixed-gamma kernel build leaves the adaptive outputs alone: zero them
@@ -490,7 +490,7 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
     a.rswitches = (int64_t *)(ws + L.rswitches);
     const bool orderable = c->replicas == 1 && p->n_inst <= tas::kMaxOrdered;
     a.order = orderable ? (const int32_t *)(ws + L.order) : nullptr;
-    a.dur = orderable ? (int64_t *)(ws + L.dur) : nullptr;
+    a.work = orderable ? (int64_t *)(ws + L.work) : nullptr;
     c->ordered = orderable;  // the first launch is ordered by the work estimate
     *out = c;
     return TAS_OK;
@@ -501,7 +501,7 @@ int tas_run(tas_ctx *c, void *stream) {
     if (!c) return TAS_EINVAL;
     c->last_stream = (hipStream_t)stream;
     if (c->ordered && c->args.order &&
-        tas_launch_order(c->args.dur, const_cast<int32_t *>(c->args.order), c->n_inst, stream))
+        tas_launch_order(c->args.work, const_cast<int32_t *>(c->args.order), c->n_inst, stream))
         return TAS_EHIP;
     if (launch(c->args, c->lds_bytes, stream)) return TAS_EHIP;
     c->ordered = c->args.order != nullptr;
@@ -594,13 +594,13 @@ int tas_replicas(tas_ctx *c, int32_t *d_assign, int64_t *d_counters, double *d_g
     return TAS_OK;
 }
 
-int tas_schedule(tas_ctx *c, int64_t *d_dur, int32_t *d_order, void *stream) {
+int tas_schedule(tas_ctx *c, int64_t *d_work, int32_t *d_order, void *stream) {
     if (!c || !c->args.order) return TAS_EINVAL;
     c->last_stream = (hipStream_t)stream;
     if (c->n_inst == 0) return TAS_OK;
     const hipStream_t s = (hipStream_t)stream;
     const size_t n = (size_t)c->n_inst;
-    if ((d_dur && hipMemcpyAsync(d_dur, c->args.dur, n * 8, hipMemcpyDeviceToDevice, s)) ||
+    if ((d_work && hipMemcpyAsync(d_work, c->args.work, n * 8, hipMemcpyDeviceToDevice, s)) ||
         (d_order && hipMemcpyAsync(d_order, c->args.order, n * 4, hipMemcpyDeviceToDevice, s)))
         return TAS_EHIP;
     return TAS_OK;

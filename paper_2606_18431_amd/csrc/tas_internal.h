@@ -94,9 +94,10 @@ struct SimArgs {
     double *rgamma;         // [n_inst][replicas] final adaptive gamma (0 without)
     int64_t *rswitches;     // [n_inst][replicas] grid-cell changes
     // launch order: workgroup b simulates instance order[b] (null: b), and
-    // each instance's wall-clock duration in 100 MHz ticks (null: not kept)
+    // each instance's computed tokens, the next launch's order key (null: not
+    // kept)
     const int32_t *order;
-    int64_t *dur;
+    int64_t *work;
 };
 
 constexpr int32_t kMaxOrdered = 16384;  // instances the order kernel sorts in LDS
@@ -138,6 +139,6 @@ constexpr int kMaxListCap = 64 * 64 - kStage;
 // Launchers implemented next to the kernels.
 int tas_launch_sim(const tas::SimArgs &a, int64_t lds_bytes, void *stream);
 int tas_launch_cluster(const tas::SimArgs &a, int64_t lds_bytes, void *stream);
-int tas_launch_order(const int64_t *dur, int32_t *order, int32_t n, void *stream);
+int tas_launch_order(const int64_t *work, int32_t *order, int32_t n, void *stream);
 int tas_launch_pctl(const uint32_t *ttft, const uint32_t *ttlt, const uint32_t *tbtmax,
                     int32_t n_inst, int32_t n_req, uint32_t *out, void *stream);

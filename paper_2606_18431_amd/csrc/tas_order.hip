@@ -3,10 +3,14 @@
 // Instances are independent and their results do not depend on when they
 // run, but a launch lasts until its slowest workgroup ends: started last, a
 // long instance leaves most of the chip idle at the end. The next launch
-// therefore starts the instances that took longest in the previous one first
-// (longest processing time first), from the wall-clock durations the
-// simulation kernel records. One workgroup sorts up to kMaxOrdered
-// (duration, index) pairs in LDS with a bitonic network.
+// therefore starts the instances with the most work first (longest
+// processing time first). The work key is the number of tokens an instance
+// computed in the previous launch (prefill, decode and recomputation after
+// preemption), which the simulation kernel records. Its wall-clock time is a
+// worse key: the waves that share a SIMD do not issue equally (older waves
+// win arbitration), so a duration says as much about the slot an instance
+// had as about its work. One workgroup sorts up to kMaxOrdered (work, index)
+// pairs in LDS with a bitonic network.
 #include <hip/hip_runtime.h>
 
 #include "tas_internal.h"
@@ -16,15 +20,15 @@ namespace {
 
 constexpr int kOrderThreads = 1024;
 
-__global__ __launch_bounds__(kOrderThreads) void order_kernel(const int64_t *dur, int32_t *order,
+__global__ __launch_bounds__(kOrderThreads) void order_kernel(const int64_t *work, int32_t *order,
                                                               int32_t n, int32_t n2) {
     extern __shared__ __align__(16) unsigned char smem[];
     uint64_t *key = (uint64_t *)smem;
-    // ascending keys: the longest duration first, ties by index
+    // ascending keys: the most work first, ties by index
     for (int i = (int)threadIdx.x; i < n2; i += kOrderThreads) {
         uint64_t k = ~0ull;
         if (i < n) {
-            const int64_t d = dur[i] < 0 ? 0 : (dur[i] > (int64_t(1) << 39) ? int64_t(1) << 39 : dur[i]);
+            const int64_t d = work[i] < 0 ? 0 : (work[i] > (int64_t(1) << 39) ? int64_t(1) << 39 : work[i]);
             k = ((uint64_t)((int64_t(1) << 39) - d) << 24) | (uint64_t)i;
         }
         key[i] = k;
@@ -50,7 +54,7 @@ __global__ __launch_bounds__(kOrderThreads) void order_kernel(const int64_t *dur
 }  // namespace
 }  // namespace tas
 
-int tas_launch_order(const int64_t *dur, int32_t *order, int32_t n, void *stream) {
+int tas_launch_order(const int64_t *work, int32_t *order, int32_t n, void *stream) {
     if (n <= 1 || n > tas::kMaxOrdered) return 0;
     int32_t n2 = 1;
     while (n2 < n) n2 <<= 1;
@@ -60,6 +64,6 @@ int tas_launch_order(const int64_t *dur, int32_t *order, int32_t n, void *stream
                                            (int)lds) != hipSuccess)
         return -4;
     hipLaunchKernelGGL(tas::order_kernel, dim3(1), dim3(tas::kOrderThreads), lds,
-                       (hipStream_t)stream, dur, order, n, n2);
+                       (hipStream_t)stream, work, order, n, n2);
     return hipGetLastError() == hipSuccess ? 0 : -4;
 }

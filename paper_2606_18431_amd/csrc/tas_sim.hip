@@ -1828,6 +1828,7 @@ struct Sim {
             int64_t *cn = A.counters + (size_t)inst * 8;
             cn[0] = iters, cn[1] = reqiters, cn[2] = tokens, cn[3] = ev_vol;
             cn[4] = ev_forced, cn[5] = t, cn[6] = maxU, cn[7] = idle;
+            if (A.work) A.work[inst] = tokens;  // the next launch's order key
             if constexpr (EXT) {  // (zero from tas_create for the other build)
                 A.gamma_out[inst] = ad ? S.as->gamma : 0.0;
                 A.switch_out[inst] = ad ? S.as->switches : 0;
@@ -1907,11 +1908,8 @@ __global__ __launch_bounds__(64) void sim_kernel(SimArgs a) {
     const int inst = a.order ? a.order[blockIdx.x] : (int)blockIdx.x;
     if (a.retry && a.status[inst] != S_ECAPACITY) return;
     const DevSetting &st = a.inst[inst];
-    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
     if (a.bs == 16) run_instance<4, EXT, CP>(a, st, inst, smem);
     else run_instance<-1, EXT, CP>(a, st, inst, smem);
-    if (a.dur && !a.retry && lane() == 0)  // for the next launch's order
-        a.dur[inst] = (int64_t)(__builtin_amdgcn_s_memrealtime() - t0);
 }
 
 // MAXW: the largest number of waves (replicas) the build serves; 8 leaves

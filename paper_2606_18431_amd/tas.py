@@ -232,8 +232,8 @@ def tas_replicas(ctx, assign=None, counters=None, gamma=None, switches=None, str
                               _stream(stream)), "tas_replicas")
 
 
-def tas_schedule(ctx, dur=None, order=None, stream=None):
-    _check(lib().tas_schedule(ctx, _ptr(dur), _ptr(order), _stream(stream)), "tas_schedule")
+def tas_schedule(ctx, work=None, order=None, stream=None):
+    _check(lib().tas_schedule(ctx, _ptr(work), _ptr(order), _stream(stream)), "tas_schedule")
 
 
 def tas_ada_grid(setting, tau_us: float = 5000.0):

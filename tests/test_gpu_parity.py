@@ -335,30 +335,31 @@ def work_estimate(w):
             for s in w.settings]
 
 
-def test_launch_order_follows_previous_durations(torch):
+def test_launch_order_follows_previous_work(torch):
     """The first run takes the instances longest first by the work estimate,
-    later runs by the previous run's durations (each a permutation), and every
-    run gives the same results, equal to the oracle."""
+    later runs by the tokens each instance computed in the previous run (each
+    order a permutation), and every run gives the same results, equal to the
+    oracle."""
     from paper_2606_18431_amd import tas
 
     w = W.make(2, n_traces=3, n_settings=8, n_req=2000)
     o = oracle.run(w)
     sim = tas.Simulation(w)
     n = w.n_inst
-    dur = torch.zeros(n, dtype=torch.int64, device="cuda")
+    work = torch.zeros(n, dtype=torch.int64, device="cuda")
     order = torch.zeros(n, dtype=torch.int32, device="cuda")
-    tas.tas_schedule(sim.ctx, dur, order)
-    prev = dur.cpu().numpy()
+    tas.tas_schedule(sim.ctx, work, order)
+    prev = work.cpu().numpy()
     assert prev.tolist() == work_estimate(w)
     for k in range(3):
         print(f"[gpu] launch order, run {k}", flush=True)
         sim.step()
         g = sim.results()
         assert_parity(w, g, o)
-        tas.tas_schedule(sim.ctx, dur, order)
-        d, od = dur.cpu().numpy(), order.cpu().numpy()
-        assert np.all(d > 0) and sorted(od.tolist()) == list(range(n))
-        # longest first, ties by index
+        tas.tas_schedule(sim.ctx, work, order)
+        d, od = work.cpu().numpy(), order.cpu().numpy()
+        assert np.array_equal(d, g["counters"][:, 2]) and sorted(od.tolist()) == list(range(n))
+        # most work first, ties by index
         assert od.tolist() == sorted(range(n), key=lambda i: (-int(prev[i]), i))
         prev = d.copy()
     sim.close()
@@ -367,26 +368,27 @@ def test_launch_order_follows_previous_durations(torch):
 @pytest.mark.parametrize("n", [1000, 16383, 16384])
 def test_launch_order_permutation_at_size(torch, n):
     """The order kernel at up to its largest size (one LDS sort of 16384):
-    every run's order is a permutation of the instances, longest previous
-    duration first; results of the ordered run equal the oracle on a sample."""
+    every run's order is a permutation of the instances, most work (computed
+    tokens) in the previous run first; results of the ordered run equal the
+    oracle on a sample."""
     from paper_2606_18431_amd import tas
 
     w = W.make(1, n_traces=256, n_settings=64, n_req=100).subset(np.arange(n))
     sim = tas.Simulation(w)
-    dur = torch.zeros(n, dtype=torch.int64, device="cuda")
+    work = torch.zeros(n, dtype=torch.int64, device="cuda")
     order = torch.zeros(n, dtype=torch.int32, device="cuda")
     prev = np.asarray(work_estimate(w), np.int64)
     for k in range(2):
         print(f"[gpu] launch order at {n} instances, run {k}", flush=True)
         sim.step()
-        tas.tas_schedule(sim.ctx, dur, order)
-        d, od = dur.cpu().numpy(), order.cpu().numpy()
+        tas.tas_schedule(sim.ctx, work, order)
+        d, od = work.cpu().numpy(), order.cpu().numpy()
         assert np.array_equal(np.sort(od), np.arange(n)) and np.all(d > 0)
         assert np.array_equal(od, np.lexsort((np.arange(n), -prev)))
         prev = d.copy()
     g = sim.results()
     sim.close()
-    assert g["rc"] == 0
+    assert g["rc"] == 0 and np.array_equal(prev, g["counters"][:, 2])
     sel = np.unique(np.concatenate([np.arange(8), np.arange(n - 8, n),
                                     np.random.default_rng(n).choice(n, 16, replace=False)]))
     o = oracle.run(w.subset(sel))
