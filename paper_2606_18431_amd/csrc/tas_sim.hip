@@ -177,12 +177,12 @@ DEV int idx_of(uint64_t pk) { return (int)(pk & kIdxMask); }
 
 // MemGuard level floor(log2(max(w,k)/k)) capped at 23, without a division:
 // with e = floor(log2 w) - floor(log2 k), the level is e when w >= k 2^e and
-// e - 1 otherwise (Eq. memguard_level).
+// e - 1 otherwise (Eq. memguard_level). Branch-free (lanes with w < k take 0
+// by a select), so a wave evaluates it without splitting.
 DEV int level_of(int w, int k, int lk) {
-    if (w < k) return 0;
-    const int e = (31 - __clz(w)) - lk;
-    const int L = ((w >> e) >= k) ? e : e - 1;
-    return L < kLevels - 1 ? L : kLevels - 1;
+    const int e = (31 - __clz(w | 1)) - lk;
+    const int L = ((w >> (e & 31)) >= k) ? e : e - 1;
+    return w < k ? 0 : (L < kLevels - 1 ? L : kLevels - 1);
 }
 
 // ------------------------------------------------------------ LDS layout
@@ -1015,12 +1015,10 @@ struct Sim {
             const int end = closed ? L : min(L, bstar);
             const int r = p + lane();
             const bool valid = r < end;
+            // (lanes past the slots read the last one; they are not valid)
             uint4 qr = nx;
-            if (!have_nx) {
-                qr = make_uint4(0u, 0u, 0u, 0u);
-                if (r < lim) qr = ldq(r);
-            }
-            if (r + kWave < lim) nx = ldq(r + kWave);
+            if (!have_nx) qr = ldq(min(r, lim - 1));
+            nx = ldq(min(r + kWave, lim - 1));
             const uint32_t g = valid ? qr.x : 0u;
             const int w = sw(qr);
             const int kvv = skv(qr);
@@ -1114,124 +1112,128 @@ struct Sim {
         uint64_t todo = all ? (nch >= 64 ? ~0ull : ((1ull << nch) - 1ull)) : emit_chunks;
         if (!todo) return INT32_MAX;
         // chunks are visited in ascending order, the next one's records loaded
-        // while this one is processed (a chunk's edits stay inside it)
+        // while this one is processed (a chunk's edits stay inside it). Lanes
+        // past the list end read its last slot and are masked out.
         int b = ffs0(todo) * kWave;
         todo &= todo - 1;
-        uint4 q = make_uint4(0u, 0u, 0u, 0u);
-        uint64_t pk = 0;
-        uint2 tg = make_uint2(0u, 0u);
-        if (b + lane() < L) q = ldq(b + lane()), pk = S.k[b + lane()], tg = S.tg[b + lane()];
+        uint4 q;
+        uint64_t pk;
+        uint2 tg;
+        {
+            const int i0 = min(b + lane(), L - 1);
+            q = ldq(i0), pk = S.k[i0], tg = S.tg[i0];
+        }
         for (;;) {
             const int bn = todo ? ffs0(todo) * kWave : -1;
             todo &= todo - 1;
             uint4 qn = make_uint4(0u, 0u, 0u, 0u);
             uint64_t pkn = 0;
             uint2 tgn = make_uint2(0u, 0u);
-            if (bn >= 0 && bn + lane() < L)
-                qn = ldq(bn + lane()), pkn = S.k[bn + lane()], tgn = S.tg[bn + lane()];
+            if (bn >= 0) {
+                const int i1 = min(bn + lane(), L - 1);
+                qn = ldq(i1), pkn = S.k[i1], tgn = S.tg[i1];
+            }
             const int r = b + lane();
-            const uint32_t g = q.x;
-            bool chg = false, fin = false, mute = false, opens = false;
-            if (g & mem) {
-                // kv includes this iteration's chunk (added at admission)
-                int w = sw(q), kv = skv(q) + n1, left = sleft(q);
-                uint32_t gs = g & ~G_INB;
-                uint32_t gm = tg.y;
-                const int idx = idx_of(pk);
-                if (idx >= N) bad_idx = true;
-                bool emit = false;
-                if (kv == w && idx < N) {
-                    emit = true;
-                    w++;
-                    left--;
-                    if (!(gs & G_FIRST)) {
-                        gs |= G_FIRST;
-                        tfirst[idx] = t_end;
-                        if constexpr (EXT) {
-                            if (pol == P_DIST && left > 0) {  // enters DistBoost's decode queue
-                                pk = pack(t_end - kDecodeQueueOff, idx);
-                                gs |= G_DIRTY;
-                                chg = true;
-                            }
-                        }
-                    } else {
-                        // times are kept modulo 2^32: a gap of 2^32 us or more
-                        // overflows the request's TTLT too
-                        const uint32_t gap = t32 - tg.x;
-                        gm = gap > gm ? gap : gm;
-                    }
-                    if (left == 0) {
-                        gs = (gs | G_DONE) & ~G_RES;
-                        ufree += blocks(kv);
-                        kv = 0;
-                        tlast[idx] = t_end;
-                        tbo[idx] = gm;
-                        fin = true;
-                    } else if (pol == P_LAS) {
-                        // the attained service grew by one token
-                        pk = pack((int64_t)w, idx);
-                        gs |= G_DIRTY;
-                        chg = true;
-                    } else if (EXT && pol == P_SARATHI) {
-                        // round robin: back of the decode queue after each token
-                        pk = pack(t_end - kDecodeQueueOff, idx);
-                        gs |= G_DIRTY;
-                        chg = true;
-                    } else if (pol == P_BOOST) {
-                        const int lo_ = (int)((gs >> G_LVL_SHIFT) & 31u);
-                        int sig = w;  // P + dec
-                        if constexpr (EXT) {
-                            if (phase_signal) sig = w - Pp[idx];  // dec >= 1 after this token
-                            if (cache_signal) sig = w - Hp[idx];  // P - h + dec
-                        }
-                        const int ln = level_of(sig, k, lk);
-                        if (ln != lo_) {
-                            pk = pack(key_of(pk) + S.bt[lo_] - S.bt[ln], idx);
-                            gs = (gs & ~G_LVL) | ((uint32_t)ln << G_LVL_SHIFT) | G_DIRTY;
-                            chg = true;
-                        }
-                    }
-                }
-                if ((pol == P_SRPT || pol == P_TRAIL) && !(gs & G_DONE)) {
-                    pk = pack((int64_t)w + left - 1 - kv, idx);
-                    chg = true;
-                }
+            const uint32_t g = r < L ? q.x : 0u;
+            // Per lane, as selects: the flag tests below are lane-dependent,
+            // and a branch on them would cost scalar exec-mask work in every
+            // chunk. Members (flags meet `mem`) advance; entries evicted in
+            // this iteration lose the eviction mark.
+            const bool memb = (g & mem) != 0;
+            const bool evi = !memb && (g & G_EVI) != 0;
+            int w = sw(q), left = sleft(q);
+            const int kv0 = skv(q);
+            int kv = kv0 + n1;  // includes this iteration's chunk (added at admission)
+            const int idx = idx_of(pk);
+            bad_idx = bad_idx || (memb && idx >= N);
+            const bool emit = memb && kv == w && idx < N;
+            const bool first = emit && !(g & G_FIRST);
+            // times are kept modulo 2^32: a gap of 2^32 us or more overflows
+            // the request's TTLT too
+            const uint32_t gap = t32 - tg.x;
+            const uint32_t gm = emit && !first && gap > tg.y ? gap : tg.y;
+            w += emit ? 1 : 0;
+            left -= emit ? 1 : 0;
+            const bool fin = emit && left == 0;
+            uint32_t gs = (memb ? g & ~G_INB : g & ~G_EVI) | (first ? G_FIRST : 0u);
+            gs = fin ? (gs | G_DONE) & ~G_RES : gs;
+            ufree += fin ? blocks(kv) : 0;
+            if (first) tfirst[idx] = t_end;
+            if (fin) {
+                tlast[idx] = t_end;
+                tbo[idx] = gm;
+            }
+            kv = fin ? 0 : (memb ? kv : kv0);
+            const bool live = emit && !fin;  // emitted and has tokens left
+            bool chg = false;
+            uint64_t pk2 = pk;
+            if (pol == P_LAS) {
+                // the attained service grew by one token
+                chg = live;
+                pk2 = chg ? pack((int64_t)w, idx) : pk;
+            } else if (pol == P_SRPT || pol == P_TRAIL) {
+                // remaining computed tokens (an evicted entry holds no KV)
+                chg = (memb && !fin) || evi;
+                pk2 = chg ? pack((int64_t)w + left - 1 - kv, idx) : pk;
+            } else if (pol == P_BOOST) {
+                const int lo_ = (int)((gs >> G_LVL_SHIFT) & 31u);
+                int sig = w;  // P + dec
                 if constexpr (EXT) {
-                    if (pol == P_LTR && !fin) {  // it ran: the count resets, or
-                        if (!(gs & G_PROMO)) {   // a promotion spends its quantum
-                            gs &= G_FLAGS;
-                        } else if ((gs >> kLtrShift) <= 1u) {
-                            gs = (gs & G_FLAGS & ~G_PROMO) | G_DIRTY;  // back to key D
-                            pk = pack((int64_t)(w - Pp[idx]) + left, idx);
-                            chg = true;
-                        } else {
-                            gs -= 1u << kLtrShift;
-                        }
-                    }
+                    // every lane reads: keep non-member lanes in bounds
+                    const int ix = min(idx, N - 1);
+                    if (phase_signal) sig = w - Pp[ix];  // dec >= 1 after this token
+                    if (cache_signal) sig = w - Hp[ix];  // P - h + dec
                 }
-                mute = !emit;
-                opens = emit && !fin && blocks(kv + 1) != blocks(kv);
-                stq(r, gs, w, kv, left);
-                if (chg) S.k[r] = pk;
-                if (emit) S.tg[r] = make_uint2(t32, gm);
-            } else if (g & G_EVI) {
-                if (pol == P_SRPT || pol == P_TRAIL) {
-                    S.k[r] = pack((int64_t)sw(q) + sleft(q) - 1, idx_of(pk));
+                const int ln = level_of(sig, k, lk);
+                chg = live && ln != lo_;
+                if (chg) {  // a level crossing (rare): re-key by the table step
+                    pk2 = pack(key_of(pk) + S.bt[lo_] - S.bt[ln], idx);
+                    gs = (gs & ~G_LVL) | ((uint32_t)ln << G_LVL_SHIFT);
+                }
+            }
+            if constexpr (EXT) {
+                if (pol == P_DIST && first && left > 0) {  // enters DistBoost's decode queue
+                    pk2 = pack(t_end - kDecodeQueueOff, idx);
+                    chg = true;
+                } else if (pol == P_SARATHI && live) {
+                    // round robin: back of the decode queue after each token
+                    pk2 = pack(t_end - kDecodeQueueOff, idx);
                     chg = true;
                 }
-                stx(r, g & ~G_EVI);
+                if (pol == P_LTR && memb && !fin) {  // it ran: the count resets, or
+                    if (!(gs & G_PROMO)) {           // a promotion spends its quantum
+                        gs &= G_FLAGS;
+                    } else if ((gs >> kLtrShift) <= 1u) {
+                        gs = (gs & G_FLAGS & ~G_PROMO) | G_DIRTY;  // back to key D
+                        pk2 = pack((int64_t)(w - Pp[idx]) + left, idx);
+                        chg = true;
+                    } else {
+                        gs -= 1u << kLtrShift;
+                    }
+                }
+            }
+            // SRPT's and TRAIL's re-keyed entries carry no re-insertion mark:
+            // compaction extracts those that fall out of order
+            const bool dirty = chg && pol != P_SRPT && pol != P_TRAIL;
+            gs |= dirty ? G_DIRTY : 0u;
+            const bool mute = memb && !emit;
+            const bool opens = live && blocks(kv + 1) != blocks(kv);
+            if (memb || evi) {
+                stq(r, gs, w, kv, left);
+                S.k[r] = pk2;
+                S.tg[r] = make_uint2(emit ? t32 : tg.x, gm);
             }
             if constexpr (EXT) {
                 // LTR+: a candidate that did not run starves one more
                 // iteration; at the threshold it is promoted for a quantum
-                if (pol == P_LTR && !(g & mem) && r < L && !(g & (G_DONE | G_PROMO))) {
+                if (pol == P_LTR && !memb && r < L && !(g & (G_DONE | G_PROMO))) {
                     const uint32_t cnt = (g >> kLtrShift) + 1u;
                     uint32_t gx = (g & G_FLAGS & ~G_EVI) | (cnt << kLtrShift);
                     if ((int)cnt >= ltr_s) {
                         gx = (g & G_FLAGS & ~G_EVI) | G_PROMO | G_DIRTY |
                              ((uint32_t)ltr_q << kLtrShift);
-                        pk = pack(iters + 1 - kPromotedOff, idx_of(pk));
-                        S.k[r] = pk;
+                        pk2 = pack(iters + 1 - kPromotedOff, idx);
+                        S.k[r] = pk2;
                         chg = true;
                     }
                     stx(r, gx);
