@@ -270,9 +270,11 @@ int tas_create_static(const tas_traces *traces, const tas_params *params, tas_ct
  * longest first: a launch lasts until its last instance ends. The first call
  * ranks them by an estimate of their work from the inputs (the sum over the
  * trace of D + ceil(P / chunk), times 5/4 for SRPT, TRAIL, LAS and Sarathi),
- * later calls by the tokens each instance computed in the previous call
- * (counter 2 of tas_counters: a measure of its work that, unlike its
- * wall-clock time, does not depend on where it ran). Consecutive workgroups
+ * later calls by the work each instance did in the previous call, counted in
+ * loop steps of its wavefront (4 per iteration, 5 per formation pass over up
+ * to 64 candidates, 3 per emission chunk: their measured relative cost), a
+ * measure that, unlike its wall-clock time, does not depend on where it ran.
+ * Consecutive workgroups
  * go to different XCDs, so the sorted order also spreads each kind of
  * instance over them. The results do not depend on the order. Calls on one
  * context share its workspace: a call on another stream must be ordered
@@ -333,8 +335,8 @@ int tas_status(tas_ctx *ctx);
 
 /* The schedule of the latest tas_run: d_work DEVICE int64 [n_inst], the key
  * the next tas_run orders the instances by, largest first (before the first
- * run: the work estimates; after a run: each instance's computed tokens in
- * it), and d_order DEVICE int32 [n_inst], the instance each workgroup took
+ * run: the work estimates; after a run: each instance's work in it in loop
+ * steps, as tas_run describes), and d_order DEVICE int32 [n_inst], the instance each workgroup took
  * (a permutation; the index order before the first run). Either pointer may
  * be NULL. TAS_EINVAL where no order is kept (replicas, or more than 16384
  * instances). */

@@ -18,7 +18,7 @@
 struct tas_ctx {
     int32_t n_traces = 0, n_req = 0, n_inst = 0, list_cap = 0, spill_cap = 0, retry_cap = 0;
     int32_t replicas = 1;  // > 1: replicas behind a join-shortest-queue router
-    bool ordered = false;  // order the next launch by `work` (estimates, then computed tokens)
+    bool ordered = false;  // order the next launch by `work` (estimates, then loop steps)
     int64_t lds_bytes = 0, lds_retry = 0;
     tas::SimArgs args{};
     std::vector<tas::DevSetting> settings;
@@ -420,7 +420,7 @@ int tas_create(const tas_traces *t, const tas_params *p, void *d_ws, size_t ws_b
                        hipMemcpyHostToDevice) == hipSuccess;
     if (ok && p->n_inst > 0) {
         // The first launch's order comes from an estimate of each instance's
-        // work, in place of the computed tokens a launch records for the next
+        // work, in place of the loop steps a launch records for the next
         // one: the requests' minimum iterations in a batch, sum(D + ceil(P /
         // c)) over the trace, weighted 5/4 for policies that re-key every
         // batch member at every token (the list is repaired after each

@@ -94,8 +94,8 @@ struct SimArgs {
     double *rgamma;         // [n_inst][replicas] final adaptive gamma (0 without)
     int64_t *rswitches;     // [n_inst][replicas] grid-cell changes
     // launch order: workgroup b simulates instance order[b] (null: b), and
-    // each instance's computed tokens, the next launch's order key (null: not
-    // kept)
+    // each instance's work in loop steps, the next launch's order key (null:
+    // not kept)
     const int32_t *order;
     int64_t *work;
 };

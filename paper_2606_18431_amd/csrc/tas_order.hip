@@ -4,13 +4,15 @@
 // run, but a launch lasts until its slowest workgroup ends: started last, a
 // long instance leaves most of the chip idle at the end. The next launch
 // therefore starts the instances with the most work first (longest
-// processing time first). The work key is the number of tokens an instance
-// computed in the previous launch (prefill, decode and recomputation after
-// preemption), which the simulation kernel records. Its wall-clock time is a
-// worse key: the waves that share a SIMD do not issue equally (older waves
-// win arbitration), so a duration says as much about the slot an instance
-// had as about its work. One workgroup sorts up to kMaxOrdered (work, index)
-// pairs in LDS with a bitonic network.
+// processing time first). The work key counts the loop steps an instance's
+// wave ran in the previous launch, weighted by their cost (iterations,
+// formation passes, emission chunks), which the simulation kernel records.
+// Its wall-clock time is a worse key: the waves that share a SIMD do not
+// issue equally (older waves win arbitration), so a duration says as much
+// about the slot an instance had as about its work. With as many instances
+// as resident slots the order only decides that arbitration, and the step
+// count still ranks the long instances first. One workgroup sorts up to
+// kMaxOrdered (work, index) pairs in LDS with a bitonic network.
 #include <hip/hip_runtime.h>
 
 #include "tas_internal.h"

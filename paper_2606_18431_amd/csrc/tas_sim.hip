@@ -303,6 +303,9 @@ struct Sim {
     int64_t pa;
     int pP, pD;
     int64_t iters, reqiters, tokens, ev_vol, ev_forced, maxU, idle;
+    // loop steps for the launch-order key: formation passes and emission
+    // chunks (32-bit: a wrap only perturbs the order of a huge instance)
+    uint32_t fpass, echunks;
     // CL: the replica (wave) index, the global indices dispatched to it in
     // order (HBM, written and read by this wave only, through L2), how many,
     // the prefetched global index of each lane, and the completions of the
@@ -326,9 +329,6 @@ struct Sim {
     // (~0: none) and a count of spill_excess calls
     uint64_t close_pk, arr_min_pk;
     int n_spilled;
-    // entries extracted by compact_extract, lanes [0, min(count, kStage));
-    // the rest go to the per-instance HBM overflow
-    R stage;
     // victim masks, lane c = chunk c: residents, and those a voluntary
     // eviction may take (MemGuard). Kept across iterations: bits change in
     // place on admission, eviction and completion; any edit that moves ranks
@@ -401,6 +401,7 @@ struct Sim {
         lo_hole = INT32_MAX;
         spill_min = ~0ull;
         iters = reqiters = tokens = ev_vol = ev_forced = maxU = idle = 0;
+        fpass = echunks = 0;
         cnt = used = 0;
         sum_ctx = 0;
         emit_chunks = 0;
@@ -999,6 +1000,7 @@ struct Sim {
         // every pass advances p or refills from the spill, so the walk ends
         // within L + spill_cap passes; a walk that does not is a broken state
         for (int pass = 0;; pass++) {
+            fpass++;
             if (UNLIKELY(pass > lcap + kStage + scap + 2)) {
                 fail(S_ESTATE);
                 return;
@@ -1111,6 +1113,7 @@ struct Sim {
         const bool all = emit_all || (EXT && pol == P_LTR);
         uint64_t todo = all ? (nch >= 64 ? ~0ull : ((1ull << nch) - 1ull)) : emit_chunks;
         if (!todo) return INT32_MAX;
+        echunks += popc(todo);
         // chunks are visited in ascending order, the next one's records loaded
         // while this one is processed (a chunk's edits stay inside it). Lanes
         // past the list end read its last slot and are masked out.
@@ -1282,9 +1285,9 @@ struct Sim {
 
     // From rank `from` on: remove holes; extract entries whose key moved
     // (flagged, or below the running maximum of the entries kept before them)
-    // into the staging slots and, beyond 64, the HBM overflow. Returns the
-    // number extracted. No holes lie below `from`.
-    DEV int compact_extract(int from) {
+    // into `stage` (lanes [0, min(count, 64))) and, beyond 64, the HBM
+    // overflow. Returns the number extracted. No holes lie below `from`.
+    DEV int compact_extract(int from, R &stage) {
         vm_ok = false;
         const int start = (from >> 6) << 6;
         uint64_t pmax = start > 0 ? uniu(S.k[start - 1]) : 0ull;
@@ -1447,7 +1450,8 @@ struct Sim {
             lo_mod = L;
         }
         if (UNLIKELY(lo_mod < L || n_holes >= kHoleLimit || L > cap_now())) {
-            const int nx = compact_extract(min(min(lo_mod, lo_hole), L));
+            R stage;
+            const int nx = compact_extract(min(min(lo_mod, lo_hole), L), stage);
             if (nx > kStage) hbm_fence();
             if (L > cap_now()) spill_excess();  // a refill during formation used the overflow region
             if (nx > 0 && status == 0) {
@@ -1586,7 +1590,8 @@ struct Sim {
         wsync();
         if (lane() < kLevels) S.bt[lane()] = v;
         wsync();
-        const int nx = compact_extract(0);  // every live entry is flagged
+        R stage;
+        const int nx = compact_extract(0, stage);  // every live entry is flagged
         if (nx > kStage) hbm_fence();
         if (nx > 0 && status == 0) {
             add_entries(stage, min(nx, kStage));
@@ -1830,7 +1835,12 @@ struct Sim {
             int64_t *cn = A.counters + (size_t)inst * 8;
             cn[0] = iters, cn[1] = reqiters, cn[2] = tokens, cn[3] = ev_vol;
             cn[4] = ev_forced, cn[5] = t, cn[6] = maxU, cn[7] = idle;
-            if (A.work) A.work[inst] = tokens;  // the next launch's order key
+            // the next launch's order key: the loop steps this wave ran,
+            // weighted by their measured cost (an iteration's fixed work 4,
+            // a formation pass over up to 64 candidates 5, an emission chunk
+            // 3). Unlike wall-clock time it does not depend on the slot the
+            // instance ran in.
+            if (A.work) A.work[inst] = 4 * iters + 5 * (int64_t)fpass + 3 * (int64_t)echunks;
             if constexpr (EXT) {  // (zero from tas_create for the other build)
                 A.gamma_out[inst] = ad ? S.as->gamma : 0.0;
                 A.switch_out[inst] = ad ? S.as->switches : 0;

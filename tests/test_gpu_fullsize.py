@@ -30,6 +30,8 @@ def torch():
 
 
 def sample_instances(w, n_random=4, seed=0):
+    if w.n_inst <= 64:  # the tiny workload: every instance
+        return np.arange(w.n_inst, dtype=np.int64)
     S = w.meta["n_settings"]
     T = w.n_traces
     pick = set()

@@ -337,9 +337,9 @@ def work_estimate(w):
 
 def test_launch_order_follows_previous_work(torch):
     """The first run takes the instances longest first by the work estimate,
-    later runs by the tokens each instance computed in the previous run (each
-    order a permutation), and every run gives the same results, equal to the
-    oracle."""
+    later runs by the loop steps each instance ran in the previous run (each
+    order a permutation; the steps are the same in every run), and every run
+    gives the same results, equal to the oracle."""
     from paper_2606_18431_amd import tas
 
     w = W.make(2, n_traces=3, n_settings=8, n_req=2000)
@@ -358,7 +358,10 @@ def test_launch_order_follows_previous_work(torch):
         assert_parity(w, g, o)
         tas.tas_schedule(sim.ctx, work, order)
         d, od = work.cpu().numpy(), order.cpu().numpy()
-        assert np.array_equal(d, g["counters"][:, 2]) and sorted(od.tolist()) == list(range(n))
+        # 4 steps per iteration at least
+        assert np.all(d >= 4 * g["counters"][:, 0]) and sorted(od.tolist()) == list(range(n))
+        if k > 0:
+            assert np.array_equal(d, prev)  # deterministic
         # most work first, ties by index
         assert od.tolist() == sorted(range(n), key=lambda i: (-int(prev[i]), i))
         prev = d.copy()
@@ -368,8 +371,8 @@ def test_launch_order_follows_previous_work(torch):
 @pytest.mark.parametrize("n", [1000, 16383, 16384])
 def test_launch_order_permutation_at_size(torch, n):
     """The order kernel at up to its largest size (one LDS sort of 16384):
-    every run's order is a permutation of the instances, most work (computed
-    tokens) in the previous run first; results of the ordered run equal the
+    every run's order is a permutation of the instances, most work (loop
+    steps) in the previous run first; results of the ordered run equal the
     oracle on a sample."""
     from paper_2606_18431_amd import tas
 
@@ -388,7 +391,7 @@ def test_launch_order_permutation_at_size(torch, n):
         prev = d.copy()
     g = sim.results()
     sim.close()
-    assert g["rc"] == 0 and np.array_equal(prev, g["counters"][:, 2])
+    assert g["rc"] == 0 and np.all(prev >= 4 * g["counters"][:, 0])
     sel = np.unique(np.concatenate([np.arange(8), np.arange(n - 8, n),
                                     np.random.default_rng(n).choice(n, 16, replace=False)]))
     o = oracle.run(w.subset(sel))
