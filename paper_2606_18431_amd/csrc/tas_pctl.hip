@@ -8,7 +8,7 @@
 // over the 32-bit values, 8 bits per pass, most significant digit first; the
 // three ranks share each pass over the data (one LDS histogram per rank; the
 // first pass, where no prefix is fixed yet, needs only one). Integer work
-// bound by HBM reads: 4 passes x 4 bytes per value.
+// bound by HBM reads: 4 passes x 4 bytes per value, read 16 bytes per lane.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -41,8 +41,7 @@ __global__ __launch_bounds__(kThreads) void pctl_kernel(const uint32_t *ttft, co
         for (int j = tid; j < 3 * 256; j += kThreads) (&hist[0][0])[j] = 0;
         __syncthreads();
         const uint32_t p0 = pre[0], p1 = pre[1], p2 = pre[2];
-        for (int i = tid; i < n; i += kThreads) {
-            const uint32_t x = v[i];
+        const auto count = [&](uint32_t x) {
             const uint32_t d = (x >> sh) & 255u;
             if (pass == 0) {
                 atomicAdd(&hist[0][d], 1u);
@@ -52,7 +51,19 @@ __global__ __launch_bounds__(kThreads) void pctl_kernel(const uint32_t *ttft, co
                 if (hx == (p1 >> (sh + 8))) atomicAdd(&hist[1][d], 1u);
                 if (hx == (p2 >> (sh + 8))) atomicAdd(&hist[2][d], 1u);
             }
+        };
+        // 16-byte loads over the aligned body of the row, single values
+        // before and after it
+        const int head = (int)(((16u - ((uint32_t)(uintptr_t)v & 15u)) & 15u) >> 2);
+        const int nh = head < n ? head : n;
+        const int nv = (n - nh) >> 2;
+        if (tid < nh) count(v[tid]);
+        const uint4 *v4 = (const uint4 *)(v + nh);
+        for (int i = tid; i < nv; i += kThreads) {
+            const uint4 x = v4[i];
+            count(x.x), count(x.y), count(x.z), count(x.w);
         }
+        for (int i = nh + 4 * nv + tid; i < n; i += kThreads) count(v[i]);
         __syncthreads();
         const int wv = tid >> 6, ln = tid & 63;
         if (wv < 3) {

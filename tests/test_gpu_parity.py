@@ -291,6 +291,18 @@ def test_error_spill_capacity(torch):
     assert g["rc"] == -8 and np.any(g["status"] == -8)
 
 
+@pytest.mark.parametrize("n_req", [1, 2, 3, 5, 1001, 1003])
+def test_percentiles_at_unaligned_row_sizes(torch, n_req):
+    """Request counts that are not multiples of 4 put the latency rows of
+    most instances off a 16-byte boundary: the percentile kernel reads a
+    head, an aligned body and a tail of every row; all nine percentiles and
+    every latency equal the oracle's."""
+    w = W.make(1, n_traces=2, n_settings=6, n_req=n_req)
+    o = oracle.run(w)
+    assert o["rc"] == 0
+    assert_parity(w, gpu_run(w), o)
+
+
 def test_deterministic_and_order_independent(torch):
     w = W.make(2, n_traces=2, n_settings=6, n_req=2500)
     g1 = gpu_run(w)
