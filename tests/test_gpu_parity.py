@@ -217,7 +217,8 @@ EXTENDED = [W.setting(0, W.SPF), W.setting(0, W.SJF), W.setting(0, W.LAS), W.set
             W.setting(0, W.BOOST, gamma=1e-3, signal=1, **W.UNIBOOST),
             W.setting(0, W.BOOST, gamma=1e-3, ada=dict(W.ADA, window=8, min_samples=4),
                       **W.UNIBOOST),
-            W.setting(0, W.SARATHI), W.setting(0, W.BOOST, gamma=1e-3, signal=2, **W.UNIBOOST)]
+            W.setting(0, W.SARATHI), W.setting(0, W.BOOST, gamma=1e-3, signal=2, **W.UNIBOOST),
+            W.setting(0, W.LTR, ltr=(3, 2))]
 
 
 @pytest.mark.parametrize("extended", [False, True], ids=["base", "extended"])
@@ -237,6 +238,26 @@ def test_edge_cases(torch, name, extended):
     if extended:
         assert np.array_equal(g["gamma"].view(np.int64), o["gamma"].view(np.int64))
         assert np.array_equal(g["switches"], o["switches"])
+
+
+def test_largest_request_count(torch):
+    """2^20 - 1 requests per trace, the most the boundary accepts (request
+    indices fill the packed key's 21-bit field with room to spare): groups
+    of eight short requests every 70 ms into a server of four sequences
+    (about 0.8 utilisation, 1.5 M iterations) under FCFS, UniBoost and SJF
+    (LTR+), every latency and percentile equal to the oracle."""
+    n = (1 << 20) - 1
+    rng = np.random.default_rng(20)
+    a = (np.arange(n) // 8).astype(np.int64) * 70_000
+    p = rng.integers(16, 257, n).astype(np.int32)
+    d = rng.integers(1, 9, n).astype(np.int32)
+    sets = [W.setting(0, W.FCFS), W.setting(0, W.BOOST, gamma=1e-3, **W.UNIBOOST),
+            W.setting(0, W.LTR, ltr=(8, 4))]
+    w = W.Workload("largest-n", a[None], p[None], d[None], W.Engine(max_seqs=4),
+                   np.stack(sets))
+    o = oracle.run(w)
+    assert o["rc"] == 0
+    assert_parity(w, gpu_run(w), o)
 
 
 @pytest.mark.parametrize("div", [1, 2, 3, 7, 64, 100, 997, (1 << 20) + 7, (1 << 31) - 1])
