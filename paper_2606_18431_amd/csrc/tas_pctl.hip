@@ -5,10 +5,11 @@
 // t_p = inf{t : Fbar(t) <= (100-p)/100} (arXiv 2606.18431, Phase 4).
 //
 // One 256-thread workgroup per (instance, metric) runs an exact radix select
-// over the 32-bit values, 8 bits per pass, most significant digit first; the
-// three ranks share each pass over the data (one LDS histogram per rank; the
-// first pass, where no prefix is fixed yet, needs only one). Integer work
-// bound by HBM reads: 4 passes x 4 bytes per value, read 16 bytes per lane.
+// over the 32-bit values, 11, 11 and 10 bits per pass, most significant digit
+// first; the three ranks share each pass over the data (one LDS histogram of
+// 2048 bins per rank; the first pass, where no prefix is fixed yet, needs
+// only one). Integer work bound by HBM reads: 3 passes x 4 bytes per value,
+// read 16 bytes per lane.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -18,11 +19,15 @@ namespace tas {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kPasses = 3;
+constexpr int kBins = 2048;                 // 11-bit digits (the last pass: 10 bits)
+constexpr int kShift[kPasses] = {21, 10, 0};
+constexpr int kBits[kPasses] = {11, 11, 10};
 
 __global__ __launch_bounds__(kThreads) void pctl_kernel(const uint32_t *ttft, const uint32_t *ttlt,
                                                         const uint32_t *tbt, int n_inst, int n,
                                                         uint32_t *out) {
-    __shared__ uint32_t hist[3][256];
+    __shared__ uint32_t hist[3][kBins];
     __shared__ uint32_t pre[3];
     __shared__ int rk[3];
     const int b = blockIdx.x;
@@ -36,20 +41,22 @@ __global__ __launch_bounds__(kThreads) void pctl_kernel(const uint32_t *ttft, co
         rk[tid] = (int)(((int64_t)q * n + 99) / 100);
         pre[tid] = 0;
     }
-    for (int pass = 0; pass < 4; pass++) {
-        const int sh = 24 - 8 * pass;
-        for (int j = tid; j < 3 * 256; j += kThreads) (&hist[0][0])[j] = 0;
+    for (int pass = 0; pass < kPasses; pass++) {
+        const int sh = kShift[pass];
+        const uint32_t dmask = (1u << kBits[pass]) - 1u;
+        const int hs = sh + kBits[pass];  // bits above this digit: the fixed prefix
+        for (int j = tid; j < 3 * kBins; j += kThreads) (&hist[0][0])[j] = 0;
         __syncthreads();
         const uint32_t p0 = pre[0], p1 = pre[1], p2 = pre[2];
         const auto count = [&](uint32_t x) {
-            const uint32_t d = (x >> sh) & 255u;
+            const uint32_t d = (x >> sh) & dmask;
             if (pass == 0) {
                 atomicAdd(&hist[0][d], 1u);
             } else {
-                const uint32_t hx = x >> (sh + 8);
-                if (hx == (p0 >> (sh + 8))) atomicAdd(&hist[0][d], 1u);
-                if (hx == (p1 >> (sh + 8))) atomicAdd(&hist[1][d], 1u);
-                if (hx == (p2 >> (sh + 8))) atomicAdd(&hist[2][d], 1u);
+                const uint32_t hx = x >> hs;
+                if (hx == (p0 >> hs)) atomicAdd(&hist[0][d], 1u);
+                if (hx == (p1 >> hs)) atomicAdd(&hist[1][d], 1u);
+                if (hx == (p2 >> hs)) atomicAdd(&hist[2][d], 1u);
             }
         };
         // 16-byte loads over the aligned body of the row, single values
@@ -65,12 +72,14 @@ __global__ __launch_bounds__(kThreads) void pctl_kernel(const uint32_t *ttft, co
         }
         for (int i = nh + 4 * nv + tid; i < n; i += kThreads) count(v[i]);
         __syncthreads();
+        // wave r < 3 finds rank r: each lane sums 32 consecutive bins, a wave
+        // scan finds the lane whose bins hold the rank, that lane walks them
         const int wv = tid >> 6, ln = tid & 63;
         if (wv < 3) {
             const uint32_t *h = pass == 0 ? hist[0] : hist[wv];
-            const int h0 = (int)h[4 * ln], h1 = (int)h[4 * ln + 1], h2 = (int)h[4 * ln + 2],
-                      h3 = (int)h[4 * ln + 3];
-            const int s = h0 + h1 + h2 + h3;
+            constexpr int kPer = kBins / 64;
+            int s = 0;
+            for (int j = 0; j < kPer; j++) s += (int)h[kPer * ln + j];
             int inc = s;
 #pragma unroll
             for (int o = 1; o < 64; o <<= 1) {
@@ -82,17 +91,13 @@ __global__ __launch_bounds__(kThreads) void pctl_kernel(const uint32_t *ttft, co
             const uint64_t m = __ballot(exc < r && r <= inc);
             if (m) {
                 const int src = __ffsll((unsigned long long)m) - 1;
-                int rr = r - __shfl(exc, src);
-                const int b0 = __shfl(h0, src), b1 = __shfl(h1, src), b2 = __shfl(h2, src);
-                int bin = 4 * src;
-                if (rr > b0) {
-                    rr -= b0, bin++;
-                    if (rr > b1) {
-                        rr -= b1, bin++;
-                        if (rr > b2) rr -= b2, bin++;
+                if (ln == src) {
+                    int rr = r - exc, bin = kPer * ln;
+                    for (int j = 0; j < kPer - 1; j++, bin++) {
+                        const int c = (int)h[bin];
+                        if (rr <= c) break;
+                        rr -= c;
                     }
-                }
-                if (ln == 0) {
                     pre[wv] |= (uint32_t)bin << sh;
                     rk[wv] = rr;
                 }
