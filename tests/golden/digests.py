@@ -3,7 +3,8 @@
 A digest is the first 8 bytes of BLAKE2b over one instance's outputs in a
 fixed byte order: TTFT, TTLT and maximum gap per request (uint32, little
 endian), the eight counters (int64), the nine percentiles (uint32) and the
-status (int32). Equal digests mean equal outputs, element for element (up to
+status (int32). An instance that failed (a nonzero status, such as a latency
+past the 32-bit range) contributes its status alone. Equal digests mean equal outputs, element for element (up to
 a 2^-64 collision chance). The stored digests are written by
 ``make_fullsize_digests.py`` from the CPU oracle alone; the GPU tests compute
 the same digests from the HIP path's outputs and compare.
@@ -28,8 +29,12 @@ def instance_digests(ttft, ttlt, tbtmax, counters, pct, status) -> list[str]:
     out = []
     for i in range(len(ttft)):
         h = hashlib.blake2b(digest_size=DIGEST_BYTES)
-        for a in (ttft[i], ttlt[i], tbtmax[i], counters[i], pct[i], status[i:i + 1]):
-            h.update(a.tobytes())
+        if status[i] != 0:  # a failed instance: its status is its only defined output
+            h.update(b"failed")
+            h.update(status[i:i + 1].tobytes())
+        else:
+            for a in (ttft[i], ttlt[i], tbtmax[i], counters[i], pct[i], status[i:i + 1]):
+                h.update(a.tobytes())
         out.append(h.hexdigest())
     return out
 

@@ -1,8 +1,10 @@
 """Every instance at full size: the chat-heavy (4096 x 10,000), reasoning-heavy
-(4096 x 10,000) and bursty (4096 x 20,000) sweeps, and the large sweep's
-checked subset (every 64th instance and all settings of four traces, 508 of
-16,384 x 50,000), each simulated in one tas_run in the launch configuration
-the benchmark times, against the CPU oracle.
+(4096 x 10,000) and bursty (4096 x 20,000) sweeps, the large sweep's checked
+subset (every 64th instance and all settings of four traces, 508 of 16,384 x
+50,000), and every instance of the large-sweep traces under the comparator
+grid (2,560, SJF (LTR+) among them) and the adaptive-gamma grid (2,048), each
+simulated in one tas_run in the launch configuration the benchmark times,
+against the CPU oracle.
 
 The oracle's outputs are stored as per-instance digests
 (tests/golden/fullsize_digests.json, written by make_fullsize_digests.py from
@@ -22,6 +24,7 @@ from paper_2606_18431_amd import workloads as W
 HERE = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, os.path.join(HERE, "golden"))
 from digests import input_digest, instance_digests, large_sweep_subset  # noqa: E402
+from make_fullsize_digests import KEYS, make  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 GOLD = json.load(open(os.path.join(HERE, "golden", "fullsize_digests.json")))["workloads"]
@@ -50,22 +53,26 @@ def explain(w, i, got):
     return "no difference on rerun"
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
-def test_every_instance_matches_oracle_digest(torch, cfg):
+@pytest.mark.parametrize("key", KEYS)
+def test_every_instance_matches_oracle_digest(torch, key):
     from paper_2606_18431_amd import tas
 
-    ref = GOLD[str(cfg)]
-    w = W.make(cfg)
+    if key not in GOLD:
+        pytest.skip(f"no stored digests for {key} (make_fullsize_digests.py --only {key})")
+    ref = GOLD[key]
+    w = make(key)
     assert input_digest(w) == ref["inputs"], "the input generator drifted"
     sel = np.asarray(ref["instances"], np.int64) if "instances" in ref else np.arange(w.n_inst)
-    if cfg == 4:
+    if key == "4":
         assert np.array_equal(sel, large_sweep_subset(w))
-    print(f"[gpu] full-size digests {W.NAMES[cfg]}: {w.n_inst} instances x {w.n_req}, "
+    print(f"[gpu] full-size digests {ref['name']}: {w.n_inst} instances x {w.n_req}, "
           f"checking {len(sel)}", flush=True)
     sim = tas.Simulation(w)
     sim.step()
     g = sim.results(latencies=False)
-    assert g["rc"] == 0, tas.tas_strerror(g["rc"])
+    # (LAS overflows the 32-bit latency range on the comparator grid: those
+    # instances are compared by their status)
+    assert g["rc"] == ref.get("rc", 0), tas.tas_strerror(g["rc"])
     dev = sim.pct.device
     lat = [torch.empty((w.n_inst, w.n_req), dtype=torch.int32, device=dev) for _ in range(3)]
     tas.tas_latencies(sim.ctx, *lat)
@@ -88,4 +95,5 @@ def test_every_instance_matches_oracle_digest(torch, cfg):
         detail = explain(w, int(sel[j]), {k: v[j] for k, v in got.items()})
         raise AssertionError(f"{len(bad)} of {n} instances differ from the oracle; first: "
                              f"instance {int(sel[j])}: {detail}")
-    assert int(got["counters"][:, 1].sum()) == ref["reqiters"]
+    if ref.get("failed", 0) == 0:  # (failed instances' counters are not compared)
+        assert int(got["counters"][:, 1].sum()) == ref["reqiters"]
