@@ -2,13 +2,15 @@
 for every instance of the chat-heavy, reasoning-heavy and bursty sweeps, for
 the large sweep's checked subset (every 64th instance and all settings of
 four traces), and for every instance of the large-sweep traces under the
-comparator grid (SJF (LTR+) among them) and the adaptive-gamma grid. Calls
-only the oracle and the seeded input generator.
+comparator grid (SJF (LTR+) among them), the adaptive-gamma, phase-ladder and
+cache-aware grids, and for every instance of the starvation mix. Calls only
+the oracle and the seeded input generator.
 
     python tests/golden/make_fullsize_digests.py [--threads N] [--only KEY ...]
 
-Keys: 1, 2, 3, 4, 4-comparators, 4-ada (--only recomputes those and keeps
-the rest of an existing file). About an hour on 8 host threads in all.
+Keys: 1, 2, 3, 4, 4-comparators, 4-ada, 4-ladder, 4-cache, 5 (--only
+recomputes those and keeps the rest of an existing file). About two hours on
+8 host threads in all.
 """
 from __future__ import annotations
 
@@ -28,7 +30,7 @@ from paper_2606_18431_amd import workloads as W  # noqa: E402
 from digests import input_digest, instance_digests, large_sweep_subset  # noqa: E402
 
 OUT = os.path.join(HERE, "fullsize_digests.json")
-KEYS = ("1", "2", "3", "4", "4-comparators", "4-ada")
+KEYS = ("1", "2", "3", "4", "4-comparators", "4-ada", "4-ladder", "4-cache", "5")
 
 
 def make(key: str):

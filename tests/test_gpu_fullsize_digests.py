@@ -1,10 +1,11 @@
 """Every instance at full size: the chat-heavy (4096 x 10,000), reasoning-heavy
 (4096 x 10,000) and bursty (4096 x 20,000) sweeps, the large sweep's checked
 subset (every 64th instance and all settings of four traces, 508 of 16,384 x
-50,000), and every instance of the large-sweep traces under the comparator
-grid (2,560, SJF (LTR+) among them) and the adaptive-gamma grid (2,048), each
-simulated in one tas_run in the launch configuration the benchmark times,
-against the CPU oracle.
+50,000), every instance of the large-sweep traces under the comparator grid
+(2,560, SJF (LTR+) among them), the adaptive-gamma, phase-ladder and
+cache-aware grids (2,048 each), and every instance of the starvation mix
+(256 x 20,000), each simulated in one tas_run in the launch configuration
+the benchmark times, against the CPU oracle.
 
 The oracle's outputs are stored as per-instance digests
 (tests/golden/fullsize_digests.json, written by make_fullsize_digests.py from
