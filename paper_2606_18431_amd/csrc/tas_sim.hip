@@ -39,6 +39,15 @@ namespace tas {
 namespace {
 
 #define DEV __device__ __forceinline__
+
+// The checking build (a library of its own, compiled with
+// TAS_CHECK_INVARIANTS=1) verifies the state of every instance after each
+// iteration and fails the instance with S_ESTATE at the first violation;
+// its results are otherwise those of the ordinary build.
+#ifndef TAS_CHECK_INVARIANTS
+#define TAS_CHECK_INVARIANTS 0
+#endif
+constexpr bool kCheck = TAS_CHECK_INVARIANTS != 0;
 #define UNLIKELY(x) __builtin_expect(!!(x), 0)
 #define LIKELY(x) __builtin_expect(!!(x), 1)
 
@@ -1604,6 +1613,78 @@ struct Sim {
         }
     }
 
+    // ---------------------------------------------------------- checks
+
+    // The batch just formed respects the sequence cap, the token budget and
+    // the KV budget, and every member computes at least one token.
+    DEV void check_batch() {
+        if (cnt < 1 || cnt > M || used < cnt || used > T || U < 0 || U > Kb) fail(S_ESTATE);
+    }
+
+    // The state between iterations: the list's residents, waiting entries
+    // and holes match their counts; the KV in use is the residents' blocks,
+    // within the budget; the keys of the entries other than holes ascend
+    // strictly; holes lie at or after lo_hole; no mark of an iteration (in
+    // the batch, evicted, selected for spilling, key moved) survives it; an
+    // entry's KV lies within its signal and a waiting entry holds none; the
+    // spill holds waiting entries only, its minimum is exact; and every
+    // request taken so far is done, on chip or spilled.
+    DEV void check_state() {
+        bool bad = U < 0 || U > Kb || L < 0 || L > cap_now() || spill_n < 0 || spill_n > scap;
+        int nres = 0, nwait = 0, nhole = 0, blk = 0;
+        uint64_t pmax = 0;  // 1 + the largest key of the live entries so far (0: none)
+        for (int b = 0; b < L && !bad; b += kWave) {
+            const int r = b + lane();
+            const bool v = r < L;
+            const int i = min(r, L - 1);  // lanes past the list read its last slot
+            const uint4 q = ldq(i);
+            const uint32_t g = q.x;
+            const uint64_t pk = S.k[i];
+            const bool done = v && (g & G_DONE) != 0;
+            const bool live = v && !done;
+            const bool rs = live && (g & G_RES) != 0;
+            const bool wt = live && (g & G_RES) == 0;
+            const int w = sw(q), kv = skv(q), left = sleft(q);
+            nres += rs ? 1 : 0;
+            nwait += wt ? 1 : 0;
+            nhole += done ? 1 : 0;
+            blk += rs ? blocks(kv) : 0;
+            const uint64_t inc = scan_maxu(live ? pk + 1 : 0ull);
+            uint64_t exc = prev_lane_u64(inc, 0ull);
+            if (pmax > exc) exc = pmax;
+            bool e = v && (g & (G_INB | G_EVI | G_MARK)) != 0;
+            e = e || (live && (g & G_DIRTY) != 0);
+            e = e || (live && pk + 1 <= exc);  // not above a live key before it
+            e = e || (done && r < lo_hole);
+            e = e || (live && (kv < 0 || kv > w || left < 1 || idx_of(pk) >= N));
+            e = e || (wt && kv != 0);
+            bad = bad || ballot(e) != 0;
+            const uint64_t cm = rlu(inc, 63);
+            if (cm > pmax) pmax = cm;
+        }
+        if (!bad) {
+            nres = wsum(nres), nwait = wsum(nwait), nhole = wsum(nhole), blk = wsum(blk);
+            bad = nres != nR || nwait != nW || nhole != n_holes || blk != U ||
+                  completed + nR + nW + spill_n != next;
+        }
+        if (!bad && spill_n > 0) {
+            hbm_fence();
+            uint64_t mn = ~0ull;
+            bool e = false;
+            for (int b = 0; b < spill_n; b += kWave) {
+                const int i = b + lane();
+                if (i < spill_n) {
+                    const Rec x = spill[i];
+                    if (x.pk < mn) mn = x.pk;
+                    e = e || (x.gs & (G_RES | G_DONE | G_INB | G_EVI | G_MARK | G_DIRTY)) != 0 ||
+                        x.kv != 0 || x.left < 1 || idx_of(x.pk) >= N;
+                }
+            }
+            bad = ballot(e) != 0 || wminu(mn) != spill_min;
+        }
+        if (bad) fail(S_ESTATE);
+    }
+
     // ---------------------------------------------------------- driver
 
     DEV void run() {
@@ -1657,6 +1738,10 @@ struct Sim {
                     break;
                 }
             }
+            if constexpr (kCheck) {
+                check_batch();
+                if (status) break;
+            }
             // formation evicted nothing, refilled nothing, stopped short of
             // the token budget and took every resident
             const bool rep_form = ev_vol + ev_forced == ev0 && !emit_all && used < T && cnt == nR;
@@ -1699,6 +1784,9 @@ struct Sim {
             rep = nrep && (next == next0 || (!EXT && arr_min_pk > close_pk && n_spilled == sp0 &&
                                              close_pk != ~0ull));
             if (!EXT && rep && next != next0) resident_chunks();
+            if constexpr (kCheck) {
+                if (status == 0) check_state();
+            }
         }
         finish();
     }
@@ -1747,6 +1835,10 @@ struct Sim {
                 fail(S_ESTATE);
                 return;
             }
+            if constexpr (kCheck) {
+                check_batch();
+                if (status) return;
+            }
             if (U > maxU) maxU = U;
             const int64_t dt = (int64_t)base + (int64_t)tok * used + (int64_t)ctx_quot((uint64_t)sum_ctx);
             const int64_t t_end = t + dt;
@@ -1762,6 +1854,9 @@ struct Sim {
                 return;
             }
             maintenance(lo_mod);
+            if constexpr (kCheck) {
+                if (status == 0) check_state();
+            }
         }
     }
 

@@ -19,6 +19,9 @@ from . import workloads as W
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libtas.so")
+# the checking build: the same entry points, and every instance's state is
+# verified after each iteration (a violation fails it with TAS_ESTATE)
+CHECK_LIB_PATH = os.path.join(PKG, "libtas_check.so")
 LEVELS = 24
 
 TAS_OK, TAS_EINVAL, TAS_EINFEASIBLE, TAS_ENOMEM, TAS_EHIP = 0, -1, -2, -3, -4
@@ -113,6 +116,16 @@ def lib():
         L.tas_list_cap.restype = i32
         _lib = L
     return _lib
+
+
+def select_library(path: str) -> str:
+    """Make the library at `path` the one that later calls load (LIB_PATH, or
+    CHECK_LIB_PATH); returns the previous path. A context belongs to the
+    library that created it: finish with it before switching back."""
+    global LIB_PATH, _lib
+    prev = LIB_PATH
+    LIB_PATH, _lib = path, None
+    return prev
 
 
 def _ptr(x):

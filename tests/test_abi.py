@@ -32,6 +32,15 @@ def test_library_exports_every_declared_symbol():
     assert set(tas.EXPORTS) <= set(names)
 
 
+def test_checking_build_exports_the_same_symbols():
+    """libtas_check.so (every instance's state verified after each
+    iteration) is a drop-in replacement: the same entry points."""
+    assert os.path.exists(tas.CHECK_LIB_PATH), "libtas_check.so is missing: run the build"
+    lib = ctypes.CDLL(tas.CHECK_LIB_PATH)
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+
+
 def test_struct_layouts_match_header(tmp_path):
     """The ctypes mirrors have the C compiler's size and field offsets."""
     structs = [tas.tas_setting, tas.tas_params, tas.tas_traces]
