@@ -103,7 +103,7 @@ struct SimArgs {
 constexpr int32_t kMaxOrdered = 16384;  // instances the order kernel sorts in LDS
 
 constexpr int kMaxReplicas = 16;
-constexpr int64_t kJsqLdsBytes = kMaxReplicas * 4 * 2 + kMaxReplicas * 8 * 8;
+constexpr int64_t kJsqLdsBytes = kMaxReplicas * 4 * 3 + kMaxReplicas * 8 * 8;
 
 // Bytes of the adaptive-gamma block: its state (gamma, gamma_hat, counters),
 // then the window in completion order and sorted, 4 bytes per latency each.

@@ -1797,8 +1797,7 @@ struct Sim {
     // With limit = INT64_MAX it runs to the end of what was dispatched.
     DEV void run_until(int64_t limit) {
         if (status) return;
-        load_pf();  // the router may have dispatched since the last call
-        take_arrivals();
+        take_arrivals();  // the router may have dispatched since the last call
         for (;;) {
             if (status) return;
             if (UNLIKELY(nW + nR == 0)) {
@@ -1871,6 +1870,9 @@ struct Sim {
             __hip_atomic_store(&jl[Nk], j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             A.assign[(size_t)inst * (size_t)N + (size_t)j] = wv;
         }
+        // the prefetch window [pf, pf + 64) takes the new entry now, as a
+        // reload from the list would (pf <= next <= Nk)
+        if (lane() == Nk - pf) pidx = j, pa = arr[j], pP = Pp[j], pD = Dp[j];
         Nk++;
         hbm_fence();
     }
@@ -1956,10 +1958,10 @@ DEV void run_instance(const SimArgs &a, const DevSetting &st, int inst, unsigned
 // request of the global trace, in order, each replica first simulates the
 // iterations that start before its arrival; then the request goes to the
 // replica holding the fewest requests at that instant (ties to the lowest
-// replica). Every wave passes the same two barriers per request, whatever
+// replica). Every wave passes the same barrier once per request, whatever
 // its own state, so the workgroup cannot split at a barrier.
 struct JsqLds {
-    int32_t held[kMaxReplicas];
+    int32_t held[2][kMaxReplicas];  // by the parity of the global request index
     int32_t status[kMaxReplicas];
     int64_t cn[kMaxReplicas][8];
 };
@@ -1971,19 +1973,24 @@ DEV void run_cluster(const SimArgs &a, const DevSetting &st, int inst, unsigned 
     const int R = a.replicas, w = (int)(threadIdx.x >> 6), N = a.n_req;
     Sim<BSH, true, true> s(a, st, inst, smem + kJsqLdsBytes + (size_t)w * (size_t)a.wave_lds, w);
     const int64_t *arr = a.arrival + (size_t)st.trace * (size_t)N;
+    s.load_pf();  // nothing dispatched yet: an empty window, kept current by dispatch
     for (int j = 0;; j++) {  // j = N: run what was dispatched to the end
         const int64_t aj = j < N ? arr[j] : INT64_MAX;
         s.run_until(aj);
         if (j == N) break;
-        if (lane() == 0) J->held[w] = s.held_at(aj);
+        // One barrier per request: the counts alternate between two
+        // buffers. A wave that runs ahead writes the other one, and it
+        // comes back to this one only after passing the next request's
+        // barrier, which every wave reaches after reading this one.
+        int32_t *held = J->held[j & 1];
+        if (lane() == 0) held[w] = s.held_at(aj);
         __syncthreads();
-        int best = 0, bn = J->held[0];
+        int best = 0, bn = held[0];
         for (int r = 1; r < R; r++) {
-            const int h = J->held[r];
+            const int h = held[r];
             if (h < bn) best = r, bn = h;
         }
         if (best == w) s.dispatch(j);
-        __syncthreads();
     }
     s.finish_cl(J->cn[w], &J->status[w]);
     __syncthreads();
