@@ -11,7 +11,9 @@ with TAS_ESTATE. Each workload below must finish with no violation and with
 the ordinary build's outputs, byte for byte. The workloads cover the spill
 and refill paths (the smallest lists), the retry pass, evictions under KV
 pressure, every comparator, adaptive gamma, the phase ladder, the
-cache-aware signal and the JSQ router.
+cache-aware signal and the JSQ router; and, at full size, every instance of
+the chat-heavy, reasoning-heavy and bursty sweeps and of the starvation mix,
+checked against the oracle's stored digests.
 """
 import os
 
@@ -123,3 +125,40 @@ def test_checking_build_finds_no_violation(torch, name):
     assert np.array_equal(checked["gamma"].view(np.int64), plain["gamma"].view(np.int64))
     if "assign" in plain:
         assert np.array_equal(checked["assign"], plain["assign"])
+
+
+@pytest.mark.parametrize("key", ["1", "2", "3", "5"])
+def test_checking_build_at_full_size(torch, key):
+    """Every instance of the chat-heavy, reasoning-heavy and bursty sweeps and
+    of the starvation mix, at full size, under the checking build: no
+    violation, and per-instance digests equal to the oracle's."""
+    import json
+    import sys
+
+    from paper_2606_18431_amd import tas
+
+    here = os.path.dirname(os.path.abspath(__file__))
+    sys.path.insert(0, os.path.join(here, "golden"))
+    from digests import input_digest, instance_digests
+    from make_fullsize_digests import make
+
+    ref = json.load(open(os.path.join(here, "golden", "fullsize_digests.json")))["workloads"][key]
+    w = make(key)
+    assert input_digest(w) == ref["inputs"], "the input generator drifted"
+    print(f"[gpu] checked full size {ref['name']}: {w.n_inst} x {w.n_req}", flush=True)
+    prev = tas.select_library(tas.CHECK_LIB_PATH)
+    try:
+        sim = tas.Simulation(w)
+        sim.step()
+        g = sim.results()
+        sim.close()
+    finally:
+        tas.select_library(prev)
+    torch.cuda.empty_cache()
+    assert not np.any(g["status"] == tas.TAS_ESTATE), np.nonzero(g["status"] == tas.TAS_ESTATE)
+    assert g["rc"] == ref.get("rc", 0), tas.tas_strerror(g["rc"])
+    dig = instance_digests(g["ttft"], g["ttlt"], g["tbtmax"], g["counters"], g["pct"], g["status"])
+    want = ref["digests"]
+    assert len(want) // 16 == w.n_inst
+    bad = [j for j in range(w.n_inst) if dig[j] != want[16 * j:16 * (j + 1)]]
+    assert not bad, f"{len(bad)} instances differ from the oracle, first {bad[0]}"
