@@ -11,9 +11,9 @@ with TAS_ESTATE. Each workload below must finish with no violation and with
 the ordinary build's outputs, byte for byte. The workloads cover the spill
 and refill paths (the smallest lists), the retry pass, evictions under KV
 pressure, every comparator, adaptive gamma, the phase ladder, the
-cache-aware signal and the JSQ router; and, at full size, every instance of
-the chat-heavy, reasoning-heavy and bursty sweeps and of the starvation mix,
-checked against the oracle's stored digests.
+cache-aware signal and the JSQ router; and every full-size workload with
+stored oracle digests (configs 1-3, the large sweep and its other settings
+grids, the starvation mix), checked against those digests.
 """
 import os
 
@@ -127,11 +127,15 @@ def test_checking_build_finds_no_violation(torch, name):
         assert np.array_equal(checked["assign"], plain["assign"])
 
 
-@pytest.mark.parametrize("key", ["1", "2", "3", "5"])
+FULL_SIZE = ["1", "2", "3", "4", "4-comparators", "4-ada", "4-ladder", "4-cache", "5"]
+
+
+@pytest.mark.parametrize("key", FULL_SIZE)
 def test_checking_build_at_full_size(torch, key):
-    """Every instance of the chat-heavy, reasoning-heavy and bursty sweeps and
-    of the starvation mix, at full size, under the checking build: no
-    violation, and per-instance digests equal to the oracle's."""
+    """Every full-size workload with stored oracle digests, under the checking
+    build: no violation in any instance, and the checked instances' digests
+    equal the oracle's (the large sweep: its 508-instance subset; instances
+    that fail with a latency overflow are compared by their status)."""
     import json
     import sys
 
@@ -142,23 +146,35 @@ def test_checking_build_at_full_size(torch, key):
     from digests import input_digest, instance_digests
     from make_fullsize_digests import make
 
-    ref = json.load(open(os.path.join(here, "golden", "fullsize_digests.json")))["workloads"][key]
+    gold = json.load(open(os.path.join(here, "golden", "fullsize_digests.json")))["workloads"]
+    if key not in gold:
+        pytest.skip(f"no stored digests for {key}")
+    ref = gold[key]
     w = make(key)
     assert input_digest(w) == ref["inputs"], "the input generator drifted"
+    sel = np.asarray(ref["instances"], np.int64) if "instances" in ref else np.arange(w.n_inst)
     print(f"[gpu] checked full size {ref['name']}: {w.n_inst} x {w.n_req}", flush=True)
     prev = tas.select_library(tas.CHECK_LIB_PATH)
     try:
         sim = tas.Simulation(w)
         sim.step()
-        g = sim.results()
+        g = sim.results(latencies=False)
+        dev = sim.pct.device
+        lat = [torch.empty((w.n_inst, w.n_req), dtype=torch.int32, device=dev) for _ in range(3)]
+        tas.tas_latencies(sim.ctx, *lat)
+        ix = torch.as_tensor(sel, device=dev)
+        got = {k: t.index_select(0, ix).cpu().numpy().view(np.uint32)
+               for k, t in zip(("ttft", "ttlt", "tbtmax"), lat)}
+        del lat
         sim.close()
     finally:
         tas.select_library(prev)
     torch.cuda.empty_cache()
     assert not np.any(g["status"] == tas.TAS_ESTATE), np.nonzero(g["status"] == tas.TAS_ESTATE)
     assert g["rc"] == ref.get("rc", 0), tas.tas_strerror(g["rc"])
-    dig = instance_digests(g["ttft"], g["ttlt"], g["tbtmax"], g["counters"], g["pct"], g["status"])
+    dig = instance_digests(got["ttft"], got["ttlt"], got["tbtmax"], g["counters"][sel],
+                           g["pct"][sel], g["status"][sel])
     want = ref["digests"]
-    assert len(want) // 16 == w.n_inst
-    bad = [j for j in range(w.n_inst) if dig[j] != want[16 * j:16 * (j + 1)]]
-    assert not bad, f"{len(bad)} instances differ from the oracle, first {bad[0]}"
+    assert len(want) // 16 == len(sel)
+    bad = [j for j in range(len(sel)) if dig[j] != want[16 * j:16 * (j + 1)]]
+    assert not bad, f"{len(bad)} instances differ from the oracle, first {int(sel[bad[0]])}"
