@@ -132,6 +132,9 @@ def main():
                     help="oracle threads (default: every CPU this process may use, up to 16)")
     ap.add_argument("--list-cap", type=int, default=0,
                     help="on-chip candidate list per instance (0: the library default)")
+    ap.add_argument("--check", action="store_true",
+                    help="run the checking build (libtas_check.so): every instance's state is "
+                         "verified after each iteration")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (the reference for "
                          "scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -179,6 +182,9 @@ def main():
     if args.chunk:
         w.engine = dataclasses.replace(w.engine, chunk=args.chunk)
         name += f", chunk {args.chunk}"
+    if args.check:
+        tas.select_library(tas.CHECK_LIB_PATH)
+        name += ", checking build"
     print(f"[bench] building {name}", file=sys.stderr, flush=True)
     sim = tas.Simulation(w, device=dev, list_cap=args.list_cap)
     stream = torch.cuda.current_stream()
